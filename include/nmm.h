@@ -1,0 +1,217 @@
+/*
+ * nmm.h -- narrow MatMul on AMD MI355X (gfx950): the C ABI.
+ *
+ * The library computes narrow matrix multiplications y = x . W in which x has only a few rows
+ * (1..16 on the streaming path, more on the matrix-core path), at the shapes of DeepSeek-V3
+ * Multi-head Latent Attention single-token decode.  The operation is the paper's problem
+ * statement C = A x B with A in R^{M x K}, B in R^{K x N}, narrow when min(M, N) = 1
+ * (Section II-D "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"), widened to
+ * small M as in the future-work Conditions 4-5 (Section V), and its specialisation C = T x W for
+ * the MLA down-projection (Section IV-C, eq. 4).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - x and W hold 16-bit floats (fp16 or bf16, one type per call), row-major:
+ *        x[m * ldx + k]  (m < M, k < K),     W[k * ldw + n]  (k < K, n < N).
+ *    y is fp32, row-major, y[m * ldy + n], and is OVERWRITTEN (never accumulated into).
+ *    Products are formed exactly in fp32 (16-bit inputs widen exactly) and summed in fp32.
+ *  - All pointers except `stream` are device pointers on the current HIP device.  `stream` is a
+ *    hipStream_t passed as void*; NULL means the null stream.  Calls are asynchronous: they
+ *    enqueue kernels and return; results are valid once the stream's work completes.
+ *  - The caller owns every buffer.  The library never allocates or frees memory in a compute
+ *    call.  Buffers must stay alive until the enqueued work completes.
+ *  - Alignment: x and W must be 16-byte aligned, and ldx and ldw must be multiples of 8
+ *    elements (16 bytes).  A ragged N therefore needs a padded ldw >= roundup(N, 8); the kernels
+ *    read the padding columns of each row (up to roundup(N, 8)) but never use them.  W's extent
+ *    is (K-1)*ldw + roundup(N, 8) elements per matrix and x's is (M-1)*ldx + roundup(K, 8): reads
+ *    are whole 16-byte chunks.  y needs 4-byte alignment only.
+ *  - Workspace: split-K partial sums and arrival counters.  Query its size with the matching
+ *    *_workspace_size() call; pass at least that many bytes, 256-byte aligned.  A workspace must
+ *    be ZEROED once when it is allocated (nmm_workspace_init does that on a stream).  Its first
+ *    64 KiB hold the arrival counters of every call and the partial sums always follow them;
+ *    every call leaves the counters at zero again when it completes, so one workspace serves
+ *    any sequence of calls of any shapes.  It serves one call at a time: calls that may overlap
+ *    (different streams) need different workspaces.
+ *  - Results are deterministic: the same inputs give bit-identical outputs on every run.
+ *  - Errors: every call validates all arguments before enqueueing anything.  On an error it
+ *    returns a non-zero nmm_status, enqueues nothing and leaves the outputs untouched.  No
+ *    exception crosses the ABI and nothing aborts.  NMM_ERR_HIP reports a failed launch; a
+ *    device-side fault surfaces at the caller's next synchronisation.
+ *  - Empty problems: M == 0 or N == 0 is a no-op returning NMM_OK; K == 0 writes zeros (the
+ *    empty sum).
+ *  - Limits: every size and leading dimension must be < 2^31, and each W matrix's extent must
+ *    be < 2^31 bytes (buffer-resource offsets are 32-bit); otherwise NMM_ERR_SHAPE.
+ */
+#ifndef NMM_H
+#define NMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    NMM_OK = 0,
+    NMM_ERR_NULL = 1,       /* a required pointer is NULL */
+    NMM_ERR_SHAPE = 2,      /* negative size, ld smaller than the row, or a size over the limits */
+    NMM_ERR_DTYPE = 3,      /* unknown nmm_dtype */
+    NMM_ERR_ALIGN = 4,      /* a pointer or leading dimension breaks the alignment rules */
+    NMM_ERR_WORKSPACE = 5,  /* workspace NULL, misaligned or smaller than the size query */
+    NMM_ERR_HIP = 6,        /* the HIP runtime reported an error (no device, launch failure) */
+    NMM_ERR_PATH = 7,       /* unknown nmm_path, or a path that cannot run these sizes */
+    NMM_ERR_ARG = 8         /* any other invalid argument (e.g. non-finite attention scale) */
+} nmm_status;
+
+typedef enum { NMM_F16 = 1, NMM_BF16 = 2 } nmm_dtype;
+
+/* Which kernel family computes the product.  AUTO picks the streaming GEMV for M up to the
+ * measured crossover and the MFMA (matrix-core) path above it; GEMV and MFMA force a family. */
+typedef enum { NMM_PATH_AUTO = 0, NMM_PATH_GEMV = 1, NMM_PATH_MFMA = 2 } nmm_path;
+
+/*
+ * nmm_gemv -- y[M,N] = x[M,K] . W[K,N].
+ *
+ * The paper's narrow MatMul (Section II-D; Condition 2) and its three-stage vector algorithm
+ * (Algorithm 1, Section III-B: per-executor block loads, multiply + reduce to partial sums in a
+ * temporary buffer, wait for all executors, gather).  Here the executors are workgroups: each
+ * streams one K-slice of one column panel of W from HBM exactly once, keeps fp32 partial sums
+ * per column, and the last workgroup to finish a panel gathers the K-slices in a fixed order
+ * and writes y.
+ *
+ *   M, K, N     sizes (>= 0).  The GEMV path takes any M (in blocks of 16 rows).
+ *   dt          NMM_F16 or NMM_BF16, the type of both x and W.
+ *   x, ldx      device pointer and leading dimension (elements, >= K, multiple of 8).
+ *   W, ldw      device pointer and leading dimension (elements, >= N, multiple of 8).
+ *   y, ldy      fp32 output and its leading dimension (elements, >= N).
+ *   path        kernel family (see nmm_path).
+ *   workspace   device scratch of >= nmm_gemv_workspace_size(...) bytes (may be NULL when that
+ *               size is 0), zeroed once at allocation.
+ *   stream      hipStream_t or NULL.
+ */
+nmm_status nmm_gemv(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                    const void* x, int64_t ldx, const void* W, int64_t ldw,
+                    float* y, int64_t ldy, nmm_path path,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * nmm_batched_gemv -- for b < batch: y_b = x_b . W_b with
+ *   x_b = x + b*stride_x,  W_b = W + b*stride_w,  y_b = y + b*stride_y   (strides in elements).
+ * The per-head absorbed MLA matmuls (q_nope . W_UK and latent . W_UV, one W per head).  Same
+ * rules as nmm_gemv; stride_x and stride_w must be multiples of 8.  Strides may be smaller
+ * than a matrix (e.g. a strided slice of a wider tensor); the caller guarantees y_b regions do
+ * not overlap.
+ */
+nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                            const void* x, int64_t ldx, int64_t stride_x,
+                            const void* W, int64_t ldw, int64_t stride_w,
+                            float* y, int64_t ldy, int64_t stride_y, nmm_path path,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * One DeepSeek-V3 MLA single-token decode chain of narrow MatMuls, all bf16 row-major [K,N]:
+ *
+ *   down   = x . w_down              x [1,hidden], w_down [hidden, q_lora+kv_lora+rope]
+ *   c_q    = bf16(down[:q_lora])
+ *   q      = c_q . w_uq              w_uq [q_lora, heads*(nope+rope)]
+ *   q_nope = bf16(q[h, :nope])       per head h (the first nope of each head's nope+rope)
+ *   lat[h] = q_nope[h] . w_uk[h]     w_uk [heads, nope, kv_lora]
+ *   lat'   = bf16(lat)
+ *   o[h]   = lat'[h] . w_uv[h]       w_uv [heads, kv_lora, v_head]
+ *   o'     = bf16(o)                 flattened to [1, heads*v_head]
+ *   y      = o' . w_o                w_o [heads*v_head, hidden]
+ *
+ * The first step is the paper's MatMul 2 (eq. 3-4, Section IV-C/D), widened from the kv_lora |
+ * rope columns to q_lora | kv_lora | rope.  Rounding to bf16 (ties to even) between steps
+ * follows Algorithm 2's output cast (Section IV-E/F); it is fused into the producing kernel's
+ * gather, which writes both the fp32 result and the bf16 operand of the next step.
+ *
+ * Every buffer is caller-owned device memory.  The fp32 and bf16 intermediates are outputs so
+ * that each step can be checked on its own.  `events`, if not NULL, points to n_events >= 6
+ * hipEvent_t handles; event i is recorded on `stream` before step i (i < 5) and event 5 after
+ * the last step -- optional instrumentation for per-step timing.
+ */
+typedef struct {
+    int64_t hidden, q_lora, kv_lora, rope, heads, nope, v_head;   /* 7168,1536,512,64,128,128,128 */
+    const void *x, *w_down, *w_uq, *w_uk, *w_uv, *w_o;           /* bf16 inputs (see above)     */
+    float *down_f32;   /* [q_lora+kv_lora+rope] */
+    float *q_f32;      /* [heads*(nope+rope)]   */
+    float *lat_f32;    /* [heads*kv_lora]       */
+    float *o_f32;      /* [heads*v_head]        */
+    float *y;          /* [hidden]  final output */
+    void *cq_bf16;     /* [q_lora]             bf16 */
+    void *qnope_bf16;  /* [heads*nope]         bf16 */
+    void *lat_bf16;    /* [heads*kv_lora]      bf16 */
+    void *o_bf16;      /* [heads*v_head]       bf16 */
+    void *const *events;
+    int n_events;
+} nmm_mla_chain;
+
+nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/*
+ * nmm_latent_attention -- single-token latent attention, the decode step's independent dense
+ * work (the paper overlaps the vector unit's narrow MatMul with matrix-unit work that does not
+ * depend on it: Condition 1 "Data Independence", Section III-A; Section IV-B).  For each head h:
+ *     s_j      = scale * sum_{d < d_qk} q[h*ldq + d] * kv[j*ld_kv + d]        (j < seq)
+ *     p_j      = softmax_j(s)
+ *     out[h,n] = sum_j p_j * kv[j*ld_kv + n]                                  (n < d_v)
+ * i.e. V is the first d_v columns of the latent cache.  q and kv are bf16; out is fp32 with
+ * leading dimension ldo.  Scores and softmax are fp32; p is rounded to bf16 for the matrix-core
+ * product with V, accumulated in fp32.  Constraints: heads >= 0, seq >= 1, d_qk and d_v
+ * multiples of 32 with d_v <= d_qk <= ld_kv, ldq >= d_qk, ldq and ld_kv multiples of 8,
+ * q and kv 16-byte aligned, finite scale.
+ */
+nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
+                                const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
+                                float scale, float* out, int64_t ldo,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace sizes in bytes (0 when none is needed; never fails: invalid sizes give 0). */
+size_t nmm_gemv_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt, nmm_path path);
+size_t nmm_batched_gemv_workspace_size(int64_t batch, int64_t M, int64_t K, int64_t N,
+                                       nmm_dtype dt, nmm_path path);
+size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain);
+size_t nmm_latent_attention_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v);
+
+/* Zero a workspace on `stream` with a fill kernel (no memset node, so it is safe to capture). */
+nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The host-side partition the library would launch for these sizes (a pure function: no GPU
+ * access).  Algorithm 2's init stage (Section IV-F) sizes its executor pool from the core
+ * count; here the plan sizes a grid of workgroups for 256 compute units.
+ */
+typedef struct {
+    int32_t path;            /* NMM_PATH_GEMV or NMM_PATH_MFMA */
+    int32_t m_tile;          /* rows of x per launch (GEMV: 1,2,4,8,16; MFMA: 16 or 32) */
+    int32_t m_blocks;        /* launches' worth of row blocks (ceil(M / m_tile)) */
+    int32_t panel_width;     /* 8-column chunks per full panel (64, 32, 16 or 8) */
+    int32_t n_full_panels;   /* full panels */
+    int32_t tail_chunks;     /* 8-column chunks in the ragged last panel (0: none) */
+    int32_t tail_width;      /* lanes per row for the last panel (a power of two >= tail_chunks) */
+    int32_t split_k_full;    /* K-slices per full panel */
+    int32_t rows_full;       /* rows of W per K-slice of a full panel */
+    int32_t split_k_tail;    /* K-slices of the last panel */
+    int32_t rows_tail;       /* rows per K-slice of the last panel */
+    int32_t items;           /* workgroups per matrix (per batch entry, per row block) */
+    int32_t threads;         /* threads per workgroup */
+    int64_t grid;            /* total workgroups of one launch */
+    int64_t workspace_bytes;
+} nmm_plan_info;
+
+nmm_status nmm_gemv_plan(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                         nmm_path path, nmm_plan_info* info);
+
+/* Human-readable name of a status code (static storage). */
+const char* nmm_status_string(nmm_status s);
+
+/* Library version, e.g. "0.1.0" (static storage). */
+const char* nmm_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NMM_H */

@@ -1,0 +1,253 @@
+"""Narrow MatMul on AMD MI355X (gfx950): the Python binding of libnmm.so.
+
+Argument marshalling only.  Every step of the computation runs in the HIP kernels of libnmm.so
+behind the C ABI declared in include/nmm.h; torch supplies device memory, streams and events.
+The functions carry the C names (nmm_gemv, nmm_batched_gemv, nmm_mla_decode_chain,
+nmm_latent_attention, ...) and take torch tensors, from which they read pointers, sizes and
+strides.  There is no fallback: if libnmm.so is missing, importing the binding's functions
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libnmm.so")
+
+NMM_OK, NMM_ERR_NULL, NMM_ERR_SHAPE, NMM_ERR_DTYPE, NMM_ERR_ALIGN, NMM_ERR_WORKSPACE, \
+    NMM_ERR_HIP, NMM_ERR_PATH, NMM_ERR_ARG = range(9)
+NMM_F16, NMM_BF16 = 1, 2
+NMM_PATH_AUTO, NMM_PATH_GEMV, NMM_PATH_MFMA = 0, 1, 2
+
+_i64 = ctypes.c_int64
+_p = ctypes.c_void_p
+_sz = ctypes.c_size_t
+_lib = None
+
+
+class NmmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {nmm_status_string(status)}")
+
+
+class nmm_plan_info(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_int32), ("m_tile", ctypes.c_int32), ("m_blocks", ctypes.c_int32),
+                ("panel_width", ctypes.c_int32), ("n_full_panels", ctypes.c_int32),
+                ("tail_chunks", ctypes.c_int32),
+                ("tail_width", ctypes.c_int32), ("split_k_full", ctypes.c_int32),
+                ("rows_full", ctypes.c_int32), ("split_k_tail", ctypes.c_int32),
+                ("rows_tail", ctypes.c_int32), ("items", ctypes.c_int32),
+                ("threads", ctypes.c_int32), ("grid", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_int64)]
+
+    def as_dict(self) -> dict:
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+class nmm_mla_chain(ctypes.Structure):
+    _fields_ = [(n, _i64) for n in ("hidden", "q_lora", "kv_lora", "rope", "heads", "nope", "v_head")] + \
+               [(n, _p) for n in ("x", "w_down", "w_uq", "w_uk", "w_uv", "w_o", "down_f32", "q_f32",
+                                  "lat_f32", "o_f32", "y", "cq_bf16", "qnope_bf16", "lat_bf16",
+                                  "o_bf16", "events")] + [("n_events", ctypes.c_int)]
+
+
+EXPORTS = {
+    "nmm_gemv": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
+                                ctypes.c_int, _p, _sz, _p]),
+    "nmm_batched_gemv": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_int, _p, _i64, _i64, _p,
+                                        _i64, _i64, _p, _i64, _i64, ctypes.c_int, _p, _sz, _p]),
+    "nmm_mla_decode_chain": (ctypes.c_int, [ctypes.POINTER(nmm_mla_chain), _p, _sz, _p]),
+    "nmm_latent_attention": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64,
+                                            ctypes.c_float, _p, _i64, _p, _sz, _p]),
+    "nmm_gemv_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int]),
+    "nmm_batched_gemv_workspace_size": (_sz, [_i64, _i64, _i64, _i64, ctypes.c_int, ctypes.c_int]),
+    "nmm_mla_decode_chain_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_chain)]),
+    "nmm_latent_attention_workspace_size": (_sz, [_i64, _i64, _i64, _i64]),
+    "nmm_workspace_init": (ctypes.c_int, [_p, _sz, _p]),
+    "nmm_gemv_plan": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_int, ctypes.c_int,
+                                     ctypes.POINTER(nmm_plan_info)]),
+    "nmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "nmm_version": (ctypes.c_char_p, []),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """Load libnmm.so (raises if it has not been built: there is no other implementation)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_16009_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in EXPORTS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def nmm_status_string(status: int) -> str:
+    return lib().nmm_status_string(status).decode()
+
+
+def nmm_version() -> str:
+    return lib().nmm_version().decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != NMM_OK:
+        raise NmmError(status, where)
+
+
+def _dtype_code(t: torch.Tensor, dt: int | None) -> int:
+    if t.dtype == torch.bfloat16:
+        return NMM_BF16
+    if t.dtype == torch.float16:
+        return NMM_F16
+    if t.dtype in (torch.int16, torch.uint16) and dt in (NMM_F16, NMM_BF16):
+        return dt
+    raise TypeError("x and W must be bfloat16/float16 tensors, or int16 bit patterns with dt given")
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.stride(-1) != 1:
+        raise ValueError("the last dimension must be contiguous")
+    return t.stride(-2) if t.dim() >= 2 else t.shape[-1]
+
+
+class Workspace:
+    """A zeroed device buffer that grows on demand (one per device and user)."""
+
+    def __init__(self, device=None):
+        self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+        self.buf = None
+
+    def get(self, nbytes: int) -> tuple[int, int]:
+        if nbytes == 0:
+            return 0, 0
+        if self.buf is None or self.buf.numel() < nbytes:
+            self.buf = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=self.device)
+        return self.buf.data_ptr(), self.buf.numel()
+
+
+_default_ws: dict = {}
+
+
+def _workspace(ws, nbytes: int, device) -> tuple[int, int]:
+    if ws is None:
+        key = torch.device(device).index
+        ws = _default_ws.setdefault(key, Workspace(device))
+    if isinstance(ws, Workspace):
+        return ws.get(nbytes)
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def nmm_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None = None,
+             path: int = NMM_PATH_AUTO, dt: int | None = None, workspace=None, stream=None) -> torch.Tensor:
+    """y[M,N] = x[M,K] . W[K,N].  x [M, ldx], W [K, ldw], y [M, ldy] (fp32), row-major."""
+    code = _dtype_code(x, dt)
+    M, K = x.shape[0], W.shape[0]
+    N = W.shape[1] if N is None else N
+    need = lib().nmm_gemv_workspace_size(M, K, N, code, path)
+    wp, wb = _workspace(workspace, need, x.device)
+    _check(lib().nmm_gemv(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y.data_ptr(),
+                          _ld(y), path, wp, wb, _stream(stream)), "nmm_gemv")
+    return y
+
+
+def nmm_batched_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None = None,
+                     path: int = NMM_PATH_AUTO, dt: int | None = None, workspace=None,
+                     stream=None) -> torch.Tensor:
+    """y[b] = x[b] . W[b] for 3-D x [B, M, ldx], W [B, K, ldw], y [B, M, ldy] (strided views allowed)."""
+    code = _dtype_code(x, dt)
+    B, M, K = x.shape[0], x.shape[1], W.shape[1]
+    N = W.shape[2] if N is None else N
+    need = lib().nmm_batched_gemv_workspace_size(B, M, K, N, code, path)
+    wp, wb = _workspace(workspace, need, x.device)
+    _check(lib().nmm_batched_gemv(B, M, K, N, code, x.data_ptr(), _ld(x), x.stride(0), W.data_ptr(),
+                                  _ld(W), W.stride(0), y.data_ptr(), _ld(y), y.stride(0), path, wp,
+                                  wb, _stream(stream)), "nmm_batched_gemv")
+    return y
+
+
+def nmm_gemv_plan(M: int, K: int, N: int, dt: int = NMM_BF16, path: int = NMM_PATH_AUTO,
+                  batch: int = 1) -> dict:
+    info = nmm_plan_info()
+    _check(lib().nmm_gemv_plan(batch, M, K, N, dt, path, ctypes.byref(info)), "nmm_gemv_plan")
+    return info.as_dict()
+
+
+def nmm_gemv_workspace_size(M, K, N, dt=NMM_BF16, path=NMM_PATH_AUTO) -> int:
+    return int(lib().nmm_gemv_workspace_size(M, K, N, dt, path))
+
+
+def nmm_batched_gemv_workspace_size(batch, M, K, N, dt=NMM_BF16, path=NMM_PATH_AUTO) -> int:
+    return int(lib().nmm_batched_gemv_workspace_size(batch, M, K, N, dt, path))
+
+
+def nmm_workspace_init(ws: torch.Tensor, stream=None) -> None:
+    _check(lib().nmm_workspace_init(ws.data_ptr(), ws.numel() * ws.element_size(), _stream(stream)),
+           "nmm_workspace_init")
+
+
+CHAIN_DIMS = ("hidden", "q_lora", "kv_lora", "rope", "heads", "nope", "v_head")
+CHAIN_BUFFERS = ("x", "w_down", "w_uq", "w_uk", "w_uv", "w_o", "down_f32", "q_f32", "lat_f32",
+                 "o_f32", "y", "cq_bf16", "qnope_bf16", "lat_bf16", "o_bf16")
+
+
+def _chain_struct(dims: dict, bufs: dict, events=None):
+    c = nmm_mla_chain()
+    for k in CHAIN_DIMS:
+        setattr(c, k, int(dims[k]))
+    for k in CHAIN_BUFFERS:
+        t = bufs.get(k)
+        setattr(c, k, t.data_ptr() if t is not None else None)
+    keep = None
+    if events is not None:
+        handles = [e.cuda_event for e in events]
+        keep = (_p * len(handles))(*handles)
+        c.events = ctypes.cast(keep, _p)
+        c.n_events = len(handles)
+    return c, keep
+
+
+def nmm_mla_decode_chain_workspace_size(dims: dict) -> int:
+    c, _ = _chain_struct(dims, {})
+    return int(lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(c)))
+
+
+def nmm_mla_decode_chain(dims: dict, bufs: dict, *, workspace=None, stream=None, events=None) -> None:
+    """One decode chain (see nmm.h).  ``bufs`` maps the nmm_mla_chain field names to tensors;
+    ``events`` is an optional list of >= 6 torch.cuda.Event(enable_timing=True)."""
+    c, keep = _chain_struct(dims, bufs, events)
+    need = lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(c))
+    wp, wb = _workspace(workspace, need, bufs["x"].device)
+    _check(lib().nmm_mla_decode_chain(ctypes.byref(c), wp, wb, _stream(stream)), "nmm_mla_decode_chain")
+    del keep
+
+
+def nmm_latent_attention_workspace_size(heads, seq, d_qk, d_v) -> int:
+    return int(lib().nmm_latent_attention_workspace_size(heads, seq, d_qk, d_v))
+
+
+def nmm_latent_attention(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, scale: float, *,
+                         d_qk: int | None = None, d_v: int = 512, workspace=None, stream=None) -> torch.Tensor:
+    """out[h, :d_v] = softmax(scale * q[h] . kv[:, :d_qk]^T) . kv[:, :d_v]  (bf16 in, fp32 out)."""
+    heads, seq = q.shape[0], kv.shape[0]
+    d_qk = q.shape[1] if d_qk is None else d_qk
+    need = lib().nmm_latent_attention_workspace_size(heads, seq, d_qk, d_v)
+    wp, wb = _workspace(workspace, need, q.device)
+    _check(lib().nmm_latent_attention(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(),
+                                      _ld(kv), float(scale), out.data_ptr(), _ld(out), wp, wb,
+                                      _stream(stream)), "nmm_latent_attention")
+    return out

@@ -1,0 +1,215 @@
+// The C-ABI entry points of include/nmm.h: argument checks, planning and launches.
+// Every function validates everything before enqueueing anything and never throws.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+
+#include "nmm_internal.h"
+
+using namespace nmm;
+
+namespace {
+
+size_t rup256(size_t v) { return (v + 255) / 256 * 256; }
+
+nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, void* stream) {
+    nmm_status st = validate_gemv(a, path);
+    if (st != NMM_OK) return st;
+    GemvPlan p;
+    st = plan_gemv(a.batch, a.M, a.K, a.N, a.dt, path, &p);
+    if (st != NMM_OK) return st;
+    if (a.batch == 0 || a.M == 0 || a.N == 0) return NMM_OK;
+    if (a.K > 0) {
+        st = validate_workspace(ws, ws_bytes, p.ws_bytes);
+        if (st != NMM_OK) return st;
+    }
+    return launch_gemv(a, p, ws, stream);
+}
+
+// The five narrow MatMuls of one decode chain, with their fused bf16 hand-offs.
+struct Chain {
+    GemvArgs step[5];
+    GemvPlan plan[5];
+    size_t ws_off[5];
+    size_t ws_total;
+};
+
+bool chain_dims_ok(const nmm_mla_chain& c) {
+    const int64_t d[] = {c.hidden, c.q_lora, c.kv_lora, c.rope, c.heads, c.nope, c.v_head};
+    for (int64_t v : d)
+        if (v <= 0 || v >= (int64_t(1) << 31)) return false;
+    return c.nope + c.rope < (int64_t(1) << 31) / c.heads;
+}
+
+nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
+    if (!chain_dims_ok(c)) return NMM_ERR_SHAPE;
+    const int64_t n_down = c.q_lora + c.kv_lora + c.rope;
+    const int64_t qk = c.nope + c.rope;
+    Chain ch;
+    GemvArgs* s = ch.step;
+    // down = x . w_down ; c_q = bf16(down[:q_lora])
+    s[0].K = c.hidden; s[0].N = n_down; s[0].x = c.x; s[0].ldx = c.hidden;
+    s[0].w = c.w_down; s[0].ldw = n_down; s[0].y = c.down_f32; s[0].ldy = n_down;
+    s[0].ybf = c.cq_bf16; s[0].ybf_group = n_down; s[0].ybf_keep = c.q_lora; s[0].ybf_ldm = c.q_lora;
+    // q = c_q . w_uq ; q_nope = bf16(q[h, :nope])
+    s[1].K = c.q_lora; s[1].N = c.heads * qk; s[1].x = c.cq_bf16; s[1].ldx = c.q_lora;
+    s[1].w = c.w_uq; s[1].ldw = c.heads * qk; s[1].y = c.q_f32; s[1].ldy = c.heads * qk;
+    s[1].ybf = c.qnope_bf16; s[1].ybf_group = qk; s[1].ybf_keep = c.nope; s[1].ybf_ldm = c.heads * c.nope;
+    // lat[h] = q_nope[h] . w_uk[h] ; lat' = bf16(lat)
+    s[2].batch = c.heads; s[2].K = c.nope; s[2].N = c.kv_lora;
+    s[2].x = c.qnope_bf16; s[2].ldx = c.nope; s[2].sx = c.nope;
+    s[2].w = c.w_uk; s[2].ldw = c.kv_lora; s[2].sw = c.nope * c.kv_lora;
+    s[2].y = c.lat_f32; s[2].ldy = c.kv_lora; s[2].sy = c.kv_lora;
+    s[2].ybf = c.lat_bf16; s[2].ybf_group = c.kv_lora; s[2].ybf_keep = c.kv_lora;
+    s[2].ybf_ldm = c.kv_lora; s[2].ybf_sb = c.kv_lora;
+    // o[h] = lat'[h] . w_uv[h] ; o' = bf16(o)
+    s[3].batch = c.heads; s[3].K = c.kv_lora; s[3].N = c.v_head;
+    s[3].x = c.lat_bf16; s[3].ldx = c.kv_lora; s[3].sx = c.kv_lora;
+    s[3].w = c.w_uv; s[3].ldw = c.v_head; s[3].sw = c.kv_lora * c.v_head;
+    s[3].y = c.o_f32; s[3].ldy = c.v_head; s[3].sy = c.v_head;
+    s[3].ybf = c.o_bf16; s[3].ybf_group = c.v_head; s[3].ybf_keep = c.v_head;
+    s[3].ybf_ldm = c.v_head; s[3].ybf_sb = c.v_head;
+    // y = o' . w_o
+    s[4].K = c.heads * c.v_head; s[4].N = c.hidden; s[4].x = c.o_bf16; s[4].ldx = c.heads * c.v_head;
+    s[4].w = c.w_o; s[4].ldw = c.hidden; s[4].y = c.y; s[4].ldy = c.hidden;
+    size_t off = 0;
+    for (int i = 0; i < 5; ++i) {
+        s[i].M = 1;
+        s[i].dt = NMM_BF16;
+        nmm_status st = plan_gemv(s[i].batch, 1, s[i].K, s[i].N, NMM_BF16, NMM_PATH_GEMV, &ch.plan[i]);
+        if (st != NMM_OK) return st;
+        ch.ws_off[i] = off;
+        off += rup256(ch.plan[i].ws_bytes);
+    }
+    ch.ws_total = off;
+    *out = ch;
+    return NMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+nmm_status nmm_gemv(int64_t M, int64_t K, int64_t N, nmm_dtype dt, const void* x, int64_t ldx,
+                    const void* W, int64_t ldw, float* y, int64_t ldy, nmm_path path,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+    GemvArgs a;
+    a.M = M; a.K = K; a.N = N; a.dt = dt;
+    a.x = x; a.ldx = ldx; a.w = W; a.ldw = ldw; a.y = y; a.ldy = ldy;
+    return gemv_common(a, path, workspace, workspace_bytes, stream);
+}
+
+nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                            const void* x, int64_t ldx, int64_t stride_x,
+                            const void* W, int64_t ldw, int64_t stride_w,
+                            float* y, int64_t ldy, int64_t stride_y, nmm_path path,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+    GemvArgs a;
+    a.batch = batch; a.M = M; a.K = K; a.N = N; a.dt = dt;
+    a.x = x; a.ldx = ldx; a.sx = stride_x;
+    a.w = W; a.ldw = ldw; a.sw = stride_w;
+    a.y = y; a.ldy = ldy; a.sy = stride_y;
+    return gemv_common(a, path, workspace, workspace_bytes, stream);
+}
+
+size_t nmm_gemv_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt, nmm_path path) {
+    GemvPlan p;
+    return plan_gemv(1, M, K, N, dt, path, &p) == NMM_OK ? p.ws_bytes : 0;
+}
+
+size_t nmm_batched_gemv_workspace_size(int64_t batch, int64_t M, int64_t K, int64_t N,
+                                       nmm_dtype dt, nmm_path path) {
+    GemvPlan p;
+    return plan_gemv(batch, M, K, N, dt, path, &p) == NMM_OK ? p.ws_bytes : 0;
+}
+
+nmm_status nmm_gemv_plan(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                         nmm_path path, nmm_plan_info* info) {
+    if (!info) return NMM_ERR_NULL;
+    GemvPlan p;
+    nmm_status st = plan_gemv(batch, M, K, N, dt, path, &p);
+    if (st != NMM_OK) return st;
+    info->path = p.path;
+    info->m_tile = p.mt;
+    info->m_blocks = p.mblocks;
+    info->panel_width = p.cw_full;
+    info->n_full_panels = p.n_full;
+    info->tail_chunks = p.tail_chunks;
+    info->tail_width = p.tail_cw;
+    info->split_k_full = p.ks_full;
+    info->rows_full = p.rows_full;
+    info->split_k_tail = p.ks_tail;
+    info->rows_tail = p.rows_tail;
+    info->items = p.items;
+    info->threads = kThreads;
+    info->grid = p.grid;
+    info->workspace_bytes = static_cast<int64_t>(p.ws_bytes);
+    return NMM_OK;
+}
+
+size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain) {
+    if (!chain) return 0;
+    Chain ch;
+    return build_chain(*chain, &ch) == NMM_OK ? ch.ws_total : 0;
+}
+
+nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+    if (!chain) return NMM_ERR_NULL;
+    const nmm_mla_chain& c = *chain;
+    if (!c.x || !c.w_down || !c.w_uq || !c.w_uk || !c.w_uv || !c.w_o || !c.down_f32 || !c.q_f32 ||
+        !c.lat_f32 || !c.o_f32 || !c.y || !c.cq_bf16 || !c.qnope_bf16 || !c.lat_bf16 || !c.o_bf16)
+        return NMM_ERR_NULL;
+    Chain ch;
+    nmm_status st = build_chain(c, &ch);
+    if (st != NMM_OK) return st;
+    for (int i = 0; i < 5; ++i) {
+        st = validate_gemv(ch.step[i], NMM_PATH_GEMV);
+        if (st != NMM_OK) return st;
+    }
+    st = validate_workspace(workspace, workspace_bytes, ch.ws_total);
+    if (st != NMM_OK) return st;
+    if (c.events) {
+        if (c.n_events < 6) return NMM_ERR_ARG;
+        for (int i = 0; i < 6; ++i)
+            if (!c.events[i]) return NMM_ERR_NULL;
+    }
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < 5; ++i) {
+        if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess)
+            return NMM_ERR_HIP;
+        void* ws = ch.plan[i].ws_bytes ? static_cast<uint8_t*>(workspace) + ch.ws_off[i] : nullptr;
+        st = launch_gemv(ch.step[i], ch.plan[i], ws, stream);
+        if (st != NMM_OK) return st;
+    }
+    if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[5]), s) != hipSuccess)
+        return NMM_ERR_HIP;
+    return NMM_OK;
+}
+
+nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {
+    if (workspace_bytes == 0) return NMM_OK;
+    if (!workspace) return NMM_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(workspace) & 255u) return NMM_ERR_WORKSPACE;
+    return launch_zero_fill(workspace, workspace_bytes, stream);
+}
+
+const char* nmm_status_string(nmm_status s) {
+    switch (s) {
+        case NMM_OK: return "NMM_OK";
+        case NMM_ERR_NULL: return "NMM_ERR_NULL: a required pointer is NULL";
+        case NMM_ERR_SHAPE: return "NMM_ERR_SHAPE: invalid size, leading dimension or stride";
+        case NMM_ERR_DTYPE: return "NMM_ERR_DTYPE: unknown dtype";
+        case NMM_ERR_ALIGN: return "NMM_ERR_ALIGN: pointer or leading dimension misaligned";
+        case NMM_ERR_WORKSPACE: return "NMM_ERR_WORKSPACE: workspace missing, misaligned or too small";
+        case NMM_ERR_HIP: return "NMM_ERR_HIP: HIP runtime error";
+        case NMM_ERR_PATH: return "NMM_ERR_PATH: path unknown or unavailable for these sizes";
+        case NMM_ERR_ARG: return "NMM_ERR_ARG: invalid argument";
+    }
+    return "unknown nmm_status";
+}
+
+const char* nmm_version(void) { return "0.1.0"; }
+
+}  // extern "C"

@@ -1,0 +1,78 @@
+// Internal declarations shared by the host planner, the C-ABI entry points and the kernels.
+// Nothing here is part of the public ABI (include/nmm.h is).
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+
+#include "nmm.h"
+
+namespace nmm {
+
+// ---------------------------------------------------------------------------------------------
+// Streaming GEMV geometry.
+//
+// W is read in 16-byte chunks (8 consecutive 16-bit columns of one row).  A "panel" is a column
+// range of W: a full panel is cw_full chunks wide (64, 32, 16 or 8 chunks = 512..64 columns), and
+// a wave folds 64 / cw_full rows into one step so that every lane issues one 16-byte load per
+// step (1 KB per wave).  The ragged last panel has tail_chunks < cw_full chunks and folds
+// 64 / tail_width rows (tail_width = a power of two >= tail_chunks).  Each workgroup owns one
+// K-slice of one panel (a work "item").  Narrow panels give parallelism without deep K-splits,
+// which keeps the partial-sum traffic and the final gather short.
+// ---------------------------------------------------------------------------------------------
+constexpr int kWaves = 4;                  // waves per GEMV workgroup
+constexpr int kThreads = 64 * kWaves;      // threads per GEMV workgroup
+constexpr int kPanelChunks = 64;           // chunks per full panel
+constexpr int kPanelCols = 8 * kPanelChunks;
+constexpr int kMaxMTile = 16;              // rows of x per GEMV launch
+constexpr int kXStageBytes = 32 * 1024;    // LDS for the staged x slice of one item
+constexpr int kRedBytes = 32 * 1024;       // LDS for the cross-wave reduction
+// Every split-K workspace starts with a fixed block of arrival counters, and the partial sums
+// always follow it.  So no call's partial sums can land on another call's counters, and one
+// zeroed workspace serves any sequence of calls with different shapes.
+constexpr int64_t kMaxTickets = 16384;
+constexpr int64_t kTicketBytes = kMaxTickets * 4;
+
+struct GemvPlan {
+    int path = NMM_PATH_GEMV;
+    int mt = 1;            // M tile (1, 2, 4, 8, 16)
+    int mblocks = 1;       // ceil(M / mt)
+    int unroll = 8;        // row steps in flight per wave
+    int cw_full = kPanelChunks;  // chunks (= lanes per row) of a full panel: 64, 32, 16 or 8
+    int n_full = 0;        // full panels
+    int tail_chunks = 0;   // chunks in the last (ragged) panel, 0 if none
+    int tail_cw = 0;       // lanes per row in the last panel (power of two >= tail_chunks)
+    int ks_full = 0, rows_full = 0;
+    int ks_tail = 0, rows_tail = 0;
+    int ks_max = 1;        // max(ks_full, ks_tail)
+    int items = 0;         // workgroups per (batch entry, row block)
+    int64_t grid = 0;      // workgroups per launch
+    int64_t n_tickets = 0; // arrival counters (one per panel per batch entry per row block)
+    int64_t part_floats = 0;
+    size_t ws_bytes = 0;   // kTicketBytes of counters + partial sums (0 when not split)
+    bool split() const { return ks_max > 1; }
+};
+
+// Validated arguments of one (batched) GEMV launch.  Element strides.
+struct GemvArgs {
+    int64_t batch = 1, M = 0, K = 0, N = 0;
+    int dt = NMM_BF16;
+    const void* x = nullptr; int64_t ldx = 0, sx = 0;
+    const void* w = nullptr; int64_t ldw = 0, sw = 0;
+    float* y = nullptr; int64_t ldy = 0, sy = 0;
+    // Optional fused bf16 copy of y: output column n goes to
+    //   ybf[b*ybf_sb + m*ybf_ldm + (n / ybf_group) * ybf_keep + (n % ybf_group)]
+    // when (n % ybf_group) < ybf_keep.
+    void* ybf = nullptr; int64_t ybf_group = 0, ybf_keep = 0, ybf_ldm = 0, ybf_sb = 0;
+};
+
+// Pure host functions (no HIP calls): argument checks and the partition.
+nmm_status validate_gemv(const GemvArgs& a, int path);
+nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p);
+nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
+
+// Launchers (defined next to their kernels).  They assume validated arguments.
+nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, void* ws, void* stream);
+nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
+
+}  // namespace nmm

@@ -1,0 +1,173 @@
+// Host-side argument checks and the GEMV partition.  Pure functions: no HIP calls, no device
+// access, so they run (and are tested) on a machine without a GPU.
+//
+// The partition plays the role of Algorithm 2's init stage (Section IV-F), which splits a
+// [K, N] weight into kParts K-slices x fractalNum 16-column fractals and spreads them evenly over
+// at most 2P vector units.  Here the unit of work is a K-slice of a column panel (64 to 512
+// columns; one 16-byte chunk per lane per row).  Panels are narrowed until the grid can hold
+// about `target` equally sized workgroups with at most `ks_cap` K-slices per panel -- enough to
+// keep every compute unit streaming while the split-K gather stays short.
+#include <algorithm>
+#include <cstdlib>
+
+#include "nmm_internal.h"
+
+namespace nmm {
+namespace {
+
+constexpr int64_t kLimit = int64_t(1) << 31;
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+int64_t rup(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+
+int next_pow2(int64_t v) {
+    int p = 1;
+    while (p < v) p <<= 1;
+    return p;
+}
+
+// Tuning overrides (read once per call; unset in normal use).
+int64_t env_int(const char* name, int64_t dflt) {
+    const char* s = std::getenv(name);
+    if (!s || !*s) return dflt;
+    char* end = nullptr;
+    long long v = std::strtoll(s, &end, 10);
+    return (end && *end == '\0' && v > 0) ? v : dflt;
+}
+
+int m_tile_for(int64_t M) {
+    if (M <= 1) return 1;
+    if (M <= 2) return 2;
+    if (M <= 4) return 4;
+    if (M <= 8) return 8;
+    return kMaxMTile;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+nmm_status validate_workspace(const void* ws, size_t bytes, size_t need) {
+    if (need == 0) return NMM_OK;
+    if (!ws || bytes < need || (reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return NMM_ERR_WORKSPACE;
+    return NMM_OK;
+}
+
+nmm_status validate_gemv(const GemvArgs& a, int path) {
+    if (path != NMM_PATH_AUTO && path != NMM_PATH_GEMV && path != NMM_PATH_MFMA) return NMM_ERR_PATH;
+    if (a.dt != NMM_F16 && a.dt != NMM_BF16) return NMM_ERR_DTYPE;
+    if (a.batch < 0 || a.M < 0 || a.K < 0 || a.N < 0) return NMM_ERR_SHAPE;
+    if (a.M >= kLimit || a.K >= kLimit || a.N >= kLimit) return NMM_ERR_SHAPE;
+    if (a.ldx < 0 || a.ldw < 0 || a.ldy < 0 || a.ldx >= kLimit || a.ldw >= kLimit || a.ldy >= kLimit)
+        return NMM_ERR_SHAPE;
+    if (a.sx < 0 || a.sw < 0 || a.sy < 0) return NMM_ERR_SHAPE;
+    if (a.batch == 0 || a.M == 0 || a.N == 0) return NMM_OK;          // nothing is touched
+    if (!a.y) return NMM_ERR_NULL;
+    if (a.ldy < a.N) return NMM_ERR_SHAPE;
+    if (a.K == 0) return NMM_OK;                                      // y = 0; x and W unused
+    if (!a.x || !a.w) return NMM_ERR_NULL;
+    if (a.ldx < a.K || a.ldw < a.N) return NMM_ERR_SHAPE;
+    if (!aligned16(a.x) || !aligned16(a.w) || a.ldx % 8 || a.ldw % 8 || a.sx % 8 || a.sw % 8)
+        return NMM_ERR_ALIGN;
+    if ((reinterpret_cast<uintptr_t>(a.y) & 3u) != 0) return NMM_ERR_ALIGN;
+    const int64_t extent = ((a.K - 1) * a.ldw + rup(a.N, 8)) * 2;    // bytes of one W
+    if (extent >= kLimit) return NMM_ERR_SHAPE;
+    if (a.ybf && (a.ybf_group <= 0 || a.ybf_keep <= 0 || a.ybf_keep > a.ybf_group)) return NMM_ERR_ARG;
+    return NMM_OK;
+}
+
+nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p) {
+    if (!p) return NMM_ERR_NULL;
+    if (dt != NMM_F16 && dt != NMM_BF16) return NMM_ERR_DTYPE;
+    if (path != NMM_PATH_AUTO && path != NMM_PATH_GEMV && path != NMM_PATH_MFMA) return NMM_ERR_PATH;
+    if (batch < 0 || M < 0 || K < 0 || N < 0 || M >= kLimit || K >= kLimit || N >= kLimit)
+        return NMM_ERR_SHAPE;
+    GemvPlan q;
+    // The matrix-core path is not available in this build of the planner: AUTO and MFMA both
+    // resolve to the streaming GEMV, which handles every M in blocks of 16 rows.
+    if (path == NMM_PATH_MFMA) return NMM_ERR_PATH;
+    q.path = NMM_PATH_GEMV;
+    q.mt = m_tile_for(M);
+    q.mblocks = static_cast<int>(std::max<int64_t>(1, cdiv(M, q.mt)));
+    q.unroll = static_cast<int>(env_int("NMM_GEMV_UNROLL", q.mt >= 8 ? 4 : 8));
+    if (q.unroll != 2 && q.unroll != 4 && q.unroll != 8) q.unroll = 8;
+    const int U = q.unroll;
+
+    const int64_t chunks = cdiv(N, 8);
+    const int64_t mats = std::max<int64_t>(batch, 1) * q.mblocks;
+    // Workgroups wanted: about one per 96 KB of W, between 128 and `target` (measured on MI355X:
+    // fewer leave HBM idle, more only add split-K gather work).
+    const int64_t w_bytes = mats * K * chunks * 16;
+    const int64_t target = env_int("NMM_GEMV_TARGET", 1024);
+    const int64_t want = std::max<int64_t>(std::min<int64_t>(128, target), std::min<int64_t>(target, w_bytes / (96 << 10)));
+    // K-slices per panel: fewer for tall row tiles, whose partial sums are MT times larger
+    const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", q.mt >= 8 ? 8 : 16);
+    int min_cw = static_cast<int>(env_int("NMM_GEMV_MINCW", 8));  // narrowest full panel
+    if (min_cw > kPanelChunks || (min_cw & (min_cw - 1))) min_cw = 8;
+    // Start at 256-column panels (512 for 16-row tiles, whose loop is compute-heavier) and
+    // narrow them until the panels x K-slices can reach half the wanted grid.
+    int cw = static_cast<int>(env_int("NMM_GEMV_MAXCW", q.mt >= 16 ? 64 : 32));
+    if (cw > kPanelChunks || (cw & (cw - 1)) || cw < min_cw) cw = std::max(min_cw, 32);
+    while (cw > min_cw && mats * cdiv(chunks, cw) * ks_cap * 2 < want) cw /= 2;
+    q.cw_full = cw;
+    q.n_full = static_cast<int>(chunks / cw);
+    q.tail_chunks = static_cast<int>(chunks % cw);
+    if (q.tail_chunks) {
+        // the staged x slice of a tail item must fit the LDS budget: rows_tail * mt * 4 bytes,
+        // with rows_tail >= kWaves * (64 / tail_cw) * U
+        int lds_cw = 1;
+        while (int64_t(kWaves) * (kPanelChunks / lds_cw) * U * q.mt * 4 > kXStageBytes) lds_cw <<= 1;
+        q.tail_cw = std::max(next_pow2(q.tail_chunks), lds_cw);
+    }
+    if (batch == 0 || M == 0 || N == 0 || K == 0) {
+        q.items = 0;
+        q.grid = 0;
+        *p = q;
+        return NMM_OK;
+    }
+
+    const int64_t rstep_full = int64_t(kWaves) * (kPanelChunks / q.cw_full);   // rows per WG step
+    const int64_t rstep_tail = q.tail_chunks ? int64_t(kWaves) * (kPanelChunks / q.tail_cw) : 1;
+    const int64_t steps_per_matrix = q.n_full * cdiv(K, rstep_full) +
+                                     (q.tail_chunks ? cdiv(K, rstep_tail) : 0);
+    const int64_t total_steps = mats * steps_per_matrix;
+    const int64_t spi = std::max<int64_t>(U, cdiv(total_steps, want));       // WG steps per item
+
+    auto slice = [&](int64_t rstep, int& ks, int& rows) {
+        const int64_t unit = rstep * U;
+        const int64_t cap = std::max<int64_t>(unit, (kXStageBytes / (4 * q.mt * rstep)) / U * unit);
+        int64_t r = std::max<int64_t>(spi * rstep, cdiv(K, ks_cap));           // rows per slice
+        r = std::min<int64_t>(std::min<int64_t>(rup(r, unit), cap), rup(K, unit));
+        int64_t k = cdiv(K, r);
+        r = std::min<int64_t>(cap, rup(cdiv(K, k), unit));   // rebalance the slices
+        k = cdiv(K, r);
+        ks = static_cast<int>(k);
+        rows = static_cast<int>(r);
+    };
+    if (q.n_full) slice(rstep_full, q.ks_full, q.rows_full);
+    if (q.tail_chunks) slice(rstep_tail, q.ks_tail, q.rows_tail);
+    const int64_t panels = q.n_full + (q.tail_chunks ? 1 : 0);
+    if (mats * panels > kMaxTickets) {
+        // more panels than arrival counters: give every panel a single K-slice instead
+        auto whole = [&](int64_t rstep, int& ks, int& rows) {
+            const int64_t unit = rstep * U;
+            ks = 1;
+            rows = static_cast<int>(rup(K, unit));
+        };
+        if (q.n_full) whole(rstep_full, q.ks_full, q.rows_full);
+        if (q.tail_chunks) whole(rstep_tail, q.ks_tail, q.rows_tail);
+        if (std::max(q.rows_full, q.rows_tail) * int64_t(q.mt) * 4 > kXStageBytes) return NMM_ERR_SHAPE;
+    }
+    q.ks_max = std::max(q.ks_full, q.ks_tail);
+    q.items = q.n_full * q.ks_full + (q.tail_chunks ? q.ks_tail : 0);
+    q.grid = batch * q.mblocks * int64_t(q.items);
+    if (q.split()) {
+        q.n_tickets = mats * panels;
+        q.part_floats = mats * panels * q.ks_max * int64_t(q.mt) * kPanelCols;
+        q.ws_bytes = static_cast<size_t>(kTicketBytes + q.part_floats * 4);
+    }
+    *p = q;
+    return NMM_OK;
+}
+
+}  // namespace nmm

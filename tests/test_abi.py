@@ -1,0 +1,155 @@
+"""The C ABI without a GPU: the library loads, exports every function include/nmm.h declares,
+rejects every invalid argument before touching the device, and plans partitions that cover W
+exactly once.  No compute call is made here.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "nmm.h")
+
+nmm = pytest.importorskip("paper_2609_16009_amd")
+if not os.path.exists(nmm.LIB_PATH):
+    pytest.skip("libnmm.so not built", allow_module_level=True)
+
+L = nmm.lib()
+ALIGNED = 1 << 20          # a fake, 256-byte aligned "device address"; never dereferenced here
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    return sorted(set(re.findall(r"\b(nmm_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported():
+    names = declared_functions()
+    assert "nmm_gemv" in names and "nmm_mla_decode_chain" in names and "nmm_latent_attention" in names
+    raw = ctypes.CDLL(nmm.LIB_PATH)
+    missing = [n for n in names if not hasattr(raw, n)]
+    assert not missing, f"declared but not exported: {missing}"
+    assert set(names) <= set(nmm.EXPORTS), "the binding must cover every declared function"
+
+
+def test_status_strings_and_version():
+    for s in range(9):
+        assert L.nmm_status_string(s).decode().startswith("NMM_")
+    assert nmm.nmm_version().count(".") == 2
+
+
+def gemv(**kw):
+    a = dict(M=1, K=64, N=64, dt=nmm.NMM_BF16, x=ALIGNED, ldx=64, W=ALIGNED, ldw=64, y=ALIGNED, ldy=64,
+             path=nmm.NMM_PATH_AUTO, ws=ALIGNED, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return L.nmm_gemv(a["M"], a["K"], a["N"], a["dt"], a["x"], a["ldx"], a["W"], a["ldw"], a["y"],
+                      a["ldy"], a["path"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), nmm.NMM_ERR_NULL),
+    (dict(W=None), nmm.NMM_ERR_NULL),
+    (dict(y=None), nmm.NMM_ERR_NULL),
+    (dict(dt=3), nmm.NMM_ERR_DTYPE),
+    (dict(dt=0), nmm.NMM_ERR_DTYPE),
+    (dict(path=9), nmm.NMM_ERR_PATH),
+    (dict(M=-1), nmm.NMM_ERR_SHAPE),
+    (dict(K=-5), nmm.NMM_ERR_SHAPE),
+    (dict(ldx=32), nmm.NMM_ERR_SHAPE),
+    (dict(ldw=32), nmm.NMM_ERR_SHAPE),
+    (dict(ldy=32), nmm.NMM_ERR_SHAPE),
+    (dict(N=61, ldw=61, ldy=61), nmm.NMM_ERR_ALIGN),
+    (dict(x=ALIGNED + 2), nmm.NMM_ERR_ALIGN),
+    (dict(W=ALIGNED + 8), nmm.NMM_ERR_ALIGN),
+    (dict(ldx=66), nmm.NMM_ERR_ALIGN),
+    (dict(y=ALIGNED + 2), nmm.NMM_ERR_ALIGN),
+    (dict(M=1, K=1 << 31), nmm.NMM_ERR_SHAPE),
+    (dict(K=40000, N=40000, ldw=40000, ldy=40000, ldx=40000), nmm.NMM_ERR_SHAPE),  # W > 2 GiB
+    (dict(K=4096, N=4096, ldw=4096, ldy=4096, ldx=4096, ws=None), nmm.NMM_ERR_WORKSPACE),
+    (dict(K=4096, N=4096, ldw=4096, ldy=4096, ldx=4096, wsb=16), nmm.NMM_ERR_WORKSPACE),
+    (dict(K=4096, N=4096, ldw=4096, ldy=4096, ldx=4096, ws=ALIGNED + 64), nmm.NMM_ERR_WORKSPACE),
+])
+def test_gemv_rejects_invalid_arguments(kw, status):
+    assert gemv(**kw) == status
+
+
+@pytest.mark.parametrize("kw", [dict(M=0), dict(N=0), dict(M=0, x=None, W=None, y=None)])
+def test_empty_problems_are_noops_without_device_access(kw):
+    assert gemv(**kw) == nmm.NMM_OK
+
+
+def test_batched_rejects_misaligned_strides():
+    st = L.nmm_batched_gemv(4, 1, 64, 64, nmm.NMM_BF16, ALIGNED, 64, 68, ALIGNED, 64, 64 * 64,
+                            ALIGNED, 64, 64, 0, ALIGNED, 1 << 30, None)
+    assert st == nmm.NMM_ERR_ALIGN
+    st = L.nmm_batched_gemv(4, 1, 64, 64, nmm.NMM_BF16, ALIGNED, 64, -64, ALIGNED, 64, 64 * 64,
+                            ALIGNED, 64, 64, 0, ALIGNED, 1 << 30, None)
+    assert st == nmm.NMM_ERR_SHAPE
+    assert L.nmm_batched_gemv(0, 1, 64, 64, nmm.NMM_BF16, None, 64, 64, None, 64, 64, None, 64, 64,
+                              0, None, 0, None) == nmm.NMM_OK
+
+
+def test_chain_rejects_null_and_bad_dims():
+    assert L.nmm_mla_decode_chain(None, None, 0, None) == nmm.NMM_ERR_NULL
+    dims = dict(hidden=7168, q_lora=1536, kv_lora=512, rope=64, heads=128, nope=128, v_head=128)
+    bufs = {k: None for k in nmm.CHAIN_BUFFERS}
+    c, _ = nmm._chain_struct(dims, {})
+    assert L.nmm_mla_decode_chain(ctypes.byref(c), ALIGNED, 1 << 30, None) == nmm.NMM_ERR_NULL
+    for k in nmm.CHAIN_BUFFERS:
+        setattr(c, k, ALIGNED)
+    c.hidden = 0
+    assert L.nmm_mla_decode_chain(ctypes.byref(c), ALIGNED, 1 << 30, None) == nmm.NMM_ERR_SHAPE
+    c.hidden = 7168
+    assert L.nmm_mla_decode_chain(ctypes.byref(c), None, 0, None) == nmm.NMM_ERR_WORKSPACE
+    c.x = ALIGNED + 2
+    assert L.nmm_mla_decode_chain(ctypes.byref(c), ALIGNED, 1 << 30, None) == nmm.NMM_ERR_ALIGN
+    assert nmm.nmm_mla_decode_chain_workspace_size(dims) > 0
+    del bufs
+
+
+def test_workspace_init_validates():
+    assert L.nmm_workspace_init(None, 16, None) == nmm.NMM_ERR_NULL
+    assert L.nmm_workspace_init(ALIGNED + 4, 16, None) == nmm.NMM_ERR_WORKSPACE
+    assert L.nmm_workspace_init(None, 0, None) == nmm.NMM_OK
+
+
+SHAPES = [(1, 512, 512), (1, 7168, 2112), (1, 7168, 576), (1, 1536, 24576), (1, 16384, 7168),
+          (2, 1536, 24576), (4, 1536, 24576), (8, 1536, 24576), (16, 1536, 24576), (32, 1536, 24576),
+          (3, 1021, 1031), (1, 1, 1), (1, 13, 8), (5, 77, 3), (16, 4099, 520), (1, 128, 512),
+          (1, 512, 128), (7, 9000, 4200)]
+
+
+@pytest.mark.parametrize("M,K,N", SHAPES)
+@pytest.mark.parametrize("batch", [1, 128])
+def test_plan_covers_w_exactly_once(M, K, N, batch):
+    p = nmm.nmm_gemv_plan(M, K, N, nmm.NMM_BF16, nmm.NMM_PATH_GEMV, batch=batch)
+    chunks = -(-N // 8)
+    pw = p["panel_width"]
+    assert pw in (8, 16, 32, 64)
+    assert p["n_full_panels"] == chunks // pw and p["tail_chunks"] == chunks % pw
+    assert p["m_blocks"] * p["m_tile"] >= M and (p["m_blocks"] - 1) * p["m_tile"] < M
+    waves = p["threads"] // 64
+    for ks, rows, width, present in [(p["split_k_full"], p["rows_full"], pw, p["n_full_panels"] > 0),
+                                     (p["split_k_tail"], p["rows_tail"], p["tail_width"], p["tail_chunks"] > 0)]:
+        if not present:
+            continue
+        assert width >= 1 and (width & (width - 1)) == 0
+        rstep = waves * 64 // width
+        assert rows % rstep == 0                          # whole row-steps per K-slice
+        assert ks * rows >= K and (ks - 1) * rows < K     # slices tile K, none empty
+        assert rows * p["m_tile"] * 4 <= 32 * 1024         # staged x slice fits its LDS budget
+    if p["tail_chunks"]:
+        assert p["tail_width"] >= p["tail_chunks"]
+    items = p["n_full_panels"] * p["split_k_full"] + (p["split_k_tail"] if p["tail_chunks"] else 0)
+    assert p["items"] == items and p["grid"] == batch * p["m_blocks"] * items
+    split = max(p["split_k_full"], p["split_k_tail"]) > 1
+    assert (p["workspace_bytes"] > 0) == split
+    assert nmm.nmm_batched_gemv_workspace_size(batch, M, K, N) == p["workspace_bytes"]
+
+
+def test_plan_rejects_unavailable_path_and_bad_dtype():
+    info = nmm.nmm_plan_info()
+    assert L.nmm_gemv_plan(1, 1, 64, 64, 7, 0, ctypes.byref(info)) == nmm.NMM_ERR_DTYPE
+    assert L.nmm_gemv_plan(1, 1, 64, 64, nmm.NMM_BF16, 5, ctypes.byref(info)) == nmm.NMM_ERR_PATH
+    assert L.nmm_gemv_plan(1, 1, 64, 64, nmm.NMM_BF16, 0, None) == nmm.NMM_ERR_NULL

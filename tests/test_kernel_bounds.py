@@ -1,0 +1,103 @@
+"""CPU model of the GEMV kernel's address arithmetic (gemv.hip), run over the planned grid for
+every shape the GPU tests use: every W load must stay inside the W extent, every x read inside
+x, every LDS access inside the launch's dynamic LDS, and every y / partial-sum / ticket access
+inside its buffer.  This is the check that a launch cannot fault before it runs on a GPU.
+"""
+import numpy as np
+import pytest
+
+nmm = pytest.importorskip("paper_2609_16009_amd")
+
+WAVES, THREADS = 4, 256
+
+
+def check_launch(batch, M, K, N, ldx, ldw, ldy, sx=None, sw=None, sy=None):
+    p = nmm.nmm_gemv_plan(M, K, N, nmm.NMM_BF16, nmm.NMM_PATH_GEMV, batch=batch)
+    if K == 0 or M == 0 or N == 0:
+        return
+    mt, items, mblocks = p["m_tile"], p["items"], p["m_blocks"]
+    sx = M * ldx if sx is None else sx
+    sw = K * ldw if sw is None else sw
+    sy = M * ldy if sy is None else sy
+    extent = ((K - 1) * ldw + (N + 7) // 8 * 8) * 2
+    assert extent < 2 ** 31
+    n_panels = p["n_full_panels"] + (1 if p["tail_chunks"] else 0)
+    ks_max = max(p["split_k_full"], p["split_k_tail"])
+    part_floats = batch * mblocks * n_panels * ks_max * mt * 512
+    lg_tail = (p["tail_width"] - 1).bit_length() if p["tail_chunks"] else 0
+    rows_max = max(p["rows_full"], p["rows_tail"])
+    mg = min(mt, 4)
+    lds_floats = max(rows_max * mt, mg * THREADS * 8)
+    unroll = 4 if mt >= 8 else 8
+    tid = np.arange(THREADS)
+    lane, wave = tid & 63, tid >> 6
+    x_total = (batch - 1) * sx + (M - 1) * ldx + K       # elements a dense x needs
+    y_total = (batch - 1) * sy + (M - 1) * ldy + N
+    for item in range(items):
+        full_lg = (p["panel_width"] - 1).bit_length()
+        if item < p["n_full_panels"] * p["split_k_full"]:
+            panel, sl = divmod(item, p["split_k_full"])
+            lg, ks, rows, valid = full_lg, p["split_k_full"], p["rows_full"], p["panel_width"]
+        else:
+            panel, sl = p["n_full_panels"], item - p["n_full_panels"] * p["split_k_full"]
+            lg, ks, rows, valid = lg_tail, p["split_k_tail"], p["rows_tail"], p["tail_chunks"]
+        cw = 1 << lg
+        c = lane & (cw - 1)
+        rstep = WAVES << (6 - lg)
+        rin = wave * (64 >> lg) + (lane >> lg)
+        k0 = sl * rows
+        assert rows % (rstep * unroll) == 0 and rows * mt <= lds_floats
+        cc = np.minimum(c, valid - 1)
+        nsteps = rows // rstep
+        guard = k0 + rows > K
+        for s in range(nsteps):
+            row = k0 + rin + s * rstep
+            off = row * ldw * 2 + ((panel << full_lg) + cc) * 16
+            issued = row < K if guard else np.ones_like(row, bool)
+            if not guard:
+                assert np.all(row < K)
+            assert np.all(off[issued] >= 0) and np.all(off[issued] + 16 <= extent)
+            assert np.all((s * rstep + rin) * mt + mt - 1 < lds_floats)
+        # reduction buffer and outputs
+        assert np.max(((mg - 1) * rstep + rin) * cw + c) * 8 + 7 < lds_floats
+        pcols = cw * 8
+        for mb in range(mblocks):
+            m0 = mb * mt
+            for b in (0, batch - 1):
+                ms = np.arange(mt)[:, None]
+                cols = np.arange(pcols)[None, :]
+                n = (panel << full_lg) * 8 + cols
+                keep = (m0 + ms < M) & (n < N)
+                yi = b * sy + (m0 + ms) * ldy + n
+                assert np.all(yi[keep] < y_total) and np.all(yi[keep] >= 0)
+                if ks > 1:
+                    pbase = ((b * mblocks + mb) * n_panels + panel) * ks_max * mt * 512
+                    pi = pbase + (ks - 1) * mt * 512 + ms * 512 + cols
+                    assert np.all(pi < part_floats)
+                    assert (b * mblocks + mb) * n_panels + panel < min(batch * mblocks * n_panels, 16384)
+                xk = k0 + min(rows, K - k0) - 1
+                xi = b * sx + (m0 + ms[keep.any(axis=1)]) * ldx + xk
+                assert np.all(xi < x_total)
+
+
+SHAPES = [  # batch, M, K, N, ldx, ldw
+    (1, 1, 512, 512, 512, 512), (1, 1, 7168, 2112, 7168, 2112), (1, 1, 7168, 576, 7168, 576),
+    (1, 1, 1536, 24576, 1536, 24576), (1, 16, 1536, 24576, 1536, 24576), (1, 32, 1536, 24576, 1536, 24576),
+    (1, 2, 1536, 24576, 1536, 24576), (1, 1, 16384, 7168, 16384, 7168),
+    (1, 3, 1021, 1031, 1024, 1032), (1, 1, 1, 1, 8, 8), (1, 5, 77, 3, 80, 8), (1, 16, 4099, 520, 4104, 520),
+    (1, 7, 9000, 4200, 9000, 4200), (1, 1, 13, 8, 16, 8), (1, 2, 300, 64, 304, 64),
+    (1, 1, 33000, 24, 33000, 24), (1, 9, 1536, 3000, 1536, 3000), (1, 1, 2048, 8200, 2048, 8200),
+    (1, 2, 500, 70, 504, 72), (1, 1, 4000, 1000, 4000, 1000), (1, 1, 3000, 700, 3000, 704),
+    (128, 1, 128, 512, 128, 512), (128, 1, 512, 128, 512, 128), (3, 2, 1000, 72, 1000, 72),
+    (5, 16, 96, 1000, 96, 1000), (2, 1, 20000, 40, 20000, 40),
+]
+
+
+@pytest.mark.parametrize("batch,M,K,N,ldx,ldw", SHAPES)
+def test_gemv_launch_stays_in_bounds(batch, M, K, N, ldx, ldw):
+    check_launch(batch, M, K, N, ldx, ldw, ldy=N)
+
+
+def test_strided_query_slice_in_bounds():
+    # x rows of 128 taken every 192 elements (q_nope inside [128, 192])
+    check_launch(128, 1, 128, 512, ldx=128, ldw=512, ldy=512, sx=192)
