@@ -214,6 +214,9 @@ def _chain_struct(dims: dict, bufs: dict, events=None):
         setattr(c, k, t.data_ptr() if t is not None else None)
     keep = None
     if events is not None:
+        for e in events:
+            if not e.cuda_event:      # torch creates the HIP event at its first record
+                e.record()
         handles = [e.cuda_event for e in events]
         keep = (_p * len(handles))(*handles)
         c.events = ctypes.cast(keep, _p)

@@ -24,14 +24,19 @@ nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, v
         st = validate_workspace(ws, ws_bytes, p.ws_bytes);
         if (st != NMM_OK) return st;
     }
-    return launch_gemv(a, p, ws, stream);
+    unsigned* tickets = static_cast<unsigned*>(ws);
+    float* part = ws ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kTicketBytes) : nullptr;
+    return launch_gemv(a, p, tickets, part, stream);
 }
 
-// The five narrow MatMuls of one decode chain, with their fused bf16 hand-offs.
+// The five narrow MatMuls of one decode chain, with their fused bf16 hand-offs.  All steps
+// share one workspace: each takes its own range of the counter block at the head (so every
+// counter any call ever uses lies in that block) and its own partial-sum region after it.
 struct Chain {
     GemvArgs step[5];
     GemvPlan plan[5];
-    size_t ws_off[5];
+    int64_t tick_off[5];   // first counter of each step
+    size_t part_off[5];    // byte offset of each step's partial sums (from the workspace start)
     size_t ws_total;
 };
 
@@ -73,16 +78,24 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
     // y = o' . w_o
     s[4].K = c.heads * c.v_head; s[4].N = c.hidden; s[4].x = c.o_bf16; s[4].ldx = c.heads * c.v_head;
     s[4].w = c.w_o; s[4].ldw = c.hidden; s[4].y = c.y; s[4].ldy = c.hidden;
-    size_t off = 0;
+    size_t off = kTicketBytes;
+    int64_t ticks = 0;
+    bool any_split = false;
     for (int i = 0; i < 5; ++i) {
         s[i].M = 1;
         s[i].dt = NMM_BF16;
         nmm_status st = plan_gemv(s[i].batch, 1, s[i].K, s[i].N, NMM_BF16, NMM_PATH_GEMV, &ch.plan[i]);
         if (st != NMM_OK) return st;
-        ch.ws_off[i] = off;
-        off += rup256(ch.plan[i].ws_bytes);
+        ch.tick_off[i] = ticks;
+        ch.part_off[i] = off;
+        if (ch.plan[i].split()) {
+            any_split = true;
+            ticks += ch.plan[i].n_tickets;
+            off += rup256(static_cast<size_t>(ch.plan[i].part_floats) * 4);
+        }
     }
-    ch.ws_total = off;
+    if (ticks > kMaxTickets) return NMM_ERR_SHAPE;
+    ch.ws_total = any_split ? off : 0;
     *out = ch;
     return NMM_OK;
 }
@@ -179,8 +192,13 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
     for (int i = 0; i < 5; ++i) {
         if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess)
             return NMM_ERR_HIP;
-        void* ws = ch.plan[i].ws_bytes ? static_cast<uint8_t*>(workspace) + ch.ws_off[i] : nullptr;
-        st = launch_gemv(ch.step[i], ch.plan[i], ws, stream);
+        unsigned* tickets = nullptr;
+        float* part = nullptr;
+        if (ch.plan[i].split()) {
+            tickets = static_cast<unsigned*>(workspace) + ch.tick_off[i];
+            part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ch.part_off[i]);
+        }
+        st = launch_gemv(ch.step[i], ch.plan[i], tickets, part, stream);
         if (st != NMM_OK) return st;
     }
     if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[5]), s) != hipSuccess)

@@ -411,7 +411,7 @@ nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream) {
     return last_launch_status();
 }
 
-nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, void* ws, void* stream) {
+nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream) {
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (a.batch == 0 || a.M == 0 || a.N == 0) return NMM_OK;
     if (a.K == 0) {
@@ -455,8 +455,8 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, void* ws, void* str
     kp.mblocks = p.mblocks;
     kp.n_panels = p.n_full + (p.tail_chunks ? 1 : 0);
     if (p.split()) {
-        kp.tickets = static_cast<unsigned*>(ws);
-        kp.part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kTicketBytes);
+        kp.tickets = tickets;
+        kp.part = part;
     }
     const int rows_max = std::max(p.rows_full, p.rows_tail);
     const int mg = p.mt < 4 ? p.mt : 4;

@@ -72,7 +72,9 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
 nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
 
 // Launchers (defined next to their kernels).  They assume validated arguments.
-nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, void* ws, void* stream);
+// `tickets` points into a workspace's counter block and `part` past it (both unused when the
+// plan does not split K).
+nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
 
 }  // namespace nmm

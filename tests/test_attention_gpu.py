@@ -1,0 +1,77 @@
+"""GPU parity of nmm_latent_attention against the oracle's fp64 softmax attention.
+
+Acceptance per output: |o - o_ref| <= 4e-3 * sum_j p_ref,j |V_jn| + 1e-6 (the oracle returns the
+weighted absolute sum).  P is rounded to bf16 for the matrix-core product, a relative error of at
+most 2^-9 per weight, inside that bound.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synthetic as syn
+from gpu_util import assert_parity, dev16
+
+pytestmark = pytest.mark.gpu
+
+nmm = pytest.importorskip("paper_2609_16009_amd")
+
+
+def run_attention(q_bits, kv_bits, scale, dqk, dv, ldo=None):
+    q, kv = dev16(q_bits, syn.BF16), dev16(kv_bits, syn.BF16)
+    heads = q_bits.shape[0]
+    out = torch.full((heads, ldo or dv), np.nan, dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention(q, kv, out, scale, d_qk=dqk, d_v=dv)
+    torch.cuda.synchronize()
+    return out
+
+
+def check(q_bits, kv_bits, scale, dqk, dv, what):
+    out = run_attention(q_bits, kv_bits, scale, dqk, dv)
+    ref, ref_abs = oracle.latent_attention(q_bits, kv_bits, scale, dqk=dqk, dv=dv)
+    return assert_parity(out, ref, ref_abs, what=what), out
+
+
+def test_decode_step_attention_full_size():
+    q, kv, scale = syn.attention_case(4, 128, 4096)
+    check(q, kv, scale, 576, 512, "attention 128x4096x576/512")
+
+
+@pytest.mark.parametrize("heads,seq,dqk,dv,ldkv", [
+    (20, 1000, 96, 48, 104),      # ragged heads and positions, padded cache rows
+    (16, 50, 64, 64, 64),         # one span: no cross-workgroup merge
+    (3, 1, 32, 16, 40),           # a single position
+    (128, 4097, 576, 512, 576),   # one position past a chunk boundary
+    (33, 777, 576, 512, 584),
+])
+def test_attention_ragged(heads, seq, dqk, dv, ldkv):
+    q, kv, scale = syn.attention_case(heads * 7 + seq, heads, seq, dqk=dqk, dv=dv, ldkv=ldkv)
+    check(q, kv, scale, dqk, dv, f"attention {heads}x{seq}x{dqk}/{dv}")
+
+
+def test_attention_sharp_softmax_and_determinism():
+    # a large scale makes the softmax nearly one-hot: stresses the running max and rescaling
+    q, kv, _ = syn.attention_case(9, 32, 2000, dqk=128, dv=64)
+    _, out1 = check(q, kv, 2.0, 128, 64, "sharp softmax")
+    out2 = run_attention(q, kv, 2.0, 128, 64)
+    assert torch.equal(out1, out2)
+
+
+def test_attention_rejects_bad_arguments():
+    q = torch.zeros((16, 576), dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros((64, 576), dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros((16, 512), device="cuda")
+    L = nmm.lib()
+    s = torch.cuda.current_stream().cuda_stream
+    args = lambda **k: dict(dict(h=16, seq=64, dqk=576, dv=512, q=q.data_ptr(), ldq=576, kv=kv.data_ptr(),
+                                 ldkv=576, scale=0.1, out=out.data_ptr(), ldo=512), **k)
+    call = lambda a: L.nmm_latent_attention(a["h"], a["seq"], a["dqk"], a["dv"], a["q"], a["ldq"], a["kv"],
+                                            a["ldkv"], a["scale"], a["out"], a["ldo"], None, 0, s)
+    assert call(args(seq=0)) == nmm.NMM_ERR_SHAPE
+    assert call(args(dqk=100)) == nmm.NMM_ERR_SHAPE
+    assert call(args(dv=520)) == nmm.NMM_ERR_SHAPE
+    assert call(args(scale=float("inf"))) == nmm.NMM_ERR_ARG
+    assert call(args(q=None)) == nmm.NMM_ERR_NULL
+    assert call(args(ldkv=500)) == nmm.NMM_ERR_SHAPE
+    assert call(args(kv=kv.data_ptr() + 2)) == nmm.NMM_ERR_ALIGN
+    assert call(args(h=128, seq=4096)) == nmm.NMM_ERR_WORKSPACE
