@@ -224,6 +224,26 @@ def _chain_struct(dims: dict, bufs: dict, events=None):
     return c, keep
 
 
+class PreparedChain:
+    """A decode chain whose argument struct is built once, so that a launch is a single C call
+    (for tight loops where Python overhead would otherwise show).  ``events`` is an optional
+    list of event lists, one per slot; ``launch(slot)`` uses slot ``slot``'s events."""
+
+    def __init__(self, dims: dict, bufs: dict, workspace=None, events=None):
+        self._bufs = bufs                       # keep the tensors alive
+        self._slots = []
+        for evs in (events or [None]):
+            c, keep = _chain_struct(dims, bufs, evs)
+            self._slots.append((c, keep))
+        need = lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(self._slots[0][0]))
+        self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
+
+    def launch(self, slot: int = 0, stream=None) -> None:
+        c = self._slots[slot][0]
+        _check(lib().nmm_mla_decode_chain(ctypes.byref(c), self._wp, self._wb, _stream(stream)),
+               "nmm_mla_decode_chain")
+
+
 def nmm_mla_decode_chain_workspace_size(dims: dict) -> int:
     c, _ = _chain_struct(dims, {})
     return int(lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(c)))
