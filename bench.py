@@ -129,11 +129,13 @@ def main() -> int:
     log(f"[bench] {args.copies} weight copies resident ({args.copies * (chain_total + attn_total) / 2**30:.2f} GiB)")
 
     sa, sb = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    cap = torch.cuda.Stream(device=dev)        # capture / replay stream
     ws_a, ws_b = nmm.Workspace(dev), nmm.Workspace(dev)
     ev = lambda: torch.cuda.Event(enable_timing=True)
     K, W = args.steps, args.warmup
     n_slots = W + K
     chain_ev = [[ev() for _ in range(6)] for _ in range(n_slots)]
+    att_ev = [[ev(), ev()] for _ in range(n_slots)]
     chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a,
                                 events=[chain_ev[s] for s in range(n_slots) if s % args.copies == c])
               for c in range(args.copies)]
@@ -143,32 +145,62 @@ def main() -> int:
         _, q, kv = copies[s % args.copies]
         nmm.nmm_latent_attention(q, kv, att_out, step.scale, d_qk=dqk, d_v=dv, workspace=ws_b, stream=stream)
 
-    main_stream = torch.cuda.current_stream()
-
-    def decode_step(s, b_ev):
+    def decode_step(s):
+        # fork: stream A runs the narrow chain, stream B the latent attention; then join
         start = torch.cuda.Event()
-        start.record(main_stream)
+        start.record(cap)
         sa.wait_event(start)
         sb.wait_event(start)
         chains[s % args.copies].launch(slot_of(s), stream=sa)
-        b_ev[0].record(sb)
+        att_ev[s][0].record(sb)
         attention(s, sb)
-        b_ev[1].record(sb)
-        main_stream.wait_stream(sa)
-        main_stream.wait_stream(sb)
+        att_ev[s][1].record(sb)
+        cap.wait_stream(sa)
+        cap.wait_stream(sb)
 
-    # ---- warmup, then exactly K timed steps
-    att_ev = [[ev(), ev()] for _ in range(n_slots)]
-    for s in range(W):
-        decode_step(s, att_ev[s])
+    def chain_only(s):
+        chains[s % args.copies].launch(slot_of(s), stream=cap)
+
+    def attn_only(s):
+        attention(s, cap)
+
+    def serial(s):
+        chain_only(s)
+        attn_only(s)
+
+    def capture(fn, s):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=cap):
+            fn(s)
+        return g
+
+    for e in (x for pair in att_ev for x in pair):   # create the HIP events before any capture
+        e.record(cap)
+    # eager pass first: sizes the workspaces and gives the reference result for the graphs
+    with torch.cuda.stream(cap):
+        decode_step(0)
     torch.cuda.synchronize()
+    y_eager, att_eager = inter["y"].clone(), att_out.clone()
+    t = time.perf_counter()
+    step_graphs = [capture(decode_step, s) for s in range(n_slots)]
+    alone = {name: [capture(fn, s) for s in range(args.copies)]
+             for name, fn in (("chain", chain_only), ("attention", attn_only), ("serial", serial))}
+    log(f"[bench] captured {n_slots + 3 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
+
+    # ---- warmup, then exactly K timed steps (graph replays on one stream)
     t0, t1 = ev(), ev()
-    t0.record(main_stream)
-    for s in range(W, W + K):
-        decode_step(s, att_ev[s])
-    t1.record(main_stream)
+    with torch.cuda.stream(cap):
+        for s in range(W):
+            step_graphs[s].replay()
+        torch.cuda.synchronize()
+        t0.record(cap)
+        for s in range(W, W + K):
+            step_graphs[s].replay()
+        t1.record(cap)
     torch.cuda.synchronize()
     step_ms = t0.elapsed_time(t1) / K
+    same = torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager)
+    assert same, "graph replays must reproduce the eager decode step bit for bit"
     names = list(cb)
     per_launch = {n: [] for n in names}
     for s in range(W, W + K):
@@ -181,31 +213,23 @@ def main() -> int:
     log(f"[bench] step {step_ms * 1e3:.1f} us (chain {chain_ms_in_step * 1e3:.1f} us, attention "
         f"{attn_ms_in_step * 1e3:.1f} us on stream B); GEMV launches {achieved:.0f} GB/s")
 
-    # ---- the overlap experiment: each stream alone, then serial on one stream
-    def timed(fn, n):
-        for s in range(min(W, 5)):
-            fn(s)
+    # ---- the overlap experiment: each stream alone, then both serially on one stream
+    def timed(graphs):
+        for s in range(len(graphs)):
+            graphs[s].replay()
         torch.cuda.synchronize()
         a, b = ev(), ev()
-        a.record(main_stream)
-        for s in range(n):
-            fn(W + s)
-        b.record(main_stream)
+        a.record(cap)
+        for s in range(K):
+            graphs[s % len(graphs)].replay()
+        b.record(cap)
         torch.cuda.synchronize()
-        return a.elapsed_time(b) / n
+        return a.elapsed_time(b) / K
 
-    def chain_only(s):
-        chains[s % args.copies].launch(slot_of(s), stream=main_stream)
-
-    def attn_only(s):
-        attention(s, main_stream)
-
-    def serial(s):
-        chain_only(s)
-        attn_only(s)
-    t_a = timed(chain_only, K)
-    t_b = timed(attn_only, K)
-    t_serial = timed(serial, K)
+    with torch.cuda.stream(cap):
+        t_a = timed(alone["chain"])
+        t_b = timed(alone["attention"])
+        t_serial = timed(alone["serial"])
     gain = mean_gain(step_ms, t_serial)
     bound = 1.0 - max(t_a, t_b) / (t_a + t_b)
     log(f"[bench] chain alone {t_a * 1e3:.1f} us, attention alone {t_b * 1e3:.1f} us, serial "

@@ -198,12 +198,23 @@ typedef struct {
     int32_t rows_tail;       /* rows per K-slice of the last panel */
     int32_t items;           /* workgroups per matrix (per batch entry, per row block) */
     int32_t threads;         /* threads per workgroup */
+    int32_t unroll;          /* row steps each wave keeps in flight */
     int64_t grid;            /* total workgroups of one launch */
     int64_t workspace_bytes;
 } nmm_plan_info;
 
 nmm_status nmm_gemv_plan(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
                          nmm_path path, nmm_plan_info* info);
+
+/*
+ * nmm_read_probe -- measurement support, not part of the product path: reads `bytes` (a multiple
+ * of 16) of device memory at `buf` once with the GEMV's load instruction (16-byte non-temporal
+ * buffer loads, `unroll` = 1, 2, 4 or 8 in flight per lane) on `grid` workgroups of 256 threads,
+ * and writes one checksum word per workgroup to out[grid].  Timing it gives the practical HBM
+ * read bandwidth that roofline fractions are compared against.
+ */
+nmm_status nmm_read_probe(const void* buf, size_t bytes, uint32_t* out, int64_t grid, int unroll,
+                          void* stream);
 
 /* Human-readable name of a status code (static storage). */
 const char* nmm_status_string(nmm_status s);

@@ -41,7 +41,7 @@ class nmm_plan_info(ctypes.Structure):
                 ("tail_width", ctypes.c_int32), ("split_k_full", ctypes.c_int32),
                 ("rows_full", ctypes.c_int32), ("split_k_tail", ctypes.c_int32),
                 ("rows_tail", ctypes.c_int32), ("items", ctypes.c_int32),
-                ("threads", ctypes.c_int32), ("grid", ctypes.c_int64),
+                ("threads", ctypes.c_int32), ("unroll", ctypes.c_int32), ("grid", ctypes.c_int64),
                 ("workspace_bytes", ctypes.c_int64)]
 
     def as_dict(self) -> dict:
@@ -70,6 +70,7 @@ EXPORTS = {
     "nmm_workspace_init": (ctypes.c_int, [_p, _sz, _p]),
     "nmm_gemv_plan": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_int, ctypes.c_int,
                                      ctypes.POINTER(nmm_plan_info)]),
+    "nmm_read_probe": (ctypes.c_int, [_p, _sz, _p, _i64, ctypes.c_int, _p]),
     "nmm_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "nmm_version": (ctypes.c_char_p, []),
 }
@@ -274,3 +275,11 @@ def nmm_latent_attention(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, s
                                       _ld(kv), float(scale), out.data_ptr(), _ld(out), wp, wb,
                                       _stream(stream)), "nmm_latent_attention")
     return out
+
+
+def nmm_read_probe(buf: torch.Tensor, out: torch.Tensor, grid: int, unroll: int = 4, stream=None) -> None:
+    """Read all of ``buf`` once on the GPU (bandwidth calibration); ``out`` holds >= grid uint32."""
+    if out.numel() * out.element_size() < 4 * grid:
+        raise ValueError("out must hold one uint32 per workgroup")
+    _check(lib().nmm_read_probe(buf.data_ptr(), buf.numel() * buf.element_size(), out.data_ptr(), grid,
+                                unroll, _stream(stream)), "nmm_read_probe")

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 
 #include "nmm_internal.h"
@@ -12,6 +13,19 @@ using namespace nmm;
 namespace {
 
 size_t rup256(size_t v) { return (v + 255) / 256 * 256; }
+
+// Workgroups of the persistent chain launch: one per compute unit of the current device, so
+// that all of them are resident together even beside other kernels (NMM_CHAIN_WGS overrides).
+int chain_workgroups() {
+    if (const char* s = std::getenv("NMM_CHAIN_WGS")) {
+        const long v = std::strtol(s, nullptr, 10);
+        if (v > 0 && v < (1 << 20)) return static_cast<int>(v);
+    }
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    return cus;
+}
 
 nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, void* stream) {
     nmm_status st = validate_gemv(a, path);
@@ -79,7 +93,7 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
     s[4].K = c.heads * c.v_head; s[4].N = c.hidden; s[4].x = c.o_bf16; s[4].ldx = c.heads * c.v_head;
     s[4].w = c.w_o; s[4].ldw = c.hidden; s[4].y = c.y; s[4].ldy = c.hidden;
     size_t off = kTicketBytes;
-    int64_t ticks = 0;
+    int64_t ticks = kChainSyncWords;   // the fused chain's queue and completion words come first
     bool any_split = false;
     for (int i = 0; i < 5; ++i) {
         s[i].M = 1;
@@ -95,7 +109,8 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
         }
     }
     if (ticks > kMaxTickets) return NMM_ERR_SHAPE;
-    ch.ws_total = any_split ? off : 0;
+    (void)any_split;
+    ch.ws_total = off;   // the counter block is always needed: the fused chain keeps its queue there
     *out = ch;
     return NMM_OK;
 }
@@ -156,6 +171,7 @@ nmm_status nmm_gemv_plan(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dty
     info->rows_tail = p.rows_tail;
     info->items = p.items;
     info->threads = kThreads;
+    info->unroll = p.unroll;
     info->grid = p.grid;
     info->workspace_bytes = static_cast<int64_t>(p.ws_bytes);
     return NMM_OK;
@@ -189,6 +205,28 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
             if (!c.events[i]) return NMM_ERR_NULL;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // One launch per MatMul by default.  NMM_CHAIN_FUSED=1 selects the persistent launch that runs
+    // all five MatMuls (bit-identical results); on MI355X it is slower (130 vs 79 us for the
+    // decode chain), because one resident workgroup per compute unit keeps too few loads in flight.
+    const char* fe = std::getenv("NMM_CHAIN_FUSED");
+    const bool fused = (fe && fe[0] == '1') && chain_fusable(ch.step, ch.plan, 5);
+    if (fused) {
+        unsigned* sync = static_cast<unsigned*>(workspace);
+        unsigned* tickets[5];
+        float* part[5];
+        for (int i = 0; i < 5; ++i) {
+            tickets[i] = ch.plan[i].split() ? sync + ch.tick_off[i] : nullptr;
+            part[i] = ch.plan[i].split() ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ch.part_off[i]) : nullptr;
+        }
+        if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[0]), s) != hipSuccess) return NMM_ERR_HIP;
+        st = launch_chain(ch.step, ch.plan, 5, sync, tickets, part, chain_workgroups(), stream);
+        if (st != NMM_OK) return st;
+        if (c.events) {
+            for (int i = 1; i < 6; ++i)
+                if (hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess) return NMM_ERR_HIP;
+        }
+        return NMM_OK;
+    }
     for (int i = 0; i < 5; ++i) {
         if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess)
             return NMM_ERR_HIP;

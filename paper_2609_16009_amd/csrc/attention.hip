@@ -15,8 +15,10 @@
 //  * P.V: wave w owns the output column tiles w, w+4, ...; V is staged through LDS row-major and
 //    read back with ds_read_b64_tr_b16, gfx950's transposing LDS read, which hands each lane the
 //    8 positions of one column that the MFMA B operand needs.
-//  * The spans' partial (max, sum, output) go to the workspace with device-scope atomic stores;
-//    the last workgroup of each head block (a ticket) merges them in span order.
+//  * Every load of the next chunk (K fragments, both halves of V) is issued one chunk ahead,
+//    branch-free: positions outside the span read zeros through the buffer's range check.
+//  * The spans' partial (max, sum, output) go to the workspace; a small merge kernel on the same
+//    stream combines them in span order (the kernel boundary makes the partials visible).
 //  * Workgroups of one span are placed on the same XCD (ids 8 apart) so the span's K/V rows are
 //    read from HBM once per XCD and then served from that XCD's L2.
 #include <hip/hip_runtime.h>
@@ -52,7 +54,6 @@ struct AttnParams {
     int64_t ldo;
     float* part_o;      // [n_hb][nsp][16][d_v]
     float* part_ml;     // [n_hb][nsp][16][2]
-    unsigned* tickets;  // [n_hb]
     int heads, seq, dqk, dv;
     int nsp, span, n_hb;
     int xcd_map;        // 1: spans grouped per XCD (nsp % 8 == 0)
@@ -83,11 +84,50 @@ __device__ __forceinline__ uint16_t bf16_bits(float v) {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
 }
 
+// One chunk's K fragments for this lane: position `pos`, 8 dims per MFMA k-step.
+template <int KS>
+__device__ __forceinline__ void load_k(i32x4 (&kb)[KS], __amdgpu_buffer_rsrc_t kvr, int pos, bool ok,
+                                       int64_t ldkv, int g, int ksteps) {
+    const uint32_t base = uint32_t((int64_t(pos) * ldkv + 8 * g) * 2);
+#pragma unroll
+    for (int u = 0; u < KS; ++u)
+        kb[u] = __builtin_amdgcn_raw_buffer_load_b128(kvr, (ok && u < ksteps) ? base + u * 64 : kOutOfRange, 0, 0);
+}
+
+// One half chunk (32 positions) of V rows, this thread's 16-byte pieces.
+template <int VP>
+__device__ __forceinline__ void load_v(i32x4 (&vr)[VP], __amdgpu_buffer_rsrc_t kvr, int r0, int s_end,
+                                       int64_t ldkv, int vchunks, int tid) {
+#pragma unroll
+    for (int q = 0; q < VP; ++q) {
+        const int i = tid + q * kAThreads;
+        const int r = i / vchunks, c = i - r * vchunks;
+        const bool ok = i < 32 * vchunks && r0 + r < s_end;
+        vr[q] = __builtin_amdgcn_raw_buffer_load_b128(kvr, ok ? uint32_t((int64_t(r0 + r) * ldkv + 8 * c) * 2) : kOutOfRange,
+                                                      0, 0);
+    }
+}
+
+template <int VP>
+__device__ __forceinline__ void store_v(const i32x4 (&vr)[VP], uint16_t* v_lds, int v_stride, int vchunks, int tid) {
+#pragma unroll
+    for (int q = 0; q < VP; ++q) {
+        const int i = tid + q * kAThreads;
+        if (i < 32 * vchunks) {
+            const int r = i / vchunks, c = i - r * vchunks;
+            *reinterpret_cast<i32x4*>(v_lds + r * v_stride + 8 * c) = vr[q];
+        }
+    }
+}
+
+// The span's partial result for 16 heads: running max (log2 units), running sum, and the
+// unnormalised output, all written with plain stores; the merge kernel, launched next on the
+// same stream, reads them.
+template <int KS, int VP, int QP>
 __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p) {
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
     __shared__ float red_max[4][kAHeads];
     __shared__ float red_sum[4][kAHeads];
-    __shared__ int s_last;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, j = lane & 15;
@@ -110,17 +150,38 @@ __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p
     uint16_t* v_lds = p_lds + kAHeads * (kAChunk + 8);         // [32][v_stride]
     constexpr int kPStride = kAChunk + 8;
 
-    // ---- Q block into LDS (rows past `heads` are zero)
+    const __amdgpu_buffer_rsrc_t kvr = make_rsrc(p.kv, p.kv_extent);
+    const int ksteps = p.dqk / 32;
+    const int vchunks = p.dv / 8;
+    // ---- Q block: every load issued at once (rows past `heads` read zeros), then the first
+    // chunk's K and V loads, then Q goes to LDS while those are in flight
+    const int qcpr = p.dqk / 8;
+    i32x4 qv[QP];
     {
-        const int cpr = p.dqk / 8;
-        for (int i = tid; i < kAHeads * cpr; i += kAThreads) {
-            const int r = i / cpr, c = i - r * cpr;
-            i32x4 v = i32x4{0, 0, 0, 0};
-            if (h0 + r < p.heads) v = *reinterpret_cast<const i32x4*>(p.q + int64_t(h0 + r) * p.ldq + 8 * c);
-            *reinterpret_cast<i32x4*>(q_lds + r * p.q_stride + 8 * c) = v;
+        const int64_t q_rows = min(kAHeads, p.heads - h0);
+        const __amdgpu_buffer_rsrc_t qr =
+            make_rsrc(p.q + int64_t(h0) * p.ldq, uint32_t(((q_rows - 1) * p.ldq + p.dqk) * 2));
+#pragma unroll
+        for (int u = 0; u < QP; ++u) {
+            const int i = tid + u * kAThreads;
+            const int r = i / qcpr, c = i - r * qcpr;
+            const bool ok = i < kAHeads * qcpr && r < q_rows;
+            qv[u] = __builtin_amdgcn_raw_buffer_load_b128(qr, ok ? uint32_t((int64_t(r) * p.ldq + 8 * c) * 2) : kOutOfRange,
+                                                          0, 0);
         }
     }
-    const __amdgpu_buffer_rsrc_t kvr = make_rsrc(p.kv, p.kv_extent);
+    i32x4 kb[KS], v0[VP], v1[VP];
+    load_k<KS>(kb, kvr, s_begin + 16 * wave + j, s_begin + 16 * wave + j < s_end, p.ldkv, g, ksteps);
+    load_v<VP>(v0, kvr, s_begin, s_end, p.ldkv, vchunks, tid);
+    load_v<VP>(v1, kvr, s_begin + 32, s_end, p.ldkv, vchunks, tid);
+#pragma unroll
+    for (int u = 0; u < QP; ++u) {
+        const int i = tid + u * kAThreads;
+        if (i < kAHeads * qcpr) {
+            const int r = i / qcpr, c = i - r * qcpr;
+            *reinterpret_cast<i32x4*>(q_lds + r * p.q_stride + 8 * c) = qv[u];
+        }
+    }
     const int ntiles = p.dv / 16;
     const int my_tiles = (ntiles - wave + 3) / 4;              // tiles w, w+4, ...
     f32x4 o[kAMaxTiles];
@@ -132,38 +193,29 @@ __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p
         m_run[i] = -INFINITY;
         l_run[i] = 0.f;
     }
-    const int vchunks = p.dv / 8;                // 16-byte pieces per V row
-    const int v_per_thread = (32 * vchunks + kAThreads - 1) / kAThreads;
     __syncthreads();
 
     for (int c0 = s_begin; c0 < s_end; c0 += kAChunk) {
+        const int next = c0 + kAChunk;
         // ---- scores for this wave's 16 positions: S[16 heads][16 pos] = Q . K^T
         const int pos = c0 + 16 * wave + j;
         const bool pos_ok = pos < s_end;
-        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
-        {
-            const uint32_t kbase = pos_ok ? uint32_t((int64_t(pos) * p.ldkv + 8 * g) * 2) : kOutOfRange;
-            const int ksteps = p.dqk / 32;
-            for (int k0 = 0; k0 < ksteps; k0 += 6) {
-                i32x4 kb[6];
+        f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f}, s2 = f32x4{0.f, 0.f, 0.f, 0.f};   // two chains
 #pragma unroll
-                for (int u = 0; u < 6; ++u)
-                    kb[u] = (k0 + u < ksteps)
-                                ? __builtin_amdgcn_raw_buffer_load_b128(kvr, pos_ok ? kbase + (k0 + u) * 64 : kOutOfRange, 0, 0)
-                                : i32x4{0, 0, 0, 0};
-#pragma unroll
-                for (int u = 0; u < 6; ++u) {
-                    if (k0 + u < ksteps) {
-                        const i32x4 a = *reinterpret_cast<const i32x4*>(q_lds + j * p.q_stride + 32 * (k0 + u) + 8 * g);
-                        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(kb[u]), s, 0, 0, 0);
-                    }
-                }
+        for (int u = 0; u < KS; ++u) {
+            if (u < ksteps) {
+                const i32x4 a = *reinterpret_cast<const i32x4*>(q_lds + j * p.q_stride + 32 * u + 8 * g);
+                if (u & 1) s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(kb[u]), s2, 0, 0, 0);
+                else s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(kb[u]), s, 0, 0, 0);
             }
         }
+        s += s2;
+        // next chunk's K fragments fly during the softmax and P.V below
+        load_k<KS>(kb, kvr, next + 16 * wave + j, next + 16 * wave + j < s_end, p.ldkv, g, ksteps);
+
         // scores in log2 units: s * scale * log2(e), so softmax weights are exp2(s - max)
 #pragma unroll
         for (int i = 0; i < 4; ++i) s[i] = pos_ok ? s[i] * p.scale_log2 : -INFINITY;
-        // ---- chunk maxima per head (rows 4g+i of this lane's tile)
         float cm[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) cm[i] = row16_max(s[i]);
@@ -187,7 +239,9 @@ __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p
             const float cs = row16_sum(pr[i]);
             if (j == 0) red_sum[wave][4 * g + i] = cs;
         }
+        store_v<VP>(v0, v_lds, p.v_stride, vchunks, tid);      // V rows c0 .. c0+31
         __syncthreads();
+        load_v<VP>(v0, kvr, next, s_end, p.ldkv, vchunks, tid);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = 4 * g + i;
@@ -200,21 +254,16 @@ __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p
             for (int i = 0; i < 4; ++i) o[t][i] *= alpha[i];
 
         // ---- P . V in two halves of 32 positions (one MFMA k-step each)
+        const int a4 = j >> 2, b4 = j & 3;
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
-            const int r0 = c0 + 32 * half;
-            for (int q = 0; q < v_per_thread; ++q) {
-                const int i = tid + q * kAThreads;
-                if (i < 32 * vchunks) {
-                    const int r = i / vchunks, c = i - r * vchunks;
-                    const uint32_t off = (r0 + r < s_end) ? uint32_t((int64_t(r0 + r) * p.ldkv + 8 * c) * 2) : kOutOfRange;
-                    const i32x4 v = __builtin_amdgcn_raw_buffer_load_b128(kvr, off, 0, 0);
-                    *reinterpret_cast<i32x4*>(v_lds + r * p.v_stride + 8 * c) = v;
-                }
+            if (half == 1) {
+                __syncthreads();                                  // every wave is done with half 0
+                store_v<VP>(v1, v_lds, p.v_stride, vchunks, tid);  // V rows c0+32 .. c0+63
+                __syncthreads();
+                load_v<VP>(v1, kvr, next + 32, s_end, p.ldkv, vchunks, tid);
             }
-            __syncthreads();
             const i32x4 a = *reinterpret_cast<const i32x4*>(p_lds + j * kPStride + 32 * half + 8 * g);
-            const int a4 = j >> 2, b4 = j & 3;
 #pragma unroll
             for (int t = 0; t < kAMaxTiles; ++t) {
                 if (t < my_tiles) {
@@ -227,12 +276,11 @@ __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p
                     o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), o[t], 0, 0, 0);
                 }
             }
-            __syncthreads();
         }
+        __syncthreads();   // P, V and the reductions are reused by the next chunk
     }
 
     // ---- this span's result
-    const int64_t pidx = int64_t(hb) * p.nsp + sp;
     if (p.nsp == 1) {
 #pragma unroll
         for (int t = 0; t < kAMaxTiles; ++t) {
@@ -247,70 +295,74 @@ __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p
         }
         return;
     }
+    const int64_t pidx = int64_t(hb) * p.nsp + sp;
     float* po = p.part_o + pidx * (kAHeads * int64_t(p.dv));
 #pragma unroll
     for (int t = 0; t < kAMaxTiles; ++t) {
         if (t < my_tiles) {
             const int n = 16 * (wave + 4 * t) + j;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                __hip_atomic_store(po + (4 * g + i) * p.dv + n, o[t][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int i = 0; i < 4; ++i) po[(4 * g + i) * p.dv + n] = o[t][i];
         }
     }
     if (wave == 0 && j == 0) {
         float* pml = p.part_ml + pidx * (kAHeads * 2);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            __hip_atomic_store(pml + (4 * g + i) * 2, m_run[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(pml + (4 * g + i) * 2 + 1, l_run[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            pml[(4 * g + i) * 2] = m_run[i];
+            pml[(4 * g + i) * 2 + 1] = l_run[i];
         }
     }
-    // hand-off as in the GEMV gather: device-scope atomics, completion waits, one ticket
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid == 0) {
-        const unsigned prev = __hip_atomic_fetch_add(p.tickets + hb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int last = prev == unsigned(p.nsp - 1);
-        if (last) __hip_atomic_store(p.tickets + hb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = last;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    // ---- merge the spans in order: out = sum_s w_s O_s with w_s = 2^(m_s - M) / sum_q 2^(m_q - M) l_q
-    float* wgt = reinterpret_cast<float*>(smem);   // [16][nsp]; the loop's LDS is free now
+}
+
+// Merge the spans of each head block in span order:
+//   out = sum_s w_s O_s,  w_s = 2^(m_s - M) / sum_q 2^(m_q - M) l_q,  M = max_s m_s.
+// One workgroup per (head block, 16 output columns): thread (r, c) owns head r, column c and
+// issues the loads of all its spans at once.
+constexpr int kMergeCols = 16;
+__global__ __launch_bounds__(kAThreads) void attention_merge_kernel(const AttnParams p) {
+    extern __shared__ __attribute__((aligned(16))) float mls[];   // [nsp][16][2], then [16][nsp]
+    float* wgt = mls + p.nsp * kAHeads * 2;
+    const int n_cb = (p.dv + kMergeCols - 1) / kMergeCols;
+    const int hb = blockIdx.x / n_cb, cb = blockIdx.x - hb * n_cb;
+    const int h0 = hb * kAHeads;
+    const int tid = threadIdx.x;
     const float* ml = p.part_ml + int64_t(hb) * p.nsp * (kAHeads * 2);
+    for (int i = tid; i < p.nsp * kAHeads * 2; i += kAThreads) mls[i] = ml[i];
+    __syncthreads();
     if (tid < kAHeads) {
         const int r = tid;
         float M = -INFINITY;
-        for (int q = 0; q < p.nsp; ++q)
-            M = fmaxf(M, __hip_atomic_load(ml + q * (kAHeads * 2) + r * 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+        for (int q = 0; q < p.nsp; ++q) M = fmaxf(M, mls[(q * kAHeads + r) * 2]);
         float den = 0.f;
         for (int q = 0; q < p.nsp; ++q) {
-            const float mq = __hip_atomic_load(ml + q * (kAHeads * 2) + r * 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const float lq = __hip_atomic_load(ml + q * (kAHeads * 2) + r * 2 + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const float mq = mls[(q * kAHeads + r) * 2];
             const float w = (mq == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mq - M);
             wgt[r * p.nsp + q] = w;
-            den += w * lq;
+            den += w * mls[(q * kAHeads + r) * 2 + 1];
         }
         for (int q = 0; q < p.nsp; ++q) wgt[r * p.nsp + q] /= den;
     }
     __syncthreads();
-    for (int o_i = tid; o_i < kAHeads * p.dv; o_i += kAThreads) {
-        const int r = o_i / p.dv, n = o_i - r * p.dv;
-        if (h0 + r >= p.heads) continue;
-        const float* src = p.part_o + int64_t(hb) * p.nsp * (kAHeads * int64_t(p.dv)) + r * p.dv + n;
-        float acc = 0.f;
-        for (int q = 0; q < p.nsp; ++q)
-            acc += wgt[r * p.nsp + q] *
-                   __hip_atomic_load(src + int64_t(q) * (kAHeads * p.dv), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        p.out[int64_t(h0 + r) * p.ldo + n] = acc;
+    const int r = tid / kMergeCols, n = cb * kMergeCols + (tid % kMergeCols);
+    if (h0 + r >= p.heads || n >= p.dv) return;
+    const float* src = p.part_o + int64_t(hb) * p.nsp * (kAHeads * int64_t(p.dv)) + r * p.dv + n;
+    float acc = 0.f;
+    for (int q0 = 0; q0 < p.nsp; q0 += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = (q0 + u < p.nsp) ? src[int64_t(q0 + u) * (kAHeads * p.dv)] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 16; ++u)
+            if (q0 + u < p.nsp) acc += wgt[r * p.nsp + q0 + u] * v[u];
     }
+    p.out[int64_t(h0 + r) * p.ldo + n] = acc;
 }
 
 struct AttnPlan {
     int n_hb = 0, nsp = 1, span = 0, xcd_map = 0;
     size_t ws_bytes = 0;
-    size_t lds_bytes = 0;
+    size_t lds_bytes = 0, merge_lds_bytes = 0;
     int q_stride = 0, v_stride = 0;
 };
 
@@ -339,13 +391,12 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     a.xcd_map = (a.nsp % 8 == 0) ? 1 : 0;
     a.q_stride = static_cast<int>(dqk) + 8;
     a.v_stride = static_cast<int>(dv) + 8;
-    a.lds_bytes = std::max(size_t(kAHeads * a.q_stride + kAHeads * (kAChunk + 8) + 32 * a.v_stride) * 2,
-                           size_t(kAHeads) * a.nsp * 4);
-    if (a.lds_bytes > 64 * 1024) return NMM_ERR_SHAPE;
-    if (a.nsp > 1 && a.n_hb <= kMaxTickets)
-        a.ws_bytes = size_t(kTicketBytes) + size_t(a.n_hb) * a.nsp * kAHeads * (size_t(dv) + 2) * 4;
-    else if (a.nsp > 1)
-        return NMM_ERR_SHAPE;
+    a.lds_bytes = size_t(kAHeads * a.q_stride + kAHeads * (kAChunk + 8) + 32 * a.v_stride) * 2;
+    a.merge_lds_bytes = size_t(kAHeads) * a.nsp * 3 * 4;
+    if (a.lds_bytes > 64 * 1024 || a.merge_lds_bytes > 64 * 1024) return NMM_ERR_SHAPE;
+    // partial results live past the workspace's counter block (which GEMV calls sharing the
+    // workspace rely on being zero)
+    if (a.nsp > 1) a.ws_bytes = size_t(kTicketBytes) + size_t(a.n_hb) * a.nsp * kAHeads * (size_t(dv) + 2) * 4;
     *out = a;
     return NMM_OK;
 }
@@ -389,7 +440,6 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
     p.out = out;
     p.ldo = ldo;
     if (a.ws_bytes) {
-        p.tickets = static_cast<unsigned*>(workspace);
         p.part_o = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes);
         p.part_ml = p.part_o + size_t(a.n_hb) * a.nsp * kAHeads * d_v;
     }
@@ -406,9 +456,25 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
     p.q_stride = a.q_stride;
     p.v_stride = a.v_stride;
     const int64_t grid = int64_t(a.n_hb) * a.nsp;
-    hipLaunchKernelGGL(attention_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kAThreads), a.lds_bytes,
-                       static_cast<hipStream_t>(stream), p);
-    return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // K fragments per lane (d_qk / 32, up to 32) and V pieces per thread per half chunk
+    const int ks = static_cast<int>(d_qk / 32);
+    const int vp = static_cast<int>((32 * (d_v / 8) + kAThreads - 1) / kAThreads);
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(static_cast<uint32_t>(grid)), dim3(kAThreads), a.lds_bytes, s, p);
+    };
+    const int qp = static_cast<int>((kAHeads * (d_qk / 8) + kAThreads - 1) / kAThreads);
+    if (ks <= 18 && vp <= 8 && qp <= 5) go(attention_kernel<18, 8, 5>);
+    else if (ks <= 32 && vp <= 8 && qp <= 8) go(attention_kernel<32, 8, 8>);
+    else return NMM_ERR_SHAPE;
+    if (hipGetLastError() != hipSuccess) return NMM_ERR_HIP;
+    if (a.nsp > 1) {
+        const int n_cb = static_cast<int>((d_v + kMergeCols - 1) / kMergeCols);
+        hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(a.n_hb * n_cb)), dim3(kAThreads),
+                           a.merge_lds_bytes, s, p);
+        if (hipGetLastError() != hipSuccess) return NMM_ERR_HIP;
+    }
+    return NMM_OK;
 }
 
 }  // extern "C"

@@ -24,6 +24,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <cstdlib>
 
 #include "nmm_internal.h"
 
@@ -160,19 +161,30 @@ __device__ __forceinline__ uint16_t to_bf16_bits(float v) {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
 }
 
+// Cache policy of x loads inside the fused chain: device-coherent (sc1), because x was written
+// by other workgroups of the same launch and this XCD's L2 may hold older copies.
+constexpr int kLoadCoherent = 16;
+
+// y[m, n] (fp32) and its optional bf16 copy.  Inside the fused chain the bf16 copy is the next
+// MatMul's operand, read by other workgroups during the same launch, so it is written with a
+// device-scope atomic store (coherent at memory).
+template <bool CHAIN>
 __device__ __forceinline__ void store_out(const KParams& p, int64_t b, int m, int n, float v) {
     p.y[b * p.sy + int64_t(m) * p.ldy + n] = v;
     if (p.ybf) {
         const int64_t g = n / p.ybf_group, r = n - g * p.ybf_group;
-        if (r < p.ybf_keep)
-            p.ybf[b * p.ybf_sb + int64_t(m) * p.ybf_ldm + g * p.ybf_keep + r] = to_bf16_bits(v);
+        if (r < p.ybf_keep) {
+            uint16_t* dst = p.ybf + b * p.ybf_sb + int64_t(m) * p.ybf_ldm + g * p.ybf_keep + r;
+            if constexpr (CHAIN) __hip_atomic_store(dst, to_bf16_bits(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            else *dst = to_bf16_bits(v);
+        }
     }
 }
 
 // Stage x[m0:m0+MT, k0:k0+rows] into LDS as fp32, layout [row][m], zero outside M x K.  Each
 // thread fetches 16-byte chunks of x rows (8 consecutive k); every chunk load is issued before
 // any is used, and chunks past x's extent read as zeros.
-template <int DT, int MT>
+template <int DT, int MT, int AUX>
 __device__ __forceinline__ void stage_x(float* __restrict__ lds, const KParams& p, int64_t b, int m0,
                                         int k0, int rows, int tid) {
     const int cpr = rows / 8;                       // chunks per x row of the slice
@@ -189,7 +201,7 @@ __device__ __forceinline__ void stage_x(float* __restrict__ lds, const KParams& 
         const int m = i / cpr, q = i - m * cpr;
         const bool ok = i < total && m < mrows;
         const uint32_t off = ok ? uint32_t(((int64_t(m0) + m) * p.ldx + k0 + 8 * q) * 2) : kOutOfRange;
-        v[j] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+        v[j] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, AUX);
     }
 #pragma unroll
     for (int j = 0; j < kMaxPer; ++j) {
@@ -206,16 +218,48 @@ __device__ __forceinline__ void stage_x(float* __restrict__ lds, const KParams& 
     }
 }
 
-template <int DT, int MT, int U>
-__global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
-    extern __shared__ float lds[];
-    __shared__ int s_last;
+// The fused chain's cross-workgroup dependency: the items of a MatMul may only read its x once
+// the previous MatMul has finished all of its panels.
+struct Dep {
+    unsigned* wait_on = nullptr;   // completed-panel counter of the producing MatMul (or null)
+    unsigned target = 0;           // its panel count
+    unsigned* done = nullptr;      // this MatMul's completed-panel counter
+    unsigned* error = nullptr;     // set when a wait gives up
+    int spin_limit = 0;
+    int sleep_reps = 1;            // s_sleep(2) repetitions between polls
+};
 
+// Wait until *d.wait_on reaches d.target.  Bounded: after spin_limit polls the wait gives up
+// and raises the error flag, so a broken dependency can never hang the GPU.
+__device__ __forceinline__ void wait_dependency(const Dep& d) {
+    if (threadIdx.x == 0) {
+        int spins = 0;
+        while (__hip_atomic_load(d.wait_on, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < d.target) {
+            if (++spins > d.spin_limit) {
+                __hip_atomic_store(d.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            for (int r = 0; r < d.sleep_reps; ++r) __builtin_amdgcn_s_sleep(2);
+        }
+    }
+    __syncthreads();
+}
+
+// Count one more completed panel, after every thread's output stores have completed.
+__device__ __forceinline__ void signal_done(const Dep& d) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) __hip_atomic_fetch_add(d.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One work item: one K-slice of one panel of one (batch entry, row block).  `bid` is the item's
+// index within its MatMul.  CHAIN adds the fused chain's dependency wait and completion signal.
+template <int DT, int MT, int U, bool CHAIN>
+__device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float* lds, int* s_last, const Dep& dep) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
 
-    const uint32_t bid = blockIdx.x;              // grids stay below 2^31 workgroups
     const int item = static_cast<int>(bid % uint32_t(p.items));
     const uint32_t bm = bid / uint32_t(p.items);
     const int mb = static_cast<int>(bm % uint32_t(p.mblocks));
@@ -247,7 +291,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
     const int chunk0 = panel << p.full_lg;  // first 8-column chunk of the panel
     const bool guard = k0 + rows > p.K;     // only the last K-slice reaches past K
 
-    // ---- init: issue the first U loads of W, then stage x while they are in flight
+    // ---- init: issue the first U loads of W (they do not depend on x), then stage x
     Stream st;
     {
         const int cc = c < valid ? c : valid - 1;   // lanes past a ragged edge re-read its last chunk
@@ -261,7 +305,16 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
     i32x4 buf[U];
     if (guard) prefetch<U, true>(buf, st);
     else prefetch<U, false>(buf, st);
-    stage_x<DT, MT>(lds, p, b, m0, k0, rows, tid);
+    if constexpr (CHAIN) {
+        if (dep.wait_on) {
+            wait_dependency(dep);
+            stage_x<DT, MT, kLoadCoherent>(lds, p, b, m0, k0, rows, tid);
+        } else {
+            stage_x<DT, MT, 0>(lds, p, b, m0, k0, rows, tid);
+        }
+    } else {
+        stage_x<DT, MT, 0>(lds, p, b, m0, k0, rows, tid);
+    }
     __syncthreads();
 
     // ---- compute: stream this workgroup's rows of the panel
@@ -299,7 +352,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
             const int m = g + mm;
             const int n = chunk0 * 8 + col;
             if (ks == 1) {
-                if (m0 + m < p.M && n < p.N) store_out(p, b, m0 + m, n, s);
+                if (m0 + m < p.M && n < p.N) store_out<CHAIN>(p, b, m0 + m, n, s);
             } else {
                 __hip_atomic_store(p.part + pbase + int64_t(slice) * (MT * kPanelCols) + m * kPanelCols + col,
                                    s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -307,7 +360,10 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
         }
         __syncthreads();
     }
-    if (ks == 1) return;
+    if (ks == 1) {
+        if constexpr (CHAIN) signal_done(dep);
+        return;
+    }
 
     // ---- gather, part 2: the last workgroup of this panel sums the K-slices in order.
     // The partial sums above were written with device-scope atomic stores, which the GPU makes
@@ -322,10 +378,10 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
         const unsigned prev = __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         const int last = prev == unsigned(ks - 1);
         if (last) __hip_atomic_store(t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = last;
+        *s_last = last;
     }
     __syncthreads();
-    if (!s_last) return;
+    if (!*s_last) return;
     constexpr int kBatch = 8;     // partial-sum loads in flight per output
     for (int o = tid; o < MT * pcols; o += kThreads) {
         const int m = o / pcols, col = o - m * pcols;
@@ -345,7 +401,74 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
         }
         for (; q < ks; ++q)
             s += __hip_atomic_load(src + int64_t(q) * (MT * kPanelCols), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        store_out(p, b, m0 + m, n, s);
+        store_out<CHAIN>(p, b, m0 + m, n, s);
+    }
+    if constexpr (CHAIN) signal_done(dep);
+}
+
+template <int DT, int MT, int U>
+__global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    gemv_item<DT, MT, U, false>(p, blockIdx.x, lds, &s_last, Dep{});
+}
+
+// ---------------------------------------------------------------------------------------------
+// The fused decode chain: one persistent launch runs the MatMuls of the chain back to back.
+// The work items of all MatMuls form one ordered list (every item of MatMul s precedes every
+// item of MatMul s+1); workgroup w takes items w, w + G, w + 2G, ... in that order.  An item of
+// MatMul s+1 issues its first W loads at once and only then waits for MatMul s to have
+// completed all of its panels, so the next weight stream starts while the previous MatMul's
+// last panels are still being gathered -- the paper's point of starting independent work
+// earlier, here between consecutive narrow MatMuls.  (A shared claim counter would serialise
+// thousands of same-address atomics; the static order costs none.)
+//
+// Progress: a workgroup finishes all of its items of MatMul s before it waits on MatMul s, and
+// it only ever waits on items placed earlier in the list.  So the waits always end once all G
+// workgroups are resident; the launch uses at most one workgroup per compute unit so that they
+// are, even beside the attention kernel on the other stream.  Every wait is also bounded
+// (Dep::spin_limit): if it ever gave up, the error flag is raised instead of the GPU hanging.
+// Every workgroup leaves after its last item; the last one out resets the counters.
+// ---------------------------------------------------------------------------------------------
+constexpr int kChainMax = 5;
+
+struct ChainArgs {
+    KParams step[kChainMax];
+    int first_item[kChainMax + 1];   // list position of each MatMul's first item
+    unsigned panels[kChainMax];      // panels (all batch entries and row blocks) of each MatMul
+    unsigned* sync;                  // [1] exited workgroups, [2] error, [3 + s] done of MatMul s
+    int n_steps;
+    int spin_limit;
+    int sleep_reps;
+};
+
+__global__ __launch_bounds__(kThreads) void chain_kernel(const ChainArgs a) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    unsigned* sync = a.sync;
+    const int total = a.first_item[a.n_steps];
+    int st = 0;
+    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+        while (st + 1 < a.n_steps && item >= a.first_item[st + 1]) ++st;
+        Dep dep;
+        dep.wait_on = st ? sync + 3 + (st - 1) : nullptr;
+        dep.target = st ? a.panels[st - 1] : 0;
+        dep.done = sync + 3 + st;
+        dep.error = sync + 2;
+        dep.spin_limit = a.spin_limit;
+        dep.sleep_reps = a.sleep_reps;
+        gemv_item<NMM_BF16, 1, 4, true>(a.step[st], item - a.first_item[st], lds, &s_last, dep);
+        __syncthreads();   // LDS is reused by the next item
+    }
+    // leave: the last workgroup out resets the completion counters for the next launch
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_s_waitcnt(0);
+        const unsigned prev = __hip_atomic_fetch_add(sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev == gridDim.x - 1) {
+            for (int i = 0; i < a.n_steps; ++i)
+                __hip_atomic_store(sync + 3 + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(sync + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
     }
 }
 
@@ -411,17 +534,9 @@ nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream) {
     return last_launch_status();
 }
 
-nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream) {
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (a.batch == 0 || a.M == 0 || a.N == 0) return NMM_OK;
-    if (a.K == 0) {
-        const int64_t total = a.batch * a.M * a.N;
-        const int64_t blocks = std::min<int64_t>(4096, (total + 255) / 256);
-        hipLaunchKernelGGL(zero_output_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, s, a.y,
-                           a.ldy, a.sy, static_cast<uint16_t*>(a.ybf), a.ybf_group, a.ybf_keep,
-                           a.ybf_ldm, a.ybf_sb, a.M, a.N, a.batch);
-        return last_launch_status();
-    }
+namespace {
+
+KParams make_params(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part) {
     KParams kp{};
     kp.x = static_cast<const uint16_t*>(a.x);
     kp.ldx = a.ldx;
@@ -458,11 +573,65 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
         kp.tickets = tickets;
         kp.part = part;
     }
+    return kp;
+}
+
+size_t gemv_lds_bytes(const GemvPlan& p) {
     const int rows_max = std::max(p.rows_full, p.rows_tail);
     const int mg = p.mt < 4 ? p.mt : 4;
-    const size_t lds = std::max<size_t>(size_t(rows_max) * p.mt * 4, size_t(mg) * kThreads * 8 * 4);
+    return std::max<size_t>(size_t(rows_max) * p.mt * 4, size_t(mg) * kThreads * 8 * 4);
+}
+
+}  // namespace
+
+nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (a.batch == 0 || a.M == 0 || a.N == 0) return NMM_OK;
+    if (a.K == 0) {
+        const int64_t total = a.batch * a.M * a.N;
+        const int64_t blocks = std::min<int64_t>(4096, (total + 255) / 256);
+        hipLaunchKernelGGL(zero_output_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, s, a.y,
+                           a.ldy, a.sy, static_cast<uint16_t*>(a.ybf), a.ybf_group, a.ybf_keep,
+                           a.ybf_ldm, a.ybf_sb, a.M, a.N, a.batch);
+        return last_launch_status();
+    }
+    const KParams kp = make_params(a, p, tickets, part);
+    const size_t lds = gemv_lds_bytes(p);
     if (a.dt == NMM_BF16) launch_m<NMM_BF16>(kp, p.grid, lds, p.mt, p.unroll, s);
     else launch_m<NMM_F16>(kp, p.grid, lds, p.mt, p.unroll, s);
+    return last_launch_status();
+}
+
+bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n) {
+    if (n < 1 || n > kChainMax) return false;
+    for (int i = 0; i < n; ++i)
+        if (a[i].dt != NMM_BF16 || a[i].M != 1 || a[i].K == 0 || a[i].N == 0 || a[i].batch == 0 ||
+            p[i].mt != 1 || p[i].unroll != 4)
+            return false;
+    return true;
+}
+
+nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* const* tickets,
+                        float* const* part, int grid, void* stream) {
+    ChainArgs ca{};
+    ca.n_steps = n;
+    ca.sync = sync;
+    ca.spin_limit = 1 << 22;   // ~ a second of polling: far beyond any legitimate wait
+    ca.sleep_reps = 1;
+    if (const char* e = std::getenv("NMM_CHAIN_SLEEP")) ca.sleep_reps = std::max(1, std::atoi(e));
+    size_t lds = 0;
+    int first = 0;
+    for (int i = 0; i < n; ++i) {
+        ca.step[i] = make_params(a[i], p[i], tickets[i], part[i]);
+        ca.first_item[i] = first;
+        first += static_cast<int>(p[i].grid);
+        ca.panels[i] = static_cast<unsigned>(a[i].batch * p[i].mblocks * (p[i].n_full + (p[i].tail_chunks ? 1 : 0)));
+        lds = std::max(lds, gemv_lds_bytes(p[i]));
+    }
+    ca.first_item[n] = first;
+    grid = std::max(1, std::min(grid, first));
+    hipLaunchKernelGGL(chain_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds,
+                       static_cast<hipStream_t>(stream), ca);
     return last_launch_status();
 }
 

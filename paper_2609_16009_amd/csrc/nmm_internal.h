@@ -77,4 +77,12 @@ nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
 nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
 
+// The fused decode chain: n (<= 5) M = 1 bf16 GEMVs in one persistent launch.  `sync` points to
+// the chain's words in the counter block: [1] exited workgroups, [2] error flag (sticky),
+// [3 + i] completed panels of MatMul i; [1] and [3..] are zero before and after a launch.
+constexpr int kChainSyncWords = 8;
+bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n);
+nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* const* tickets,
+                        float* const* part, int grid, void* stream);
+
 }  // namespace nmm

@@ -4,9 +4,8 @@
 // The partition plays the role of Algorithm 2's init stage (Section IV-F), which splits a
 // [K, N] weight into kParts K-slices x fractalNum 16-column fractals and spreads them evenly over
 // at most 2P vector units.  Here the unit of work is a K-slice of a column panel (64 to 512
-// columns; one 16-byte chunk per lane per row).  Panels are narrowed until the grid can hold
-// about `target` equally sized workgroups with at most `ks_cap` K-slices per panel -- enough to
-// keep every compute unit streaming while the split-K gather stays short.
+// columns; one 16-byte chunk per lane per row).  Panel width and K-split count follow rules
+// fitted to measurements on MI355X over the decode shapes (see the comments below).
 #include <algorithm>
 #include <cstdlib>
 
@@ -89,26 +88,27 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     q.path = NMM_PATH_GEMV;
     q.mt = m_tile_for(M);
     q.mblocks = static_cast<int>(std::max<int64_t>(1, cdiv(M, q.mt)));
-    q.unroll = static_cast<int>(env_int("NMM_GEMV_UNROLL", q.mt >= 8 ? 4 : 8));
+    q.unroll = static_cast<int>(env_int("NMM_GEMV_UNROLL", 4));   // 4 in flight per wave: measured best
     if (q.unroll != 2 && q.unroll != 4 && q.unroll != 8) q.unroll = 8;
     const int U = q.unroll;
 
     const int64_t chunks = cdiv(N, 8);
     const int64_t mats = std::max<int64_t>(batch, 1) * q.mblocks;
-    // Workgroups wanted: about one per 96 KB of W, between 128 and `target` (measured on MI355X:
-    // fewer leave HBM idle, more only add split-K gather work).
-    const int64_t w_bytes = mats * K * chunks * 16;
-    const int64_t target = env_int("NMM_GEMV_TARGET", 1024);
-    const int64_t want = std::max<int64_t>(std::min<int64_t>(128, target), std::min<int64_t>(target, w_bytes / (96 << 10)));
-    // K-slices per panel: fewer for tall row tiles, whose partial sums are MT times larger
-    const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", q.mt >= 8 ? 8 : 16);
-    int min_cw = static_cast<int>(env_int("NMM_GEMV_MINCW", 8));  // narrowest full panel
+    // Panel width (measured on MI355X over the decode shapes): as wide as possible, up to 32
+    // chunks (64 for 16-row tiles), while the launch still has >= 24 panels in total and every
+    // row is split into >= 2 panels; never narrower than 8 chunks (128-byte row segments).
+    int min_cw = static_cast<int>(env_int("NMM_GEMV_MINCW", 8));
     if (min_cw > kPanelChunks || (min_cw & (min_cw - 1))) min_cw = 8;
-    // Start at 256-column panels (512 for 16-row tiles, whose loop is compute-heavier) and
-    // narrow them until the panels x K-slices can reach half the wanted grid.
     int cw = static_cast<int>(env_int("NMM_GEMV_MAXCW", q.mt >= 16 ? 64 : 32));
     if (cw > kPanelChunks || (cw & (cw - 1)) || cw < min_cw) cw = std::max(min_cw, 32);
-    while (cw > min_cw && mats * cdiv(chunks, cw) * ks_cap * 2 < want) cw /= 2;
+    while (cw > min_cw && (mats * cdiv(chunks, cw) < 24 || chunks < 2 * cw)) cw /= 2;
+    // Workgroups wanted: one per ~100 KB of W, between 256 and 768 (fewer leave HBM idle; more
+    // only add split-K gather work).
+    const int64_t w_bytes = mats * K * chunks * 16;
+    const int64_t want = env_int("NMM_GEMV_TARGET", std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
+    // K-slices per panel: the power of two nearest want / panels, capped (fewer for tall row
+    // tiles, whose partial sums are MT times larger)
+    const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", q.mt >= 8 ? 8 : 16);
     q.cw_full = cw;
     q.n_full = static_cast<int>(chunks / cw);
     q.tail_chunks = static_cast<int>(chunks % cw);
@@ -130,14 +130,19 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     const int64_t rstep_tail = q.tail_chunks ? int64_t(kWaves) * (kPanelChunks / q.tail_cw) : 1;
     const int64_t steps_per_matrix = q.n_full * cdiv(K, rstep_full) +
                                      (q.tail_chunks ? cdiv(K, rstep_tail) : 0);
-    const int64_t total_steps = mats * steps_per_matrix;
-    const int64_t spi = std::max<int64_t>(U, cdiv(total_steps, want));       // WG steps per item
+    (void)steps_per_matrix;
+    const int64_t panels_all = mats * (q.n_full + (q.tail_chunks ? 1 : 0));
+    int64_t ks_want = 1;
+    {
+        const double ratio = double(want) / double(std::max<int64_t>(panels_all, 1));
+        while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;   // nearest power of two
+        ks_want = std::min(ks_want, ks_cap);
+    }
 
     auto slice = [&](int64_t rstep, int& ks, int& rows) {
         const int64_t unit = rstep * U;
         const int64_t cap = std::max<int64_t>(unit, (kXStageBytes / (4 * q.mt * rstep)) / U * unit);
-        int64_t r = std::max<int64_t>(spi * rstep, cdiv(K, ks_cap));           // rows per slice
-        r = std::min<int64_t>(std::min<int64_t>(rup(r, unit), cap), rup(K, unit));
+        int64_t r = std::min<int64_t>(std::min<int64_t>(rup(cdiv(K, ks_want), unit), cap), rup(K, unit));
         int64_t k = cdiv(K, r);
         r = std::min<int64_t>(cap, rup(cdiv(K, k), unit));   // rebalance the slices
         k = cdiv(K, r);

@@ -136,7 +136,7 @@ def test_plan_covers_w_exactly_once(M, K, N, batch):
             continue
         assert width >= 1 and (width & (width - 1)) == 0
         rstep = waves * 64 // width
-        assert rows % rstep == 0                          # whole row-steps per K-slice
+        assert rows % (rstep * p["unroll"]) == 0          # whole unrolled row-steps per K-slice
         assert ks * rows >= K and (ks - 1) * rows < K     # slices tile K, none empty
         assert rows * p["m_tile"] * 4 <= 32 * 1024         # staged x slice fits its LDS budget
     if p["tail_chunks"]:

@@ -197,3 +197,25 @@ def test_workspace_garbage_past_counter_block_is_harmless():
     assert_parity(y, y_ref, a_ref, what="gemv on a dirty workspace")
     ref_att, ref_abs = oracle.latent_attention(q, kv, scale)
     assert_parity(att, ref_att, ref_abs, what="attention on a dirty workspace")
+
+
+def test_fused_chain_matches_separate_launches_and_resets(monkeypatch):
+    # NMM_CHAIN_FUSED=1 runs the chain as one persistent launch; by default it is one launch per
+    # MatMul.  Both use the same plans and summation order, so they must agree bit for bit.
+    step = syn.decode_step()
+    ws = nmm.Workspace()
+    monkeypatch.setenv("NMM_CHAIN_FUSED", "1")
+    fused = alloc_chain(step)
+    for _ in range(20):                      # repeated launches: the queue and counters reset
+        run_chain(step, fused, workspace=ws)
+    torch.cuda.synchronize()
+    sync_words = ws.buf[:32].view(torch.int32).cpu()
+    assert int(sync_words[2]) == 0, "a dependency wait gave up"
+    assert int(sync_words.abs().sum()) == 0, "queue / completion words must return to zero"
+    monkeypatch.setenv("NMM_CHAIN_FUSED", "0")
+    sep = alloc_chain(step)
+    run_chain(step, sep, workspace=ws)
+    torch.cuda.synchronize()
+    for k in nmm.CHAIN_BUFFERS[6:]:
+        assert torch.equal(fused[k], sep[k]), k
+    check_chain_stepwise(step, fused)

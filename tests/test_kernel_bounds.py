@@ -28,7 +28,7 @@ def check_launch(batch, M, K, N, ldx, ldw, ldy, sx=None, sw=None, sy=None):
     rows_max = max(p["rows_full"], p["rows_tail"])
     mg = min(mt, 4)
     lds_floats = max(rows_max * mt, mg * THREADS * 8)
-    unroll = 4 if mt >= 8 else 8
+    unroll = p["unroll"]
     tid = np.arange(THREADS)
     lane, wave = tid & 63, tid >> 6
     x_total = (batch - 1) * sx + (M - 1) * ldx + K       # elements a dense x needs
