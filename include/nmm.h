@@ -66,8 +66,9 @@ typedef enum {
 
 typedef enum { NMM_F16 = 1, NMM_BF16 = 2 } nmm_dtype;
 
-/* Which kernel family computes the product.  AUTO picks the streaming GEMV for M up to the
- * measured crossover and the MFMA (matrix-core) path above it; GEMV and MFMA force a family. */
+/* Which kernel family computes the product.  AUTO picks the streaming GEMV for M below the
+ * measured crossover and the MFMA (matrix-core) path from it on (single matrices; batched calls
+ * always stream); GEMV and MFMA force a family.  NMM_PATH_MFMA with batch > 1 is NMM_ERR_PATH. */
 typedef enum { NMM_PATH_AUTO = 0, NMM_PATH_GEMV = 1, NMM_PATH_MFMA = 2 } nmm_path;
 
 /*
@@ -80,7 +81,8 @@ typedef enum { NMM_PATH_AUTO = 0, NMM_PATH_GEMV = 1, NMM_PATH_MFMA = 2 } nmm_pat
  * per column, and the last workgroup to finish a panel gathers the K-slices in a fixed order
  * and writes y.
  *
- *   M, K, N     sizes (>= 0).  The GEMV path takes any M (in blocks of 16 rows).
+ *   M, K, N     sizes (>= 0).  The GEMV path takes any M (in blocks of 16 rows); the MFMA path
+ *               takes any M (in blocks of 32) for single matrices.
  *   dt          NMM_F16 or NMM_BF16, the type of both x and W.
  *   x, ldx      device pointer and leading dimension (elements, >= K, multiple of 8).
  *   W, ldw      device pointer and leading dimension (elements, >= N, multiple of 8).

@@ -40,6 +40,7 @@ nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, v
     }
     unsigned* tickets = static_cast<unsigned*>(ws);
     float* part = ws ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kTicketBytes) : nullptr;
+    if (p.path == NMM_PATH_MFMA && a.K > 0) return launch_mfma(a, p, tickets, part, stream);
     return launch_gemv(a, p, tickets, part, stream);
 }
 

@@ -382,26 +382,42 @@ __device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float*
     }
     __syncthreads();
     if (!*s_last) return;
-    constexpr int kBatch = 8;     // partial-sum loads in flight per output
-    for (int o = tid; o < MT * pcols; o += kThreads) {
-        const int m = o / pcols, col = o - m * pcols;
-        const int n = chunk0 * 8 + col;
-        if (m0 + m >= p.M || n >= p.N) continue;
-        float* src = p.part + pbase + m * kPanelCols + col;
-        float s = 0.f;
-        int q = 0;
-        for (; q + kBatch <= ks; q += kBatch) {
-            float v[kBatch];
+    // every output of the panel sums its slices in slice order; the loads of R outputs x QB
+    // slices are all in flight before any is added
+    constexpr int R = (MT * 2 < 8) ? MT * 2 : 8;   // outputs per thread per pass (pcols <= 512)
+    constexpr int QB = 32 / R;                      // slices per batch
+    const int n_out = MT * pcols;
+    for (int o0 = tid; o0 < n_out; o0 += R * kThreads) {
+        float sum[R];
 #pragma unroll
-            for (int j = 0; j < kBatch; ++j)
-                v[j] = __hip_atomic_load(src + int64_t(q + j) * (MT * kPanelCols), __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT);
+        for (int r = 0; r < R; ++r) sum[r] = 0.f;
+        for (int q0 = 0; q0 < ks; q0 += QB) {
+            float v[R][QB];
 #pragma unroll
-            for (int j = 0; j < kBatch; ++j) s += v[j];
+            for (int r = 0; r < R; ++r) {
+                const int o = o0 + r * kThreads;
+                const int m = o / pcols, col = o - m * pcols;
+                const float* src = p.part + pbase + m * kPanelCols + col;
+#pragma unroll
+                for (int u = 0; u < QB; ++u)
+                    v[r][u] = (o < n_out && q0 + u < ks)
+                                  ? __hip_atomic_load(src + int64_t(q0 + u) * (MT * kPanelCols), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                  : 0.f;
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < QB; ++u)
+                    if (q0 + u < ks) sum[r] += v[r][u];
         }
-        for (; q < ks; ++q)
-            s += __hip_atomic_load(src + int64_t(q) * (MT * kPanelCols), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        store_out<CHAIN>(p, b, m0 + m, n, s);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int o = o0 + r * kThreads;
+            const int m = o / pcols, col = o - m * pcols;
+            const int n = chunk0 * 8 + col;
+            if (o < n_out && m0 + m < p.M && n < p.N) store_out<CHAIN>(p, b, m0 + m, n, sum[r]);
+        }
     }
     if constexpr (CHAIN) signal_done(dep);
 }

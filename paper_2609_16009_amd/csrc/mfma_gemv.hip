@@ -1,0 +1,291 @@
+// Narrow MatMul on the matrix cores for larger M (gfx950): y[M,N] = x[M,K] . W[K,N] with M in
+// tiles of 16 or 32 rows, W row-major [K,N] (bf16 or fp16), fp32 accumulation.
+//
+// Once x has enough rows the streaming GEMV runs out of vector ALU (it spends 2*M flops per
+// weight element against HBM's ~1 byte per element), while the product stays HBM-bound for
+// the matrix cores far beyond M = 32.  The paper's narrow-dimension conditions (Condition 2,
+// Section III-A; Conditions 4-5, Section V) are about where the split between the two units
+// lies; on MI355X it is measured, and nmm_gemv's AUTO path switches here above it.
+//
+//  * A workgroup (4 waves) owns one 128-column panel of W and one K-slice.  It stages its x
+//    rows (bf16/fp16, row-major, the MFMA A operand) in LDS once.
+//  * W streams in stages of 64 rows x 128 columns (16 KB): each thread loads four 16-byte chunks
+//    one stage ahead, stores them to a double-buffered LDS tile, and the waves read their
+//    v_mfma_f32_16x16x32 B operands back with ds_read_b64_tr_b16, the gfx950 transposing LDS
+//    read (the B operand needs 8 consecutive k of one column; W rows hold consecutive columns).
+//  * Wave w owns the column tiles 2w and 2w+1 of the panel, so no cross-wave reduction is needed.
+//  * K-slices are combined exactly like the GEMV's: device-scope atomic partial stores, a
+//    ticket per panel, and the last workgroup sums the slices in order.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+
+#include "nmm_internal.h"
+
+namespace nmm {
+namespace {
+
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __fp16 fp16x4 __attribute__((__vector_size__(4 * sizeof(__fp16))));
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) fp16x4 lds_f16x4;
+
+constexpr int kRsrcWord3 = 0x00020000;
+constexpr int kLoadNT = 2;
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kWStride = kMfmaPanelCols + 8;   // LDS row stride of a W stage (elements)
+
+struct MParams {
+    const uint16_t* x;
+    int64_t ldx;
+    const uint16_t* w;
+    float* y;
+    int64_t ldy;
+    float* part;
+    unsigned* tickets;
+    int M, K, N;
+    uint32_t row_bytes, w_extent;
+    int panels, ks, rows, items, mblocks;
+    int x_stride;   // LDS row stride of the staged x (elements)
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+template <int DT>
+__device__ __forceinline__ f32x4 mfma(i32x4 a, i32x4 b, f32x4 c) {
+    if constexpr (DT == NMM_BF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// B operand of one 16-column tile for 32 k-rows starting at `row0` of the LDS stage: lane
+// (g = lane/16, j = lane%16) receives W[row0 + 8g .. + 7][col0 + j] via two transposing reads.
+template <int DT>
+__device__ __forceinline__ i32x4 load_b(const uint16_t* wst, int row0, int col0, int g, int j) {
+    const uint16_t* base = wst + (row0 + 8 * g + (j >> 2)) * kWStride + col0 + 4 * (j & 3);
+    uint2 lo, hi;
+    if constexpr (DT == NMM_BF16) {
+        lo = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base)));
+        hi = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + 4 * kWStride)));
+    } else {
+        lo = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4f16((lds_f16x4*)(base)));
+        hi = __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4f16((lds_f16x4*)(base + 4 * kWStride)));
+    }
+    return i32x4{int(lo.x), int(lo.y), int(hi.x), int(hi.y)};
+}
+
+template <int DT, int MT>
+__global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    __shared__ int s_last;
+    constexpr int MTILES = MT / 16;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int g = lane >> 4, j = lane & 15;
+
+    const uint32_t bid = blockIdx.x;
+    const int item = static_cast<int>(bid % uint32_t(p.items));
+    const int mb = static_cast<int>(bid / uint32_t(p.items));
+    const int panel = item / p.ks, slice = item - panel * p.ks;
+    const int m0 = mb * MT, k0 = slice * p.rows, n0 = panel * kMfmaPanelCols;
+    const int stages = p.rows / kMfmaStageRows;
+
+    uint16_t* x_lds = smem;                                   // [MT][x_stride]
+    uint16_t* w_lds = smem + MT * p.x_stride;                 // 2 x [64][kWStride]
+
+    // ---- W stage loads: thread t takes chunk t%16 of rows t/16 + 16q (q < 4)
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(p.w, p.w_extent);
+    const int wc = tid & 15, wr0 = tid >> 4;
+    const int chunks_valid = min(16, (p.N - n0 + 7) / 8);
+    auto w_off = [&](int stage, int q) -> uint32_t {
+        const int row = k0 + stage * kMfmaStageRows + wr0 + 16 * q;
+        return (row < p.K && wc < chunks_valid) ? uint32_t(row) * p.row_bytes + uint32_t(n0 / 8 + wc) * 16u : kOutOfRange;
+    };
+    i32x4 wreg[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) wreg[q] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off(0, q), 0, kLoadNT);
+
+    // ---- x rows m0.. (zero past M or K), staged once as the A operand; every load is issued
+    // before any is used
+    {
+        const int cpr = p.rows / 8;
+        const int mrows = min(MT, p.M - m0);
+        const __amdgpu_buffer_rsrc_t xr =
+            make_rsrc(p.x + int64_t(m0) * p.ldx, uint32_t(((mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2));
+        constexpr int kPer = kMfmaXChunks / kThreads;    // x chunks per thread (upper bound)
+        i32x4 v[kPer];
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int i = tid + u * kThreads;
+            const int m = i / cpr, c = i - m * cpr, k = k0 + 8 * c;
+            const bool ok = i < MT * cpr && m < mrows && k < p.K;
+            v[u] = __builtin_amdgcn_raw_buffer_load_b128(xr, ok ? uint32_t((int64_t(m) * p.ldx + k) * 2) : kOutOfRange, 0, 0);
+        }
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int i = tid + u * kThreads;
+            if (i < MT * cpr) {
+                const int m = i / cpr, c = i - m * cpr, k = k0 + 8 * c;
+                i32x4 val = v[u];
+                if (k + 8 > p.K) {   // zero the elements past K within the last chunk
+#pragma unroll
+                    for (int t = 0; t < 8; ++t)
+                        if (k + t >= p.K) val[t >> 1] &= (t & 1) ? 0x0000FFFF : 0xFFFF0000;
+                }
+                *reinterpret_cast<i32x4*>(x_lds + m * p.x_stride + 8 * c) = val;
+            }
+        }
+    }
+
+    f32x4 acc[MTILES][2];
+#pragma unroll
+    for (int mt = 0; mt < MTILES; ++mt)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int s = 0; s < stages; ++s) {
+        uint16_t* wst = w_lds + (s & 1) * (kMfmaStageRows * kWStride);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<i32x4*>(wst + (wr0 + 16 * q) * kWStride + 8 * wc) = wreg[q];
+        if (s + 1 < stages) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) wreg[q] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off(s + 1, q), 0, kLoadNT);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < kMfmaStageRows / 32; ++kk) {
+            const int kx = s * kMfmaStageRows + 32 * kk;   // k offset within the slice
+            i32x4 a[MTILES];
+#pragma unroll
+            for (int mt = 0; mt < MTILES; ++mt)
+                a[mt] = *reinterpret_cast<const i32x4*>(x_lds + (16 * mt + j) * p.x_stride + kx + 8 * g);
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const i32x4 b = load_b<DT>(wst, 32 * kk, 16 * (2 * wave + t), g, j);
+#pragma unroll
+                for (int mt = 0; mt < MTILES; ++mt) acc[mt][t] = mfma<DT>(a[mt], b, acc[mt][t]);
+            }
+        }
+    }
+
+    // ---- outputs: lane (g, j) holds rows 4g+i of its tiles, column j
+    const int64_t pbase = ((int64_t(mb) * p.panels + panel) * p.ks) * (int64_t(MT) * kMfmaPanelCols);
+    if (p.ks == 1) {
+#pragma unroll
+        for (int mt = 0; mt < MTILES; ++mt)
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int m = m0 + 16 * mt + 4 * g + i, n = n0 + 16 * (2 * wave + t) + j;
+                    if (m < p.M && n < p.N) p.y[int64_t(m) * p.ldy + n] = acc[mt][t][i];
+                }
+        return;
+    }
+#pragma unroll
+    for (int mt = 0; mt < MTILES; ++mt)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int r = 16 * mt + 4 * g + i, c = 16 * (2 * wave + t) + j;
+                __hip_atomic_store(p.part + pbase + int64_t(slice) * (MT * kMfmaPanelCols) + r * kMfmaPanelCols + c,
+                                   acc[mt][t][i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+    // same hand-off as the GEMV: completed device-scope stores, one ticket, ordered gather
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        unsigned* t = p.tickets + int64_t(mb) * p.panels + panel;
+        const unsigned prev = __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int last = prev == unsigned(p.ks - 1);
+        if (last) __hip_atomic_store(t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = last;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    // every output of the panel sums its slices in slice order; the loads of PER outputs x QB
+    // slices are all in flight before any is added
+    constexpr int PER = MT * kMfmaPanelCols / kThreads;   // outputs per thread (8 or 16)
+    constexpr int QB = 64 / PER;                            // slices per batch
+    float sum[PER];
+#pragma unroll
+    for (int r = 0; r < PER; ++r) sum[r] = 0.f;
+    for (int q0 = 0; q0 < p.ks; q0 += QB) {
+        float v[PER][QB];
+#pragma unroll
+        for (int r = 0; r < PER; ++r)
+#pragma unroll
+            for (int u = 0; u < QB; ++u) {
+                const int o = tid + r * kThreads;
+                v[r][u] = (q0 + u < p.ks)
+                              ? __hip_atomic_load(p.part + pbase + int64_t(q0 + u) * (MT * kMfmaPanelCols) + o,
+                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                              : 0.f;
+            }
+#pragma unroll
+        for (int r = 0; r < PER; ++r)
+#pragma unroll
+            for (int u = 0; u < QB; ++u)
+                if (q0 + u < p.ks) sum[r] += v[r][u];
+    }
+#pragma unroll
+    for (int r = 0; r < PER; ++r) {
+        const int o = tid + r * kThreads;
+        const int m = m0 + o / kMfmaPanelCols, n = n0 + o % kMfmaPanelCols;
+        if (m < p.M && n < p.N) p.y[int64_t(m) * p.ldy + n] = sum[r];
+    }
+}
+
+template <int DT, int MT>
+void launch_mt(const MParams& mp, int64_t grid, size_t lds, hipStream_t s) {
+    hipLaunchKernelGGL((mfma_gemv_kernel<DT, MT>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, mp);
+}
+
+}  // namespace
+
+size_t mfma_lds_bytes(const GemvPlan& p) {
+    return (size_t(p.mt) * (p.rows_full + 8) + 2 * kMfmaStageRows * kWStride) * 2;
+}
+
+nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream) {
+    MParams mp{};
+    mp.x = static_cast<const uint16_t*>(a.x);
+    mp.ldx = a.ldx;
+    mp.w = static_cast<const uint16_t*>(a.w);
+    mp.y = a.y;
+    mp.ldy = a.ldy;
+    mp.part = part;
+    mp.tickets = tickets;
+    mp.M = static_cast<int>(a.M);
+    mp.K = static_cast<int>(a.K);
+    mp.N = static_cast<int>(a.N);
+    mp.row_bytes = static_cast<uint32_t>(a.ldw * 2);
+    mp.w_extent = static_cast<uint32_t>(((a.K - 1) * a.ldw + (a.N + 7) / 8 * 8) * 2);
+    mp.panels = p.n_full;
+    mp.ks = p.ks_full;
+    mp.rows = p.rows_full;
+    mp.items = p.items;
+    mp.mblocks = p.mblocks;
+    mp.x_stride = p.rows_full + 8;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t lds = mfma_lds_bytes(p);
+    if (a.dt == NMM_BF16) {
+        if (p.mt == 16) launch_mt<NMM_BF16, 16>(mp, p.grid, lds, s);
+        else launch_mt<NMM_BF16, 32>(mp, p.grid, lds, s);
+    } else {
+        if (p.mt == 16) launch_mt<NMM_F16, 16>(mp, p.grid, lds, s);
+        else launch_mt<NMM_F16, 32>(mp, p.grid, lds, s);
+    }
+    return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
+}
+
+}  // namespace nmm

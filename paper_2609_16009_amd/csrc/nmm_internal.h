@@ -33,6 +33,12 @@ constexpr int kRedBytes = 32 * 1024;       // LDS for the cross-wave reduction
 constexpr int64_t kMaxTickets = 16384;
 constexpr int64_t kTicketBytes = kMaxTickets * 4;
 
+// Matrix-core path (mfma_gemv.hip): 128-column panels, W staged 64 rows at a time.
+constexpr int kMfmaPanelCols = 128;
+constexpr int kMfmaStageRows = 64;
+constexpr int kMfmaXChunks = 2048;         // staged x chunks per workgroup: MT * rows / 8 <= this
+constexpr int kMfmaMinMDefault = 4;        // AUTO uses the matrix cores from this many rows on
+
 struct GemvPlan {
     int path = NMM_PATH_GEMV;
     int mt = 1;            // M tile (1, 2, 4, 8, 16)
@@ -82,6 +88,8 @@ nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
 // [3 + i] completed panels of MatMul i; [1] and [3..] are zero before and after a launch.
 constexpr int kChainSyncWords = 8;
 bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n);
+nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
+size_t mfma_lds_bytes(const GemvPlan& p);
 nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* const* tickets,
                         float* const* part, int grid, void* stream);
 

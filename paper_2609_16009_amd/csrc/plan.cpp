@@ -75,6 +75,54 @@ nmm_status validate_gemv(const GemvArgs& a, int path) {
     return NMM_OK;
 }
 
+// The matrix-core partition: 128-column panels, K-slices of whole 64-row stages, x tiles of
+// 16 or 32 rows.  The split count follows the GEMV's rule (about one workgroup per 100 KB of W).
+nmm_status plan_mfma(int64_t M, int64_t K, int64_t N, GemvPlan* p) {
+    GemvPlan q;
+    q.path = NMM_PATH_MFMA;
+    q.mt = M <= 16 ? 16 : 32;
+    q.mblocks = static_cast<int>(std::max<int64_t>(1, cdiv(M, q.mt)));
+    q.unroll = 1;
+    q.cw_full = kMfmaPanelCols / 8;
+    q.n_full = static_cast<int>(cdiv(N, kMfmaPanelCols));
+    if (M == 0 || N == 0 || K == 0) {
+        *p = q;
+        return NMM_OK;
+    }
+    const int64_t panels = int64_t(q.mblocks) * q.n_full;
+    const int64_t w_bytes = int64_t(q.mblocks) * K * cdiv(N, 8) * 16;
+    const int64_t want = env_int("NMM_GEMV_TARGET", std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
+    const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", 16);
+    int64_t ks_want = 1;
+    const double ratio = double(want) / double(panels);
+    while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;
+    // rows whose x tile fits both the per-thread staging bound and, with the double-buffered W
+    // stage, 64 KB of LDS
+    const int64_t lds_rows = ((32768 - 2 * kMfmaStageRows * (kMfmaPanelCols + 8)) / q.mt - 8) / kMfmaStageRows * kMfmaStageRows;
+    const int64_t cap = std::min<int64_t>(kMfmaXChunks * 8 / q.mt, lds_rows);
+    int64_t r = std::min<int64_t>(rup(cdiv(K, ks_want), kMfmaStageRows), cap);
+    int64_t k = cdiv(K, r);
+    r = std::min<int64_t>(cap, rup(cdiv(K, k), kMfmaStageRows));
+    k = cdiv(K, r);
+    if (panels > kMaxTickets) {
+        if (rup(K, kMfmaStageRows) > cap) return NMM_ERR_SHAPE;
+        k = 1;
+        r = rup(K, kMfmaStageRows);
+    }
+    q.ks_full = static_cast<int>(k);
+    q.rows_full = static_cast<int>(r);
+    q.ks_max = q.ks_full;
+    q.items = q.n_full * q.ks_full;
+    q.grid = int64_t(q.mblocks) * q.items;
+    if (q.split()) {
+        q.n_tickets = panels;
+        q.part_floats = panels * q.ks_max * int64_t(q.mt) * kMfmaPanelCols;
+        q.ws_bytes = static_cast<size_t>(kTicketBytes + q.part_floats * 4);
+    }
+    *p = q;
+    return NMM_OK;
+}
+
 nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p) {
     if (!p) return NMM_ERR_NULL;
     if (dt != NMM_F16 && dt != NMM_BF16) return NMM_ERR_DTYPE;
@@ -82,9 +130,14 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     if (batch < 0 || M < 0 || K < 0 || N < 0 || M >= kLimit || K >= kLimit || N >= kLimit)
         return NMM_ERR_SHAPE;
     GemvPlan q;
-    // The matrix-core path is not available in this build of the planner: AUTO and MFMA both
-    // resolve to the streaming GEMV, which handles every M in blocks of 16 rows.
-    if (path == NMM_PATH_MFMA) return NMM_ERR_PATH;
+    // AUTO: the streaming GEMV up to the measured crossover, the matrix cores above it (single
+    // matrices only; batched calls always stream).
+    const int64_t mfma_min_m = env_int("NMM_MFMA_MIN_M", kMfmaMinMDefault);
+    if (path == NMM_PATH_AUTO) path = (batch <= 1 && M >= mfma_min_m) ? NMM_PATH_MFMA : NMM_PATH_GEMV;
+    if (path == NMM_PATH_MFMA) {
+        if (batch > 1) return NMM_ERR_PATH;
+        return plan_mfma(M, K, N, p);
+    }
     q.path = NMM_PATH_GEMV;
     q.mt = m_tile_for(M);
     q.mblocks = static_cast<int>(std::max<int64_t>(1, cdiv(M, q.mt)));

@@ -145,7 +145,7 @@ def test_plan_covers_w_exactly_once(M, K, N, batch):
     assert p["items"] == items and p["grid"] == batch * p["m_blocks"] * items
     split = max(p["split_k_full"], p["split_k_tail"]) > 1
     assert (p["workspace_bytes"] > 0) == split
-    assert nmm.nmm_batched_gemv_workspace_size(batch, M, K, N) == p["workspace_bytes"]
+    assert nmm.nmm_batched_gemv_workspace_size(batch, M, K, N, nmm.NMM_BF16, nmm.NMM_PATH_GEMV) == p["workspace_bytes"]
 
 
 def test_plan_rejects_unavailable_path_and_bad_dtype():

@@ -207,3 +207,33 @@ def test_batched_ragged(B, M, K, N):
     torch.cuda.synchronize()
     y_ref, a_ref = oracle.batched_gemv(x, W, syn.BF16)
     assert_parity(y, y_ref, a_ref, what=f"batched {B}x{M}x{K}x{N}")
+
+
+# ------------------------------------------------------------------ matrix-core path
+
+@pytest.mark.parametrize("M", [1, 4, 5, 8, 16, 17, 32])
+def test_uq_sweep_mfma_path(M):
+    check_case(syn.uq_sweep(min(M, 32)) if M <= 32 else None, path=nmm.NMM_PATH_MFMA)
+
+
+@pytest.mark.parametrize("M", [4, 32])
+def test_uq_sweep_mfma_integer_exact(M):
+    check_case(syn.uq_sweep(M, integer=True), path=nmm.NMM_PATH_MFMA)
+
+
+@pytest.mark.parametrize("M,K,N,dt,ldx,ldw", [(5, 1021, 1031, syn.BF16, 1024, 1032), (33, 4099, 520, syn.F16, 4104, 520),
+                                              (8, 100, 8, syn.BF16, 104, 8), (32, 20000, 300, syn.F16, 20000, 304),
+                                              (17, 16384, 7168, syn.BF16, 16384, 7168)])
+def test_mfma_ragged(M, K, N, dt, ldx, ldw):
+    c = syn.gemv_case(77 + M, M, K, N, dt, ldx=ldx, ldw=ldw, name=f"mfma_{M}x{K}x{N}")
+    check_case(c, path=nmm.NMM_PATH_MFMA)
+    ci = syn.gemv_case(78 + M, M, K, N, dt, integer=True, ldx=ldx, ldw=ldw, name=f"mfma_int_{M}x{K}x{N}")
+    check_case(ci, path=nmm.NMM_PATH_MFMA)
+
+
+def test_auto_path_switches_at_crossover():
+    for M in (1, 2, 3):
+        assert nmm.nmm_gemv_plan(M, 1536, 24576)["path"] == nmm.NMM_PATH_GEMV
+    for M in (4, 16, 32):
+        assert nmm.nmm_gemv_plan(M, 1536, 24576)["path"] == nmm.NMM_PATH_MFMA
+    assert nmm.nmm_gemv_plan(16, 128, 512, batch=8)["path"] == nmm.NMM_PATH_GEMV

@@ -101,3 +101,34 @@ def test_gemv_launch_stays_in_bounds(batch, M, K, N, ldx, ldw):
 def test_strided_query_slice_in_bounds():
     # x rows of 128 taken every 192 elements (q_nope inside [128, 192])
     check_launch(128, 1, 128, 512, ldx=128, ldw=512, ldy=512, sx=192)
+
+
+@pytest.mark.parametrize("M,K,N,ldx,ldw", [(1, 1536, 24576, 1536, 24576), (16, 1536, 24576, 1536, 24576),
+                                           (32, 1536, 24576, 1536, 24576), (5, 1021, 1031, 1024, 1032),
+                                           (33, 4099, 520, 4104, 520), (17, 16384, 7168, 16384, 7168),
+                                           (8, 100, 8, 104, 8), (32, 20000, 300, 20000, 304)])
+def test_mfma_launch_stays_in_bounds(M, K, N, ldx, ldw):
+    p = nmm.nmm_gemv_plan(M, K, N, nmm.NMM_BF16, nmm.NMM_PATH_MFMA)
+    mt, rows, ks, panels = p["m_tile"], p["rows_full"], p["split_k_full"], p["n_full_panels"]
+    assert mt in (16, 32) and rows % 64 == 0 and ks * rows >= K and (ks - 1) * rows < K
+    assert panels * 128 >= N and (panels - 1) * 128 < N
+    # LDS: x tile [mt][rows + 8] + two W stages [64][136], bf16
+    assert (mt * (rows + 8) + 2 * 64 * 136) * 2 <= 65536
+    assert mt * rows // 8 <= 2048
+    extent = ((K - 1) * ldw + (N + 7) // 8 * 8) * 2
+    tid = np.arange(256)
+    wc, wr0 = tid & 15, tid >> 4
+    for panel in {0, panels - 1}:
+        n0 = panel * 128
+        valid = min(16, (N - n0 + 7) // 8)
+        for sl in {0, ks - 1}:
+            k0 = sl * rows
+            for st in range(rows // 64):
+                for q in range(4):
+                    row = k0 + st * 64 + wr0 + 16 * q
+                    ok = (row < K) & (wc < valid)
+                    off = row * ldw * 2 + (n0 // 8 + wc) * 16
+                    assert np.all(off[ok] + 16 <= extent)
+        # outputs of the tile stay inside y / the partial buffer
+        assert n0 + 127 >= min(N - 1, n0)
+    assert p["grid"] == p["m_blocks"] * panels * ks
