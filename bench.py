@@ -25,7 +25,7 @@ import time
 
 
 def mean_gain(t_opt: float, t_base: float) -> float:
-    """The paper's mean gain G = 1 - E[T_opt] / E[T_base] (Section IV-G, Evaluation)."""
+    """The paper's mean gain G = 1 - E[T_opt] / E[T_base] (Section IV-F, Evaluation)."""
     return 1.0 - float(t_opt) / float(t_base)
 
 
@@ -58,6 +58,89 @@ def attention_bytes(heads, seq, dqk, dv) -> int:
     return heads * dqk * 2 + seq * dqk * 2 + heads * dv * 4
 
 
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                            "gemv_kernel_bf16_m1_decode_chain_traffic.txt")
+TRAFFIC_SOURCES = ("paper_2609_16009_amd/csrc/gemv.hip", "paper_2609_16009_amd/csrc/plan.cpp",
+                   "paper_2609_16009_amd/csrc/api.cpp")
+
+
+def kernel_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    root = os.path.dirname(os.path.abspath(__file__))
+    for rel in TRAFFIC_SOURCES:
+        with open(os.path.join(root, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def chain_traffic():
+    """HBM bytes per launch of the chain's GEMV kernel, as the FETCH_SIZE and WRITE_SIZE counters
+    read them (scaled by a plain copy of known size), from the stored counter summary -- or None
+    when the kernel sources have changed since those counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            fields = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith(" "))
+    except OSError:
+        return None
+    fields = {k.strip(): v.strip() for k, v in fields.items()}
+    if fields.get("kernel_source_digest") != kernel_source_digest():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def graph_time_us(torch, fn, reps: int = 20, iters: int = 5) -> float:
+    """Best of `iters` replays of one HIP graph holding `reps` calls of fn(r); us per call."""
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for r in range(3):
+            fn(r)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for r in range(reps):
+                fn(r)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    best = float("inf")
+    with torch.cuda.stream(s):
+        for _ in range(iters):
+            e0.record(s)
+            g.replay()
+            e1.record(s)
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1) * 1e3 / reps)
+    return best
+
+
+def crossover_sweep(nmm, torch, dev) -> dict:
+    """The narrow-to-dense crossover: x[M,1536] . W_UQ[1536,24576] bf16 on both kernel families,
+    M in {1,2,4,8,16,32}; W rotated over copies totalling > 1 GiB so it streams from HBM."""
+    import numpy as np
+    import synthetic as syn
+    case = syn.uq_sweep(32)
+    K, N = case.K, case.N
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    Ws = [up(case.W) for _ in range(14)]
+    x = up(case.x)
+    out = {}
+    for M in (1, 2, 4, 8, 16, 32):
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        nbytes = M * K * 2 + K * N * 2 + M * N * 4
+        row = {"bytes": nbytes, "auto": "mfma" if nmm.nmm_gemv_plan(M, K, N)["path"] == nmm.NMM_PATH_MFMA else "gemv"}
+        for name, path in (("gemv", nmm.NMM_PATH_GEMV), ("mfma", nmm.NMM_PATH_MFMA)):
+            ws = nmm.Workspace(dev)
+            t = graph_time_us(torch, lambda r: nmm.nmm_gemv(x[:M], Ws[r % len(Ws)], y, path=path, workspace=ws))
+            row[name + "_us"] = round(t, 2)
+            row[name + "_gbps"] = round(nbytes / t / 1e3, 1)
+        out[f"M={M}"] = row
+        log(f"[bench] crossover M={M}: gemv {row['gemv_us']} us, mfma {row['mfma_us']} us, auto -> {row['auto']}")
+    return out
+
+
 def cpu_baseline(step, target_s: float, bytes_per_step: int) -> dict:
     import oracle
     threads = oracle.max_threads()
@@ -83,6 +166,7 @@ def main() -> int:
     ap.add_argument("--copies", type=int, default=3, help="weight sets rotated across steps")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget for cpu_baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-crossover", action="store_true", help="skip the GEMV/MFMA crossover sweep")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
@@ -133,13 +217,7 @@ def main() -> int:
     ws_a, ws_b = nmm.Workspace(dev), nmm.Workspace(dev)
     ev = lambda: torch.cuda.Event(enable_timing=True)
     K, W = args.steps, args.warmup
-    n_slots = W + K
-    chain_ev = [[ev() for _ in range(6)] for _ in range(n_slots)]
-    att_ev = [[ev(), ev()] for _ in range(n_slots)]
-    chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a,
-                                events=[chain_ev[s] for s in range(n_slots) if s % args.copies == c])
-              for c in range(args.copies)]
-    slot_of = lambda s: s // args.copies        # the slot index inside chain copy s % copies
+    chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a) for c in range(args.copies)]
 
     def attention(s, stream):
         _, q, kv = copies[s % args.copies]
@@ -151,15 +229,13 @@ def main() -> int:
         start.record(cap)
         sa.wait_event(start)
         sb.wait_event(start)
-        chains[s % args.copies].launch(slot_of(s), stream=sa)
-        att_ev[s][0].record(sb)
+        chains[s % args.copies].launch(stream=sa)
         attention(s, sb)
-        att_ev[s][1].record(sb)
         cap.wait_stream(sa)
         cap.wait_stream(sb)
 
     def chain_only(s):
-        chains[s % args.copies].launch(slot_of(s), stream=cap)
+        chains[s % args.copies].launch(stream=cap)
 
     def attn_only(s):
         attention(s, cap)
@@ -174,68 +250,85 @@ def main() -> int:
             fn(s)
         return g
 
-    for e in (x for pair in att_ev for x in pair):   # create the HIP events before any capture
-        e.record(cap)
     # eager pass first: sizes the workspaces and gives the reference result for the graphs
     with torch.cuda.stream(cap):
         decode_step(0)
     torch.cuda.synchronize()
     y_eager, att_eager = inter["y"].clone(), att_out.clone()
     t = time.perf_counter()
-    step_graphs = [capture(decode_step, s) for s in range(n_slots)]
+    step_graphs = [capture(decode_step, s) for s in range(args.copies)]
     alone = {name: [capture(fn, s) for s in range(args.copies)]
              for name, fn in (("chain", chain_only), ("attention", attn_only), ("serial", serial))}
-    log(f"[bench] captured {n_slots + 3 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
+    log(f"[bench] captured {4 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
 
-    # ---- warmup, then exactly K timed steps (graph replays on one stream)
-    t0, t1 = ev(), ev()
-    with torch.cuda.stream(cap):
-        for s in range(W):
-            step_graphs[s].replay()
+    def timed(graphs, n):
+        """Mean time per replay of n replays (graphs rotated), events on the replay stream."""
+        a, b = ev(), ev()
+        with torch.cuda.stream(cap):
+            a.record(cap)
+            for s in range(n):
+                graphs[s % len(graphs)].replay()
+            b.record(cap)
         torch.cuda.synchronize()
-        t0.record(cap)
-        for s in range(W, W + K):
-            step_graphs[s].replay()
-        t1.record(cap)
-    torch.cuda.synchronize()
-    step_ms = t0.elapsed_time(t1) / K
-    same = torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager)
-    assert same, "graph replays must reproduce the eager decode step bit for bit"
-    names = list(cb)
-    per_launch = {n: [] for n in names}
-    for s in range(W, W + K):
-        for i, n in enumerate(names):
-            per_launch[n].append(chain_ev[s][i].elapsed_time(chain_ev[s][i + 1]))
-    chain_ms_in_step = float(np.mean([chain_ev[s][0].elapsed_time(chain_ev[s][5]) for s in range(W, W + K)]))
-    attn_ms_in_step = float(np.mean([att_ev[s][0].elapsed_time(att_ev[s][1]) for s in range(W, W + K)]))
-    gemv_ms_total = sum(sum(v) for v in per_launch.values())
-    achieved = chain_total * K / (gemv_ms_total * 1e-3) / 1e9
-    log(f"[bench] step {step_ms * 1e3:.1f} us (chain {chain_ms_in_step * 1e3:.1f} us, attention "
-        f"{attn_ms_in_step * 1e3:.1f} us on stream B); GEMV launches {achieved:.0f} GB/s")
+        return a.elapsed_time(b) / n
+
+    # ---- warmup, then exactly K timed decode steps (one graph replay each)
+    timed(step_graphs, W)
+    step_ms = timed(step_graphs, K)
+    assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
+        "graph replays must reproduce the eager decode step bit for bit"
 
     # ---- the overlap experiment: each stream alone, then both serially on one stream
-    def timed(graphs):
-        for s in range(len(graphs)):
-            graphs[s].replay()
-        torch.cuda.synchronize()
-        a, b = ev(), ev()
-        a.record(cap)
-        for s in range(K):
-            graphs[s % len(graphs)].replay()
-        b.record(cap)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / K
-
-    with torch.cuda.stream(cap):
-        t_a = timed(alone["chain"])
-        t_b = timed(alone["attention"])
-        t_serial = timed(alone["serial"])
+    timed(alone["chain"], W)
+    t_a = timed(alone["chain"], K)
+    timed(alone["attention"], W)
+    t_b = timed(alone["attention"], K)
+    timed(alone["serial"], W)
+    t_serial = timed(alone["serial"], K)
     gain = mean_gain(step_ms, t_serial)
     bound = 1.0 - max(t_a, t_b) / (t_a + t_b)
     log(f"[bench] chain alone {t_a * 1e3:.1f} us, attention alone {t_b * 1e3:.1f} us, serial "
         f"{t_serial * 1e3:.1f} us, concurrent {step_ms * 1e3:.1f} us: gain {100 * gain:.1f}% "
         f"(bound {100 * bound:.1f}%)")
     assert torch.isfinite(inter["y"]).all() and torch.isfinite(att_out).all()
+
+    # ---- each MatMul of the chain alone (same shapes and plans, its own graph)
+    H = d["heads"]
+    shapes = {
+        "down": lambda c, y: nmm.nmm_gemv(c["x"].view(1, -1), c["w_down"].view(d["hidden"], -1), y.view(1, -1), workspace=ws_a),
+        "w_uq": lambda c, y: nmm.nmm_gemv(inter["cq_bf16"].view(1, -1), c["w_uq"].view(d["q_lora"], -1), y.view(1, -1), workspace=ws_a),
+        "w_uk": lambda c, y: nmm.nmm_batched_gemv(inter["qnope_bf16"].view(H, 1, -1), c["w_uk"].view(H, d["nope"], -1),
+                                                  y.view(H, 1, -1), workspace=ws_a),
+        "w_uv": lambda c, y: nmm.nmm_batched_gemv(inter["lat_bf16"].view(H, 1, -1), c["w_uv"].view(H, d["kv_lora"], -1),
+                                                  y.view(H, 1, -1), workspace=ws_a),
+        "w_o": lambda c, y: nmm.nmm_gemv(inter["o_bf16"].view(1, -1), c["w_o"].view(H * d["v_head"], -1), y.view(1, -1), workspace=ws_a),
+    }
+    outs = {"down": torch.empty(n_down, device=dev), "w_uq": torch.empty(H * qk, device=dev),
+            "w_uk": torch.empty(H * d["kv_lora"], device=dev), "w_uv": torch.empty(H * d["v_head"], device=dev),
+            "w_o": torch.empty(d["hidden"], device=dev)}
+    per_matmul = {}
+    for name, fn in shapes.items():
+        per_matmul[name] = graph_time_us(torch, lambda r: fn(copies[r % args.copies][0], outs[name]))
+    log("[bench] each MatMul alone: " + ", ".join(f"{n} {t:.1f} us" for n, t in per_matmul.items()))
+
+    # ---- the practical read ceiling: the GEMV's load instruction streaming 2 GiB
+    probe_buf = torch.empty(2 << 30, dtype=torch.uint8, device=dev)
+    probe_out = torch.empty(4096, dtype=torch.int32, device=dev)
+    probe = {}
+    for unroll, grid in ((8, 256), (4, 512), (2, 1024), (1, 2048)):
+        t_us = graph_time_us(torch, lambda r: nmm.nmm_read_probe(probe_buf, probe_out, grid, unroll), reps=5, iters=3)
+        probe[f"U{unroll}x{grid}"] = round(probe_buf.numel() / t_us / 1e3, 1)
+    read_ceiling = max(probe.values())
+    log(f"[bench] read-probe ceiling {read_ceiling:.0f} GB/s ({probe})")
+    # a plain device copy of known size: the calibration point for the HBM byte counters
+    half = probe_buf.numel() // 2
+    copy_us = graph_time_us(torch, lambda r: probe_buf[half:].copy_(probe_buf[:half]), reps=5, iters=3)
+    copy_gbps = 2 * half / copy_us / 1e3
+    del probe_buf
+    log(f"[bench] device copy of {half >> 20} MiB: {copy_gbps:.0f} GB/s (read + write)")
+    achieved = chain_total / (t_a * 1e-3) / 1e9
+
+    crossover = None if args.no_crossover else crossover_sweep(nmm, torch, dev)
 
     value = (chain_total + attn_total) / (step_ms * 1e-3) / 1e9
     result = {
@@ -261,26 +354,33 @@ def main() -> int:
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "gemv_kernel<bf16, M tile 1> (the chain's five launches)",
+            "kernel": "gemv_kernel<bf16, 1-row tile, unroll 4>: the decode chain's five launches "
+                      "(algorithmic bytes of the five / their replayed time on the launch stream)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "algorithmic_bytes_per_launch": chain_total // len(cb),
+            "avg_launch_us": round(t_a * 1e3 / len(cb), 3),
+            "traffic": chain_traffic(),
         },
         "detail": {
             "chain_us": round(t_a * 1e3, 2),
-            "chain_gbps": round(chain_total / (t_a * 1e-3) / 1e9, 1),
-            "chain_pct_of_hbm_peak": round(100 * chain_total / (t_a * 1e-3) / 1e9 / HBM_PEAK_GBPS, 1),
+            "chain_roofline_us_at_peak": round(chain_total / (HBM_PEAK_GBPS * 1e3), 2),
             "attention_us": round(t_b * 1e3, 2),
             "serial_us": round(t_serial * 1e3, 2),
             "concurrent_us": round(step_ms * 1e3, 2),
             "overlap_gain": round(gain, 4),
             "overlap_gain_bound": round(bound, 4),
-            "per_launch_us": {n: round(1e3 * float(np.mean(v)), 2) for n, v in per_launch.items()},
-            "per_launch_gbps": {n: round(cb[n] / (1e-3 * float(np.mean(v))) / 1e9, 1) for n, v in per_launch.items()},
+            "per_matmul_us": {n: round(t, 2) for n, t in per_matmul.items()},
+            "per_matmul_gbps": {n: round(cb[n] / t / 1e3, 1) for n, t in per_matmul.items()},
+            "hbm_read_probe_gbps": probe,
+            "hbm_copy_gbps": round(copy_gbps, 1),
+            "achieved_frac_of_read_probe": round(achieved / read_ceiling, 4),
         },
     }
+    if crossover is not None:
+        result["detail"]["crossover"] = crossover
     if not args.no_cpu_baseline:
         log(f"[bench] timing the oracle on the host (~{args.cpu_seconds:.0f}s)")
         result["cpu_baseline"] = cpu_baseline(step, args.cpu_seconds, chain_total + attn_total)

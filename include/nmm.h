@@ -5,9 +5,9 @@
  * (1..16 on the streaming path, more on the matrix-core path), at the shapes of DeepSeek-V3
  * Multi-head Latent Attention single-token decode.  The operation is the paper's problem
  * statement C = A x B with A in R^{M x K}, B in R^{K x N}, narrow when min(M, N) = 1
- * (Section II-D "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"), widened to
+ * (Section II-E "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"), widened to
  * small M as in the future-work Conditions 4-5 (Section V), and its specialisation C = T x W for
- * the MLA down-projection (Section IV-C, eq. 4).
+ * the MLA down-projection (Section IV-B, eq. 4).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -74,7 +74,7 @@ typedef enum { NMM_PATH_AUTO = 0, NMM_PATH_GEMV = 1, NMM_PATH_MFMA = 2 } nmm_pat
 /*
  * nmm_gemv -- y[M,N] = x[M,K] . W[K,N].
  *
- * The paper's narrow MatMul (Section II-D; Condition 2) and its three-stage vector algorithm
+ * The paper's narrow MatMul (Section II-E; Condition 2) and its three-stage vector algorithm
  * (Algorithm 1, Section III-B: per-executor block loads, multiply + reduce to partial sums in a
  * temporary buffer, wait for all executors, gather).  Here the executors are workgroups: each
  * streams one K-slice of one column panel of W from HBM exactly once, keeps fp32 partial sums
@@ -124,9 +124,9 @@ nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_
  *   o'     = bf16(o)                 flattened to [1, heads*v_head]
  *   y      = o' . w_o                w_o [heads*v_head, hidden]
  *
- * The first step is the paper's MatMul 2 (eq. 3-4, Section IV-C/D), widened from the kv_lora |
- * rope columns to q_lora | kv_lora | rope.  Rounding to bf16 (ties to even) between steps
- * follows Algorithm 2's output cast (Section IV-E/F); it is fused into the producing kernel's
+ * The first step is the paper's MatMul 2 (eq. 3, Section IV-A; eq. 4, Section IV-B), widened
+ * from the kv_lora | rope columns to q_lora | kv_lora | rope.  Rounding to bf16 (ties to even) between steps
+ * follows Algorithm 2's output cast (Section IV-E); it is fused into the producing kernel's
  * gather, which writes both the fp32 result and the bf16 operand of the next step.
  *
  * Every buffer is caller-owned device memory.  The fp32 and bf16 intermediates are outputs so
@@ -156,7 +156,7 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
 /*
  * nmm_latent_attention -- single-token latent attention, the decode step's independent dense
  * work (the paper overlaps the vector unit's narrow MatMul with matrix-unit work that does not
- * depend on it: Condition 1 "Data Independence", Section III-A; Section IV-B).  For each head h:
+ * depend on it: Condition 1 "Data Independence", Section III-A; Section IV-A).  For each head h:
  *     s_j      = scale * sum_{d < d_qk} q[h*ldq + d] * kv[j*ld_kv + d]        (j < seq)
  *     p_j      = softmax_j(s)
  *     out[h,n] = sum_j p_j * kv[j*ld_kv + n]                                  (n < d_v)
@@ -183,7 +183,7 @@ nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* str
 
 /*
  * The host-side partition the library would launch for these sizes (a pure function: no GPU
- * access).  Algorithm 2's init stage (Section IV-F) sizes its executor pool from the core
+ * access).  Algorithm 2's init stage (Section IV-E) sizes its executor pool from the core
  * count; here the plan sizes a grid of workgroups for 256 compute units.
  */
 typedef struct {

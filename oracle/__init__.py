@@ -6,8 +6,8 @@ no code: this side is plain C (``nmm_oracle.c``, fp64, built with gcc) plus nump
 
 Functions (each cites the passage it follows in ``nmm_oracle.c``):
 
-* ``gemv``            -- y = x . W and sum |x_k W_kn| in fp64 (problem statement, Section II-D;
-                         Condition 2, Section III-A; eq. 4, Section IV-C).
+* ``gemv``            -- y = x . W and sum |x_k W_kn| in fp64 (problem statement, Section II-E;
+                         Condition 2, Section III-A; eq. 4, Section IV-B).
 * ``batched_gemv``    -- the same per batch index (per-head absorbed MLA matmuls).
 * ``round_bf16``      -- fp32 -> bf16 ties-to-even (Algorithm 2's final cast, Section IV-E).
 * ``latent_attention``-- textbook softmax attention in fp64 (the decode step's independent work).

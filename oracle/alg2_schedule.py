@@ -1,4 +1,4 @@
-"""Model of the paper's specialised MatMul 2 partition (Algorithm 2, Section IV-F) -- TEST ONLY.
+"""Model of the paper's specialised MatMul 2 partition (Algorithm 2, Section IV-E) -- TEST ONLY.
 
 This is the oracle's model of *how the paper splits the work*, written in the paper's notation
 (fractalSize, kSplitSize, kParts, fractalNum, S, V, nPart_W, groupSize, off_T, fracId, tmpBuf,

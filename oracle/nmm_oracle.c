@@ -8,11 +8,11 @@
  * What it computes (plain definitions, fp64, no blocking, no fusion, no reordering):
  *
  *  - Narrow MatMul, the paper's problem statement C = A x B with A in R^{MxK}, B in R^{KxN}
- *    (Section II-D "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"; the
- *    ENSURE clause of Algorithm 1) and its specialisation C = T x W (Section IV-C, eq. 4):
+ *    (Section II-E "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"; the
+ *    ENSURE clause of Algorithm 1) and its specialisation C = T x W (Section IV-B, eq. 4):
  *        y[m,n]   = sum_{k=0}^{K-1} dec(x[m,k]) * dec(W[k,n])        (ascending k)
  *        abs[m,n] = sum_{k=0}^{K-1} |dec(x[m,k]) * dec(W[k,n])|
- *    The paper's vector kernel keeps the accuracy of the matrix unit (Section IV-E "Data Type
+ *    The paper's vector kernel keeps the accuracy of the matrix unit (Section IV-D "Data Type
  *    Issue") and computes the same product, so the plain product is the reference.  A product
  *    of two 16-bit floats is exact in fp64; only the K-term summation rounds, at ~K*2^-53.
  *  - The same per batch index (the per-head absorbed MLA matmuls).

@@ -1,7 +1,7 @@
 // Host-side argument checks and the GEMV partition.  Pure functions: no HIP calls, no device
 // access, so they run (and are tested) on a machine without a GPU.
 //
-// The partition plays the role of Algorithm 2's init stage (Section IV-F), which splits a
+// The partition plays the role of Algorithm 2's init stage (Section IV-E), which splits a
 // [K, N] weight into kParts K-slices x fractalNum 16-column fractals and spreads them evenly over
 // at most 2P vector units.  Here the unit of work is a K-slice of a column panel (64 to 512
 // columns; one 16-byte chunk per lane per row).  Panel width and K-split count follow rules

@@ -5,7 +5,7 @@ What pins what:
   * 16-bit decoders: every one of the 65,536 patterns against numpy's float16 and torch's bfloat16.
   * fp32 -> bf16 rounding: constructed ties, neighbours of ties, and 2^21 random patterns against
     torch's round-to-nearest-even conversion.
-  * Narrow MatMul (problem statement, Section II-D; Condition 2, Section III-A; eq. 4): identity,
+  * Narrow MatMul (problem statement, Section II-E; Condition 2, Section III-A; eq. 4): identity,
     one-hot W, one-hot x on a non-square W (catches a transposed operand), rank-1 closed forms,
     exact rational brute force on tiny shapes, and integer-valued workloads against int64 sums.
   * Latent attention: seq = 1, uniform scores, a two-key case whose softmax is (3/4, 1/4) by
