@@ -278,6 +278,24 @@ def main() -> int:
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
         "graph replays must reproduce the eager decode step bit for bit"
 
+    # ---- the same K decode steps launched eagerly on the two streams (each stream has its own
+    # hardware queue, so the branches really run side by side; a graph replay issues all of its
+    # nodes through one queue, where a dependent node waits for every node queued before it)
+    def eager_steps(n):
+        a, b = ev(), ev()
+        a.record(cap)
+        for s in range(n):
+            decode_step(s)
+        b.record(cap)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    eager_steps(W)
+    eager_ms = eager_steps(K)
+    assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
+        "eager two-stream steps must reproduce the first eager step bit for bit"
+    log(f"[bench] decode step: graph replay {step_ms * 1e3:.1f} us, eager on two streams {eager_ms * 1e3:.1f} us")
+
     # ---- the overlap experiment: each stream alone, then both serially on one stream
     timed(alone["chain"], W)
     t_a = timed(alone["chain"], K)

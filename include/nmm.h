@@ -162,9 +162,12 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
  *     out[h,n] = sum_j p_j * kv[j*ld_kv + n]                                  (n < d_v)
  * i.e. V is the first d_v columns of the latent cache.  q and kv are bf16; out is fp32 with
  * leading dimension ldo.  Scores and softmax are fp32; p is rounded to bf16 for the matrix-core
- * product with V, accumulated in fp32.  Constraints: heads >= 0, seq >= 1, d_qk and d_v
- * multiples of 32 with d_v <= d_qk <= ld_kv, ldq >= d_qk, ldq and ld_kv multiples of 8,
- * q and kv 16-byte aligned, finite scale.
+ * product with V, accumulated in fp32.  Constraints (NMM_ERR_SHAPE / _ALIGN / _ARG before any
+ * launch): heads >= 0, seq >= 1, d_qk a multiple of 32 in [32, 1024], d_v a multiple of 16 in
+ * [16, 512], ld_kv >= max(d_qk, d_v), ldq >= d_qk, ldo >= d_v; ldq and ld_kv multiples of 8 and
+ * ldo a multiple of 4; q and kv 16-byte aligned, out 16-byte aligned; finite scale.  Results are
+ * deterministic for a given shape (fixed span partition and summation order); the workspace
+ * (nmm_latent_attention_workspace_size) holds per-span partial results.
  */
 nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
                                 const void* q, int64_t ldq, const void* kv, int64_t ld_kv,

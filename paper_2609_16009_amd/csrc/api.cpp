@@ -2,6 +2,7 @@
 // Every function validates everything before enqueueing anything and never throws.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -16,6 +17,20 @@ size_t rup256(size_t v) { return (v + 255) / 256 * 256; }
 
 // Workgroups of the persistent chain launch: one per compute unit of the current device, so
 // that all of them are resident together even beside other kernels (NMM_CHAIN_WGS overrides).
+// Row-steps in flight per lane in the fused chain (NMM_CHAIN_UNROLL overrides).
+int chain_unroll() {
+    if (const char* s = std::getenv("NMM_CHAIN_UNROLL")) {
+        const long v = std::strtol(s, nullptr, 10);
+        if (v == 4 || v == 8 || v == 16) return static_cast<int>(v);
+    }
+    return 16;
+}
+
+bool chain_fused_requested() {
+    const char* fe = std::getenv("NMM_CHAIN_FUSED");
+    return fe && fe[0] == '1';
+}
+
 int chain_workgroups() {
     if (const char* s = std::getenv("NMM_CHAIN_WGS")) {
         const long v = std::strtol(s, nullptr, 10);
@@ -50,6 +65,7 @@ nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, v
 struct Chain {
     GemvArgs step[5];
     GemvPlan plan[5];
+    int64_t flag_off;      // first completion flag of the fused launch
     int64_t tick_off[5];   // first counter of each step
     size_t part_off[5];    // byte offset of each step's partial sums (from the workspace start)
     size_t ws_total;
@@ -62,7 +78,7 @@ bool chain_dims_ok(const nmm_mla_chain& c) {
     return c.nope + c.rope < (int64_t(1) << 31) / c.heads;
 }
 
-nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
+nmm_status build_chain(const nmm_mla_chain& c, Chain* out, int unroll = 0) {
     if (!chain_dims_ok(c)) return NMM_ERR_SHAPE;
     const int64_t n_down = c.q_lora + c.kv_lora + c.rope;
     const int64_t qk = c.nope + c.rope;
@@ -99,7 +115,7 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
     for (int i = 0; i < 5; ++i) {
         s[i].M = 1;
         s[i].dt = NMM_BF16;
-        nmm_status st = plan_gemv(s[i].batch, 1, s[i].K, s[i].N, NMM_BF16, NMM_PATH_GEMV, &ch.plan[i]);
+        nmm_status st = plan_gemv(s[i].batch, 1, s[i].K, s[i].N, NMM_BF16, NMM_PATH_GEMV, &ch.plan[i], unroll);
         if (st != NMM_OK) return st;
         ch.tick_off[i] = ticks;
         ch.part_off[i] = off;
@@ -109,6 +125,8 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
             off += rup256(static_cast<size_t>(ch.plan[i].part_floats) * 4);
         }
     }
+    ch.flag_off = ticks;
+    ticks += chain_flags(ch.step, ch.plan, 5);
     if (ticks > kMaxTickets) return NMM_ERR_SHAPE;
     (void)any_split;
     ch.ws_total = off;   // the counter block is always needed: the fused chain keeps its queue there
@@ -180,8 +198,10 @@ nmm_status nmm_gemv_plan(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dty
 
 size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain) {
     if (!chain) return 0;
-    Chain ch;
-    return build_chain(*chain, &ch) == NMM_OK ? ch.ws_total : 0;
+    // enough for either form of the chain (separate launches or the fused launch)
+    Chain a, b;
+    if (build_chain(*chain, &a) != NMM_OK || build_chain(*chain, &b, chain_unroll()) != NMM_OK) return 0;
+    return std::max(a.ws_total, b.ws_total);
 }
 
 nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
@@ -192,7 +212,8 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
         !c.lat_f32 || !c.o_f32 || !c.y || !c.cq_bf16 || !c.qnope_bf16 || !c.lat_bf16 || !c.o_bf16)
         return NMM_ERR_NULL;
     Chain ch;
-    nmm_status st = build_chain(c, &ch);
+    const bool want_fused = chain_fused_requested();
+    nmm_status st = build_chain(c, &ch, want_fused ? chain_unroll() : 0);
     if (st != NMM_OK) return st;
     for (int i = 0; i < 5; ++i) {
         st = validate_gemv(ch.step[i], NMM_PATH_GEMV);
@@ -206,11 +227,9 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
             if (!c.events[i]) return NMM_ERR_NULL;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // One launch per MatMul by default.  NMM_CHAIN_FUSED=1 selects the persistent launch that runs
-    // all five MatMuls (bit-identical results); on MI355X it is slower (130 vs 79 us for the
-    // decode chain), because one resident workgroup per compute unit keeps too few loads in flight.
-    const char* fe = std::getenv("NMM_CHAIN_FUSED");
-    const bool fused = (fe && fe[0] == '1') && chain_fusable(ch.step, ch.plan, 5);
+    // One launch per MatMul by default; NMM_CHAIN_FUSED=1 selects the persistent launch that runs
+    // all five MatMuls with per-panel dependencies.
+    const bool fused = want_fused && chain_fusable(ch.step, ch.plan, 5);
     if (fused) {
         unsigned* sync = static_cast<unsigned*>(workspace);
         unsigned* tickets[5];
@@ -220,7 +239,7 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
             part[i] = ch.plan[i].split() ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ch.part_off[i]) : nullptr;
         }
         if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[0]), s) != hipSuccess) return NMM_ERR_HIP;
-        st = launch_chain(ch.step, ch.plan, 5, sync, tickets, part, chain_workgroups(), stream);
+        st = launch_chain(ch.step, ch.plan, 5, sync, sync + ch.flag_off, tickets, part, chain_workgroups(), stream);
         if (st != NMM_OK) return st;
         if (c.events) {
             for (int i = 1; i < 6; ++i)

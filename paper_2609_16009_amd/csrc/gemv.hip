@@ -181,30 +181,38 @@ __device__ __forceinline__ void store_out(const KParams& p, int64_t b, int m, in
     }
 }
 
-// Stage x[m0:m0+MT, k0:k0+rows] into LDS as fp32, layout [row][m], zero outside M x K.  Each
-// thread fetches 16-byte chunks of x rows (8 consecutive k); every chunk load is issued before
-// any is used, and chunks past x's extent read as zeros.
-template <int DT, int MT, int AUX>
-__device__ __forceinline__ void stage_x(float* __restrict__ lds, const KParams& p, int64_t b, int m0,
-                                        int k0, int rows, int tid) {
+// Stage x[m0:m0+MT, k0:k0+rows] into LDS as fp32, layout [row][m], zero outside M x K, in two
+// halves: stage_x_issue issues every 16-byte chunk load of the slice (8 consecutive k of one x
+// row; chunks past x's extent read as zeros) and stage_x_commit widens them into LDS.  W loads
+// issued between the two stay in flight while x is committed (loads complete in issue order).
+constexpr int kXPer = (kXStageBytes / 4 / 8 + kThreads - 1) / kThreads;   // x chunks per thread
+
+template <int MT, int AUX>
+__device__ __forceinline__ void stage_x_issue(i32x4 (&v)[kXPer], const KParams& p, int64_t b, int m0, int k0,
+                                              int rows, int tid) {
     const int cpr = rows / 8;                       // chunks per x row of the slice
     const int total = cpr * MT;
     const int mrows = min(MT, p.M - m0);
     // x's extent reaches the 16-byte chunk holding each row's last element (ABI rule)
     const uint32_t x_extent = uint32_t(((int64_t(m0) + mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2);
     const __amdgpu_buffer_rsrc_t xr = make_rsrc(p.x + b * p.sx, x_extent);
-    constexpr int kMaxPer = (kXStageBytes / 4 / 8 + kThreads - 1) / kThreads;   // chunks per thread
-    i32x4 v[kMaxPer];
 #pragma unroll
-    for (int j = 0; j < kMaxPer; ++j) {
+    for (int j = 0; j < kXPer; ++j) {
         const int i = tid + j * kThreads;
         const int m = i / cpr, q = i - m * cpr;
         const bool ok = i < total && m < mrows;
         const uint32_t off = ok ? uint32_t(((int64_t(m0) + m) * p.ldx + k0 + 8 * q) * 2) : kOutOfRange;
         v[j] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, AUX);
     }
+}
+
+template <int DT, int MT>
+__device__ __forceinline__ void stage_x_commit(float* __restrict__ lds, const i32x4 (&v)[kXPer], const KParams& p,
+                                               int k0, int rows, int tid) {
+    const int cpr = rows / 8;
+    const int total = cpr * MT;
 #pragma unroll
-    for (int j = 0; j < kMaxPer; ++j) {
+    for (int j = 0; j < kXPer; ++j) {
         const int i = tid + j * kThreads;
         if (i < total) {
             const int m = i / cpr, q = i - m * cpr;
@@ -218,103 +226,177 @@ __device__ __forceinline__ void stage_x(float* __restrict__ lds, const KParams& 
     }
 }
 
-// The fused chain's cross-workgroup dependency: the items of a MatMul may only read its x once
-// the previous MatMul has finished all of its panels.
-struct Dep {
-    unsigned* wait_on = nullptr;   // completed-panel counter of the producing MatMul (or null)
-    unsigned target = 0;           // its panel count
-    unsigned* done = nullptr;      // this MatMul's completed-panel counter
-    unsigned* error = nullptr;     // set when a wait gives up
-    int spin_limit = 0;
-    int sleep_reps = 1;            // s_sleep(2) repetitions between polls
+// ---------------------------------------------------------------------------------------------
+// One work item: one K-slice of one panel of one (batch entry, row block).
+// ---------------------------------------------------------------------------------------------
+struct Item {
+    int64_t b;                    // batch entry
+    int mb;                       // row block
+    int panel, slice, ks, rows, valid;
+    int lg, cw, c, rstep, rin;
+    int k0, m0, chunk0;
 };
 
-// Wait until *d.wait_on reaches d.target.  Bounded: after spin_limit polls the wait gives up
-// and raises the error flag, so a broken dependency can never hang the GPU.
-__device__ __forceinline__ void wait_dependency(const Dep& d) {
-    if (threadIdx.x == 0) {
-        int spins = 0;
-        while (__hip_atomic_load(d.wait_on, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < d.target) {
-            if (++spins > d.spin_limit) {
-                __hip_atomic_store(d.error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-            for (int r = 0; r < d.sleep_reps; ++r) __builtin_amdgcn_s_sleep(2);
-        }
-    }
-    __syncthreads();
-}
-
-// Count one more completed panel, after every thread's output stores have completed.
-__device__ __forceinline__ void signal_done(const Dep& d) {
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x == 0) __hip_atomic_fetch_add(d.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// One work item: one K-slice of one panel of one (batch entry, row block).  `bid` is the item's
-// index within its MatMul.  CHAIN adds the fused chain's dependency wait and completion signal.
-template <int DT, int MT, int U, bool CHAIN>
-__device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float* lds, int* s_last, const Dep& dep) {
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-
+template <int MT>
+__device__ __forceinline__ Item item_of(const KParams& p, uint32_t bid, int tid) {
+    Item it;
+    const int lane = tid & 63, wave = tid >> 6;
     const int item = static_cast<int>(bid % uint32_t(p.items));
     const uint32_t bm = bid / uint32_t(p.items);
-    const int mb = static_cast<int>(bm % uint32_t(p.mblocks));
-    const int64_t b = bm / uint32_t(p.mblocks);
-
-    // which panel and K-slice this workgroup owns
-    int panel, slice, lg, ks, rows, valid;
+    it.mb = static_cast<int>(bm % uint32_t(p.mblocks));
+    it.b = bm / uint32_t(p.mblocks);
     if (item < p.n_full * p.ks_full) {
-        panel = item / p.ks_full;
-        slice = item - panel * p.ks_full;
-        lg = p.full_lg;
-        ks = p.ks_full;
-        rows = p.rows_full;
-        valid = 1 << p.full_lg;
+        it.panel = item / p.ks_full;
+        it.slice = item - it.panel * p.ks_full;
+        it.lg = p.full_lg;
+        it.ks = p.ks_full;
+        it.rows = p.rows_full;
+        it.valid = 1 << p.full_lg;
     } else {
-        panel = p.n_full;
-        slice = item - p.n_full * p.ks_full;
-        lg = p.tail_lg;
-        ks = p.ks_tail;
-        rows = p.rows_tail;
-        valid = p.tail_chunks;
+        it.panel = p.n_full;
+        it.slice = item - p.n_full * p.ks_full;
+        it.lg = p.tail_lg;
+        it.ks = p.ks_tail;
+        it.rows = p.rows_tail;
+        it.valid = p.tail_chunks;
     }
-    const int cw = 1 << lg;                 // lanes across the panel's columns
-    const int c = lane & (cw - 1);
-    const int rstep = kWaves << (6 - lg);   // rows per workgroup step
-    const int rin = wave * (64 >> lg) + (lane >> lg);
-    const int k0 = slice * rows;
-    const int m0 = mb * MT;
-    const int chunk0 = panel << p.full_lg;  // first 8-column chunk of the panel
-    const bool guard = k0 + rows > p.K;     // only the last K-slice reaches past K
+    it.cw = 1 << it.lg;                        // lanes across the panel's columns
+    it.c = lane & (it.cw - 1);
+    it.rstep = kWaves << (6 - it.lg);          // rows per workgroup step
+    it.rin = wave * (64 >> it.lg) + (lane >> it.lg);
+    it.k0 = it.slice * it.rows;
+    it.m0 = it.mb * MT;
+    it.chunk0 = it.panel << p.full_lg;         // first 8-column chunk of the panel
+    return it;
+}
 
-    // ---- init: issue the first U loads of W (they do not depend on x), then stage x
+// Where the item's lane reads W; lanes past a ragged panel edge re-read its last chunk.
+__device__ __forceinline__ Stream stream_of(const KParams& p, const Item& it) {
     Stream st;
-    {
-        const int cc = c < valid ? c : valid - 1;   // lanes past a ragged edge re-read its last chunk
-        st.rsrc = make_rsrc(p.w + b * p.sw, p.w_extent);
-        st.off = uint32_t(k0 + rin) * p.row_bytes + uint32_t(chunk0 + cc) * 16u;
-        st.step_bytes = uint32_t(rstep) * p.row_bytes;
-        st.row = k0 + rin;
-        st.rstep = rstep;
-        st.K = p.K;
+    const int cc = it.c < it.valid ? it.c : it.valid - 1;
+    st.rsrc = make_rsrc(p.w + it.b * p.sw, p.w_extent);
+    st.off = uint32_t(it.k0 + it.rin) * p.row_bytes + uint32_t(it.chunk0 + cc) * 16u;
+    st.step_bytes = uint32_t(it.rstep) * p.row_bytes;
+    st.row = it.k0 + it.rin;
+    st.rstep = it.rstep;
+    st.K = p.K;
+    return st;
+}
+
+template <int MT>
+__device__ __forceinline__ int64_t part_base(const KParams& p, const Item& it) {
+    return (((it.b * p.mblocks + it.mb) * p.n_panels + it.panel) * int64_t(p.ks_max)) * (int64_t(MT) * kPanelCols);
+}
+
+// Gather, part 1: each wave folds its row groups with a fixed butterfly of cross-lane exchanges
+// (lanes r*cw + c and (r^j)*cw + c hold the same columns), then the four waves are summed
+// through LDS in wave order.  A panel with one K-slice writes y; otherwise the slice's partial
+// sums go to the workspace with device-scope stores (coherent past the per-XCD L2 caches).
+template <int MT, bool CHAIN>
+__device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, float (&acc)[MT][8], float* lds,
+                                            int tid) {
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int off = it.cw; off < 64; off <<= 1) {
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc[m][j] += __shfl_xor(acc[m][j], off);
     }
-    i32x4 buf[U];
-    if (guard) prefetch<U, true>(buf, st);
-    else prefetch<U, false>(buf, st);
-    if constexpr (CHAIN) {
-        if (dep.wait_on) {
-            wait_dependency(dep);
-            stage_x<DT, MT, kLoadCoherent>(lds, p, b, m0, k0, rows, tid);
-        } else {
-            stage_x<DT, MT, 0>(lds, p, b, m0, k0, rows, tid);
+    constexpr int MG = MT < 4 ? MT : 4;
+    const int pcols = it.cw * 8;
+    const int64_t pbase = part_base<MT>(p, it);
+#pragma unroll
+    for (int g = 0; g < MT; g += MG) {
+        if (lane < it.cw) {
+#pragma unroll
+            for (int mm = 0; mm < MG; ++mm) {
+                float* dst = lds + ((wave * MG + mm) * it.cw + it.c) * 8;
+                *reinterpret_cast<f32x4*>(dst) = f32x4{acc[g + mm][0], acc[g + mm][1], acc[g + mm][2], acc[g + mm][3]};
+                *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[g + mm][4], acc[g + mm][5], acc[g + mm][6], acc[g + mm][7]};
+            }
         }
-    } else {
-        stage_x<DT, MT, 0>(lds, p, b, m0, k0, rows, tid);
+        __syncthreads();
+        for (int o = tid; o < MG * pcols; o += kThreads) {
+            const int mm = o / pcols, col = o - mm * pcols;
+            float v = lds[mm * pcols + col];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) v += lds[(w * MG + mm) * pcols + col];
+            const int m = g + mm;
+            const int n = it.chunk0 * 8 + col;
+            if (it.ks == 1) {
+                if (it.m0 + m < p.M && n < p.N) store_out<CHAIN>(p, it.b, it.m0 + m, n, v);
+            } else {
+                __hip_atomic_store(p.part + pbase + int64_t(it.slice) * (MT * kPanelCols) + m * kPanelCols + col,
+                                   v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        __syncthreads();
     }
+}
+
+// Gather, part 2 (the panel's last workgroup only): every output of the panel sums its K-slices
+// in slice order; the loads of R outputs x QB slices are all in flight before any is added.
+template <int MT, bool CHAIN>
+__device__ __forceinline__ void gather_panel(const KParams& p, const Item& it, int tid) {
+    constexpr int R = (MT * 2 < 8) ? MT * 2 : 8;   // outputs per thread per pass (pcols <= 512)
+    constexpr int QB = 32 / R;                      // slices per batch
+    const int pcols = it.cw * 8;
+    const int n_out = MT * pcols;
+    const int64_t pbase = part_base<MT>(p, it);
+    for (int o0 = tid; o0 < n_out; o0 += R * kThreads) {
+        float sum[R];
+#pragma unroll
+        for (int r = 0; r < R; ++r) sum[r] = 0.f;
+        for (int q0 = 0; q0 < it.ks; q0 += QB) {
+            float v[R][QB];
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                const int o = o0 + r * kThreads;
+                const int m = o / pcols, col = o - m * pcols;
+                const float* src = p.part + pbase + m * kPanelCols + col;
+#pragma unroll
+                for (int u = 0; u < QB; ++u)
+                    v[r][u] = (o < n_out && q0 + u < it.ks)
+                                  ? __hip_atomic_load(src + int64_t(q0 + u) * (MT * kPanelCols), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                  : 0.f;
+            }
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+#pragma unroll
+                for (int u = 0; u < QB; ++u)
+                    if (q0 + u < it.ks) sum[r] += v[r][u];
+        }
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int o = o0 + r * kThreads;
+            const int m = o / pcols, col = o - m * pcols;
+            const int n = it.chunk0 * 8 + col;
+            if (o < n_out && it.m0 + m < p.M && n < p.N) store_out<CHAIN>(p, it.b, it.m0 + m, n, sum[r]);
+        }
+    }
+}
+
+// The panel's arrival counter.  The caller has waited for its partial stores (s_waitcnt 0) and
+// synchronised; the device-scope ticket then orders the hand-off without flushing the L2.
+__device__ __forceinline__ unsigned* ticket_of(const KParams& p, const Item& it) {
+    return p.tickets + (it.b * p.mblocks + it.mb) * p.n_panels + it.panel;
+}
+
+// One work item of a separate GEMV launch.
+template <int DT, int MT, int U>
+__device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float* lds, int* s_last) {
+    const int tid = threadIdx.x;
+    const Item it = item_of<MT>(p, bid, tid);
+
+    // ---- init: issue x's loads, then the first U loads of W, then commit x to LDS while the W
+    // loads are still in flight
+    const Stream st = stream_of(p, it);
+    i32x4 xv[kXPer];
+    stage_x_issue<MT, 0>(xv, p, it.b, it.m0, it.k0, it.rows, tid);
+    i32x4 buf[U];
+    prefetch<U, true>(buf, st);   // one straight-line path, so x's wait leaves these in flight
+    stage_x_commit<DT, MT>(lds, xv, p, it.k0, it.rows, tid);
     __syncthreads();
 
     // ---- compute: stream this workgroup's rows of the panel
@@ -324,167 +406,201 @@ __device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float*
 #pragma unroll
         for (int j = 0; j < 8; ++j) acc[m][j] = 0.f;
     {
-        const int nsteps = rows / rstep;
-        const float* xs = lds + rin * MT;
-        if (guard) stream_rows<DT, MT, U, true>(acc, buf, st, nsteps, xs, rstep * MT);
-        else stream_rows<DT, MT, U, false>(acc, buf, st, nsteps, xs, rstep * MT);
+        const int nsteps = it.rows / it.rstep;
+        const float* xs = lds + it.rin * MT;
+        stream_rows<DT, MT, U, true>(acc, buf, st, nsteps, xs, it.rstep * MT);
     }
     __syncthreads();   // x slice no longer needed: LDS becomes the reduction buffer
 
-    // ---- gather, part 1: reduce the workgroup's row groups (fixed order) per m-group
-    constexpr int MG = MT < 4 ? MT : 4;
-    const int pcols = cw * 8;                                  // columns of this panel
-    const int64_t pbase = (((b * p.mblocks + mb) * p.n_panels + panel) * int64_t(p.ks_max)) *
-                          (int64_t(MT) * kPanelCols);
-#pragma unroll
-    for (int g = 0; g < MT; g += MG) {
-#pragma unroll
-        for (int mm = 0; mm < MG; ++mm) {
-            float* dst = lds + ((mm * rstep + rin) * cw + c) * 8;
-            *reinterpret_cast<f32x4*>(dst) = f32x4{acc[g + mm][0], acc[g + mm][1], acc[g + mm][2], acc[g + mm][3]};
-            *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[g + mm][4], acc[g + mm][5], acc[g + mm][6], acc[g + mm][7]};
-        }
-        __syncthreads();
-        for (int o = tid; o < MG * pcols; o += kThreads) {
-            const int mm = o / pcols, col = o - mm * pcols;
-            float s = 0.f;
-            for (int r = 0; r < rstep; ++r) s += lds[(mm * rstep + r) * pcols + col];
-            const int m = g + mm;
-            const int n = chunk0 * 8 + col;
-            if (ks == 1) {
-                if (m0 + m < p.M && n < p.N) store_out<CHAIN>(p, b, m0 + m, n, s);
-            } else {
-                __hip_atomic_store(p.part + pbase + int64_t(slice) * (MT * kPanelCols) + m * kPanelCols + col,
-                                   s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-        }
-        __syncthreads();
-    }
-    if (ks == 1) {
-        if constexpr (CHAIN) signal_done(dep);
-        return;
-    }
-
-    // ---- gather, part 2: the last workgroup of this panel sums the K-slices in order.
-    // The partial sums above were written with device-scope atomic stores, which the GPU makes
-    // coherent at memory (past the per-XCD L2 caches); the ticket is a device-scope atomic too,
-    // and the last workgroup reads the partials with device-scope atomic loads.  Waiting for
-    // every store to complete (s_waitcnt 0) before the ticket increment, and for the ticket's
-    // value before the loads, orders the hand-off without writing back or invalidating the L2.
+    // ---- gather
+    reduce_item<MT, false>(p, it, acc, lds, tid);
+    if (it.ks == 1) return;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-        unsigned* t = p.tickets + (b * p.mblocks + mb) * p.n_panels + panel;
+        unsigned* t = ticket_of(p, it);
         const unsigned prev = __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int last = prev == unsigned(ks - 1);
+        const int last = prev == unsigned(it.ks - 1);
         if (last) __hip_atomic_store(t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         *s_last = last;
     }
     __syncthreads();
-    if (!*s_last) return;
-    // every output of the panel sums its slices in slice order; the loads of R outputs x QB
-    // slices are all in flight before any is added
-    constexpr int R = (MT * 2 < 8) ? MT * 2 : 8;   // outputs per thread per pass (pcols <= 512)
-    constexpr int QB = 32 / R;                      // slices per batch
-    const int n_out = MT * pcols;
-    for (int o0 = tid; o0 < n_out; o0 += R * kThreads) {
-        float sum[R];
-#pragma unroll
-        for (int r = 0; r < R; ++r) sum[r] = 0.f;
-        for (int q0 = 0; q0 < ks; q0 += QB) {
-            float v[R][QB];
-#pragma unroll
-            for (int r = 0; r < R; ++r) {
-                const int o = o0 + r * kThreads;
-                const int m = o / pcols, col = o - m * pcols;
-                const float* src = p.part + pbase + m * kPanelCols + col;
-#pragma unroll
-                for (int u = 0; u < QB; ++u)
-                    v[r][u] = (o < n_out && q0 + u < ks)
-                                  ? __hip_atomic_load(src + int64_t(q0 + u) * (MT * kPanelCols), __ATOMIC_RELAXED,
-                                                      __HIP_MEMORY_SCOPE_AGENT)
-                                  : 0.f;
-            }
-#pragma unroll
-            for (int r = 0; r < R; ++r)
-#pragma unroll
-                for (int u = 0; u < QB; ++u)
-                    if (q0 + u < ks) sum[r] += v[r][u];
-        }
-#pragma unroll
-        for (int r = 0; r < R; ++r) {
-            const int o = o0 + r * kThreads;
-            const int m = o / pcols, col = o - m * pcols;
-            const int n = chunk0 * 8 + col;
-            if (o < n_out && m0 + m < p.M && n < p.N) store_out<CHAIN>(p, b, m0 + m, n, sum[r]);
-        }
-    }
-    if constexpr (CHAIN) signal_done(dep);
+    if (*s_last) gather_panel<MT, false>(p, it, tid);
 }
 
 template <int DT, int MT, int U>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
     extern __shared__ float lds[];
     __shared__ int s_last;
-    gemv_item<DT, MT, U, false>(p, blockIdx.x, lds, &s_last, Dep{});
+    gemv_item<DT, MT, U>(p, blockIdx.x, lds, &s_last);
 }
 
 // ---------------------------------------------------------------------------------------------
-// The fused decode chain: one persistent launch runs the MatMuls of the chain back to back.
-// The work items of all MatMuls form one ordered list (every item of MatMul s precedes every
-// item of MatMul s+1); workgroup w takes items w, w + G, w + 2G, ... in that order.  An item of
-// MatMul s+1 issues its first W loads at once and only then waits for MatMul s to have
-// completed all of its panels, so the next weight stream starts while the previous MatMul's
-// last panels are still being gathered -- the paper's point of starting independent work
-// earlier, here between consecutive narrow MatMuls.  (A shared claim counter would serialise
-// thousands of same-address atomics; the static order costs none.)
+// The fused decode chain: one persistent launch runs the MatMuls of the chain back to back
+// (bf16, one row).  The work items of all MatMuls form one ordered list (every item of MatMul s
+// precedes every item of MatMul s+1); workgroup w takes items w, w + G, w + 2G, ... in order.
 //
-// Progress: a workgroup finishes all of its items of MatMul s before it waits on MatMul s, and
-// it only ever waits on items placed earlier in the list.  So the waits always end once all G
-// workgroups are resident; the launch uses at most one workgroup per compute unit so that they
-// are, even beside the attention kernel on the other stream.  Every wait is also bounded
-// (Dep::spin_limit): if it ever gave up, the error flag is raised instead of the GPU hanging.
-// Every workgroup leaves after its last item; the last one out resets the counters.
+//  * Dependencies are per panel: when a panel's outputs (fp32 y and the bf16 hand-off) are
+//    complete, the workgroup that wrote them raises the panel's flag.  An item of MatMul s+1
+//    waits only for the panels of MatMul s that produce its own K-slice of x, so the next
+//    weight stream starts as soon as the inputs it needs exist, not when the whole previous
+//    MatMul has finished -- the paper's point of starting independent work earlier, here
+//    between consecutive narrow MatMuls.
+//  * Each item issues the first U row-steps of the NEXT item's W (which depend on nothing)
+//    right after its own partial sums are out, so that the split-K ticket round trip, the
+//    gather and the next dependency wait all overlap with weight loads in flight.
+//
+// Progress: a workgroup takes its items in list order, and an item only waits on items placed
+// earlier in the list, so the earliest unfinished item can always run once all G workgroups are
+// resident.  The launch is clamped to the number that the device can hold at once.  Every wait
+// is also bounded (spin_limit polls): if one ever gave up, the error word is raised instead of
+// the GPU hanging.  The last workgroup out clears the flags for the next launch.
 // ---------------------------------------------------------------------------------------------
 constexpr int kChainMax = 5;
 
 struct ChainArgs {
     KParams step[kChainMax];
-    int first_item[kChainMax + 1];   // list position of each MatMul's first item
-    unsigned panels[kChainMax];      // panels (all batch entries and row blocks) of each MatMul
-    unsigned* sync;                  // [1] exited workgroups, [2] error, [3 + s] done of MatMul s
+    int first_item[kChainMax + 1];   // list position of each MatMul's first item; [n] = total
+    int flag_off[kChainMax + 1];     // first completion flag of each MatMul's panels; [n] = total
+    unsigned* sync;                  // [1] exited workgroups, [2] error word
+    unsigned* flags;                 // one per panel (batch entry x column panel) of every MatMul
     int n_steps;
     int spin_limit;
     int sleep_reps;
 };
 
+// The panel (flattened over batch entries) of the producing MatMul that wrote element j of its
+// bf16 hand-off buffer: j = b * ybf_sb + g * keep + r holds output column g * group + r.
+__device__ __forceinline__ int producer_panel(const KParams& pp, int64_t j) {
+    int64_t b = 0, rem = j;
+    if (pp.ybf_sb > 0) {
+        b = j / pp.ybf_sb;
+        rem = j - b * pp.ybf_sb;
+    }
+    const int64_t g = rem / pp.ybf_keep, r = rem - g * pp.ybf_keep;
+    const int64_t n = g * pp.ybf_group + r;
+    const int pan = static_cast<int>(min(n >> (3 + pp.full_lg), int64_t(pp.n_full)));
+    return static_cast<int>(b) * pp.n_panels + pan;
+}
+
+// Wait until every producer panel covering this item's x slice has raised its flag.  Wave 0
+// polls up to 64 flags at once; bounded by spin_limit polls.
+__device__ __forceinline__ void wait_panels(const ChainArgs& a, int st, const Item& it, int tid) {
+    const KParams& pc = a.step[st];
+    const KParams& pp = a.step[st - 1];
+    const int64_t jb = it.b * pc.sx;
+    const int qa = producer_panel(pp, jb + it.k0);
+    const int qb = producer_panel(pp, jb + min(it.k0 + it.rows, pc.K) - 1);
+    if (tid < 64) {
+        const unsigned* f = a.flags + a.flag_off[st - 1];
+        for (int q0 = qa; q0 <= qb; q0 += 64) {
+            const int q = q0 + tid;
+            bool ok = q > qb;
+            int spins = 0;
+            while (true) {
+                if (!ok) ok = __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+                if (__all(ok)) break;
+                if (++spins > a.spin_limit) {
+                    if (tid == 0) __hip_atomic_store(a.sync + 2, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                for (int r = 0; r < a.sleep_reps; ++r) __builtin_amdgcn_s_sleep(2);
+            }
+        }
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ void raise_flag(const ChainArgs& a, int st, const Item& it) {
+    const KParams& p = a.step[st];
+    __hip_atomic_store(a.flags + a.flag_off[st] + it.b * p.n_panels + it.panel, 1u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int U>
 __global__ __launch_bounds__(kThreads) void chain_kernel(const ChainArgs a) {
     extern __shared__ float lds[];
     __shared__ int s_last;
-    unsigned* sync = a.sync;
+    const int tid = threadIdx.x;
     const int total = a.first_item[a.n_steps];
+    int item = blockIdx.x;
     int st = 0;
-    for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    Item it;
+    Stream ss;
+    i32x4 buf[U];
+    if (item < total) {
         while (st + 1 < a.n_steps && item >= a.first_item[st + 1]) ++st;
-        Dep dep;
-        dep.wait_on = st ? sync + 3 + (st - 1) : nullptr;
-        dep.target = st ? a.panels[st - 1] : 0;
-        dep.done = sync + 3 + st;
-        dep.error = sync + 2;
-        dep.spin_limit = a.spin_limit;
-        dep.sleep_reps = a.sleep_reps;
-        gemv_item<NMM_BF16, 1, 4, true>(a.step[st], item - a.first_item[st], lds, &s_last, dep);
-        __syncthreads();   // LDS is reused by the next item
+        it = item_of<1>(a.step[st], item - a.first_item[st], tid);
+        ss = stream_of(a.step[st], it);
+        prefetch<U, true>(buf, ss);
     }
-    // leave: the last workgroup out resets the completion counters for the next launch
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_s_waitcnt(0);
-        const unsigned prev = __hip_atomic_fetch_add(sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev == gridDim.x - 1) {
-            for (int i = 0; i < a.n_steps; ++i)
-                __hip_atomic_store(sync + 3 + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(sync + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    while (item < total) {
+        const KParams& p = a.step[st];
+        if (st > 0) wait_panels(a, st, it, tid);
+        {
+            i32x4 xv[kXPer];
+            stage_x_issue<1, kLoadCoherent>(xv, p, it.b, it.m0, it.k0, it.rows, tid);
+            stage_x_commit<NMM_BF16, 1>(lds, xv, p, it.k0, it.rows, tid);
         }
+        __syncthreads();
+        float acc[1][8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[0][j] = 0.f;
+        stream_rows<NMM_BF16, 1, U, true>(acc, buf, ss, it.rows / it.rstep, lds + it.rin, it.rstep);
+        __syncthreads();
+        reduce_item<1, true>(p, it, acc, lds, tid);
+        __builtin_amdgcn_s_waitcnt(0);   // this item's stores are complete
+        __syncthreads();
+        unsigned prev = 0;
+        if (tid == 0) {
+            if (it.ks == 1) raise_flag(a, st, it);
+            else prev = __hip_atomic_fetch_add(ticket_of(p, it), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        // the next item's first loads go out before anything waits on the ticket
+        const int nitem = item + static_cast<int>(gridDim.x);
+        int nst = st;
+        Item nit = it;
+        Stream nss = ss;
+        if (nitem < total) {
+            while (nst + 1 < a.n_steps && nitem >= a.first_item[nst + 1]) ++nst;
+            nit = item_of<1>(a.step[nst], nitem - a.first_item[nst], tid);
+            nss = stream_of(a.step[nst], nit);
+            prefetch<U, true>(buf, nss);
+        }
+        if (it.ks > 1) {
+            if (tid == 0) {
+                const int last = prev == unsigned(it.ks - 1);
+                if (last) __hip_atomic_store(ticket_of(p, it), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                s_last = last;
+            }
+            __syncthreads();
+            if (s_last) {
+                gather_panel<1, true>(p, it, tid);
+                __builtin_amdgcn_s_waitcnt(0);
+                __syncthreads();
+                if (tid == 0) raise_flag(a, st, it);
+            }
+        }
+        __syncthreads();   // LDS is reused by the next item
+        item = nitem;
+        st = nst;
+        it = nit;
+        ss = nss;
+    }
+    // leave: the last workgroup out clears the completion flags for the next launch
+    __syncthreads();
+    if (tid == 0) {
+        __builtin_amdgcn_s_waitcnt(0);
+        const unsigned prev = __hip_atomic_fetch_add(a.sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = prev == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (s_last) {
+        for (int i = tid; i < a.flag_off[a.n_steps]; i += kThreads)
+            __hip_atomic_store(a.flags + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (tid == 0) __hip_atomic_store(a.sync + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -520,6 +636,12 @@ void launch_t(const KParams& kp, int64_t grid, size_t lds, hipStream_t s) {
 
 template <int DT, int MT>
 void launch_u(const KParams& kp, int64_t grid, size_t lds, int unroll, hipStream_t s) {
+    if constexpr (MT <= 2) {
+        if (unroll == 16) {
+            launch_t<DT, MT, 16>(kp, grid, lds, s);
+            return;
+        }
+    }
     if (unroll == 8) launch_t<DT, MT, 8>(kp, grid, lds, s);
     else if (unroll == 4) launch_t<DT, MT, 4>(kp, grid, lds, s);
     else launch_t<DT, MT, 2>(kp, grid, lds, s);
@@ -622,33 +744,63 @@ bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n) {
     if (n < 1 || n > kChainMax) return false;
     for (int i = 0; i < n; ++i)
         if (a[i].dt != NMM_BF16 || a[i].M != 1 || a[i].K == 0 || a[i].N == 0 || a[i].batch == 0 ||
-            p[i].mt != 1 || p[i].unroll != 4)
+            p[i].mt != 1 || p[i].unroll != p[0].unroll ||
+            (p[i].unroll != 4 && p[i].unroll != 8 && p[i].unroll != 16))
             return false;
     return true;
 }
 
-nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* const* tickets,
-                        float* const* part, int grid, void* stream) {
+int chain_flags(const GemvArgs* a, const GemvPlan* p, int n) {
+    int64_t total = 0;
+    for (int i = 0; i < n; ++i) total += a[i].batch * p[i].mblocks * (p[i].n_full + (p[i].tail_chunks ? 1 : 0));
+    return static_cast<int>(std::min<int64_t>(total, int64_t(1) << 30));
+}
+
+namespace {
+
+template <int U>
+nmm_status launch_chain_u(const ChainArgs& ca, int grid, size_t lds, hipStream_t s) {
+    // never more workgroups than the device holds at once: the dependency waits rely on it
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, chain_kernel<U>, kThreads, lds) != hipSuccess ||
+        per_cu < 1)
+        return NMM_ERR_HIP;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+        return NMM_ERR_HIP;
+    grid = std::max(1, std::min(grid, per_cu * cus));
+    hipLaunchKernelGGL(chain_kernel<U>, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, ca);
+    return last_launch_status();
+}
+
+}  // namespace
+
+nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
+                        unsigned* const* tickets, float* const* part, int grid, void* stream) {
     ChainArgs ca{};
     ca.n_steps = n;
     ca.sync = sync;
+    ca.flags = flags;
     ca.spin_limit = 1 << 22;   // ~ a second of polling: far beyond any legitimate wait
     ca.sleep_reps = 1;
     if (const char* e = std::getenv("NMM_CHAIN_SLEEP")) ca.sleep_reps = std::max(1, std::atoi(e));
     size_t lds = 0;
-    int first = 0;
+    int first = 0, fo = 0;
     for (int i = 0; i < n; ++i) {
         ca.step[i] = make_params(a[i], p[i], tickets[i], part[i]);
         ca.first_item[i] = first;
+        ca.flag_off[i] = fo;
         first += static_cast<int>(p[i].grid);
-        ca.panels[i] = static_cast<unsigned>(a[i].batch * p[i].mblocks * (p[i].n_full + (p[i].tail_chunks ? 1 : 0)));
+        fo += static_cast<int>(a[i].batch * p[i].mblocks * (p[i].n_full + (p[i].tail_chunks ? 1 : 0)));
         lds = std::max(lds, gemv_lds_bytes(p[i]));
     }
     ca.first_item[n] = first;
+    ca.flag_off[n] = fo;
     grid = std::max(1, std::min(grid, first));
-    hipLaunchKernelGGL(chain_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds,
-                       static_cast<hipStream_t>(stream), ca);
-    return last_launch_status();
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    if (p[0].unroll == 16) return launch_chain_u<16>(ca, grid, lds, s);
+    if (p[0].unroll == 8) return launch_chain_u<8>(ca, grid, lds, s);
+    return launch_chain_u<4>(ca, grid, lds, s);
 }
 
 }  // namespace nmm

@@ -74,7 +74,10 @@ struct GemvArgs {
 
 // Pure host functions (no HIP calls): argument checks and the partition.
 nmm_status validate_gemv(const GemvArgs& a, int path);
-nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p);
+// unroll > 0 requests that many row-steps in flight (2, 4, 8, or 16 for tiles of <= 2 rows);
+// 0 takes the default (NMM_GEMV_UNROLL overrides it).
+nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p,
+                     int unroll = 0);
 nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
 
 // Launchers (defined next to their kernels).  They assume validated arguments.
@@ -84,13 +87,15 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
 nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
 
 // The fused decode chain: n (<= 5) M = 1 bf16 GEMVs in one persistent launch.  `sync` points to
-// the chain's words in the counter block: [1] exited workgroups, [2] error flag (sticky),
-// [3 + i] completed panels of MatMul i; [1] and [3..] are zero before and after a launch.
+// the chain's words in the counter block: [1] exited workgroups, [2] error word (sticky);
+// `flags` to chain_flags() completion flags, one per panel of every MatMul.  [1] and the flags
+// are zero before and after a launch.
 constexpr int kChainSyncWords = 8;
+int chain_flags(const GemvArgs* a, const GemvPlan* p, int n);
 bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n);
 nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 size_t mfma_lds_bytes(const GemvPlan& p);
-nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* const* tickets,
-                        float* const* part, int grid, void* stream);
+nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
+                        unsigned* const* tickets, float* const* part, int grid, void* stream);
 
 }  // namespace nmm

@@ -123,7 +123,8 @@ nmm_status plan_mfma(int64_t M, int64_t K, int64_t N, GemvPlan* p) {
     return NMM_OK;
 }
 
-nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p) {
+nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p,
+                     int unroll) {
     if (!p) return NMM_ERR_NULL;
     if (dt != NMM_F16 && dt != NMM_BF16) return NMM_ERR_DTYPE;
     if (path != NMM_PATH_AUTO && path != NMM_PATH_GEMV && path != NMM_PATH_MFMA) return NMM_ERR_PATH;
@@ -141,12 +142,18 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     q.path = NMM_PATH_GEMV;
     q.mt = m_tile_for(M);
     q.mblocks = static_cast<int>(std::max<int64_t>(1, cdiv(M, q.mt)));
-    q.unroll = static_cast<int>(env_int("NMM_GEMV_UNROLL", 4));   // 4 in flight per wave: measured best
-    if (q.unroll != 2 && q.unroll != 4 && q.unroll != 8) q.unroll = 8;
-    const int U = q.unroll;
-
     const int64_t chunks = cdiv(N, 8);
     const int64_t mats = std::max<int64_t>(batch, 1) * q.mblocks;
+    const int64_t w_bytes = mats * K * chunks * 16;
+    // Measured on MI355X over the decode shapes: for 1- and 2-row tiles and weights up to
+    // 100 MB, 16 row-steps in flight per lane with about one workgroup per compute unit and as
+    // few K-slices as the panel count allows (the split-K gather is a serial tail); larger
+    // weights stream best with 4 in flight and more, split workgroups.
+    const bool deep = q.mt <= 2 && w_bytes <= int64_t(100) << 20;
+    q.unroll = unroll > 0 ? unroll : static_cast<int>(env_int("NMM_GEMV_UNROLL", deep ? 16 : 4));
+    if (q.unroll != 2 && q.unroll != 4 && q.unroll != 8 && q.unroll != 16) q.unroll = 8;
+    if (q.unroll == 16 && q.mt > 2) q.unroll = 8;                  // 16 only for 1- and 2-row tiles
+    const int U = q.unroll;
     // Panel width (measured on MI355X over the decode shapes): as wide as possible, up to 32
     // chunks (64 for 16-row tiles), while the launch still has >= 24 panels in total and every
     // row is split into >= 2 panels; never narrower than 8 chunks (128-byte row segments).
@@ -154,11 +161,14 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     if (min_cw > kPanelChunks || (min_cw & (min_cw - 1))) min_cw = 8;
     int cw = static_cast<int>(env_int("NMM_GEMV_MAXCW", q.mt >= 16 ? 64 : 32));
     if (cw > kPanelChunks || (cw & (cw - 1)) || cw < min_cw) cw = std::max(min_cw, 32);
-    while (cw > min_cw && (mats * cdiv(chunks, cw) < 24 || chunks < 2 * cw)) cw /= 2;
     // Workgroups wanted: one per ~100 KB of W, between 256 and 768 (fewer leave HBM idle; more
-    // only add split-K gather work).
-    const int64_t w_bytes = mats * K * chunks * 16;
-    const int64_t want = env_int("NMM_GEMV_TARGET", std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
+    // only add split-K gather work); 256 for the deep-prefetch plans.
+    const int64_t want = env_int("NMM_GEMV_TARGET",
+                                 deep ? 256 : std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
+    while (cw > min_cw && (mats * cdiv(chunks, cw) < 24 || chunks < 2 * cw)) cw /= 2;
+    // deep plans trade K-slices for narrower panels while twice the panels still fit the target
+    if (deep && U == 16 && !std::getenv("NMM_GEMV_MAXCW"))
+        while (cw > min_cw && 2 * mats * cdiv(chunks, cw) <= want) cw /= 2;
     // K-slices per panel: the power of two nearest want / panels, capped (fewer for tall row
     // tiles, whose partial sums are MT times larger)
     const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", q.mt >= 8 ? 8 : 16);

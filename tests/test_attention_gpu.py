@@ -37,6 +37,15 @@ def test_decode_step_attention_full_size():
     check(q, kv, scale, 576, 512, "attention 128x4096x576/512")
 
 
+@pytest.mark.parametrize("splits,chunk", [("1", "64"), ("8", "32"), ("8", "64"), ("64", "32"), ("64", "64"), ("21", "64")])
+def test_decode_step_attention_every_partition(monkeypatch, splits, chunk):
+    # the span count and chunk size change the summation order, never the result beyond tolerance
+    monkeypatch.setenv("NMM_ATTN_SPLITS", splits)
+    monkeypatch.setenv("NMM_ATTN_CHUNK", chunk)
+    q, kv, scale = syn.attention_case(14, 128, 4096)
+    check(q, kv, scale, 576, 512, f"attention 128x4096, {splits} spans, {chunk}-position chunks")
+
+
 @pytest.mark.parametrize("heads,seq,dqk,dv,ldkv", [
     (20, 1000, 96, 48, 104),      # ragged heads and positions, padded cache rows
     (16, 50, 64, 64, 64),         # one span: no cross-workgroup merge

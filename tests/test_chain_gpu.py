@@ -199,19 +199,24 @@ def test_workspace_garbage_past_counter_block_is_harmless():
     assert_parity(att, ref_att, ref_abs, what="attention on a dirty workspace")
 
 
-def test_fused_chain_matches_separate_launches_and_resets(monkeypatch):
-    # NMM_CHAIN_FUSED=1 runs the chain as one persistent launch; by default it is one launch per
-    # MatMul.  Both use the same plans and summation order, so they must agree bit for bit.
-    step = syn.decode_step()
+@pytest.mark.parametrize("unroll", ["4", "16"])
+@pytest.mark.parametrize("make", [small_step, syn.decode_step], ids=["small", "full"])
+def test_fused_chain_matches_separate_launches_and_resets(monkeypatch, unroll, make):
+    # NMM_CHAIN_FUSED=1 runs the chain as one persistent launch with per-panel dependencies; by
+    # default it is one launch per MatMul.  With the same plans (the same unroll) both sum in the
+    # same order, so they must agree bit for bit, launch after launch.
+    step = make()
     ws = nmm.Workspace()
+    monkeypatch.setenv("NMM_CHAIN_UNROLL", unroll)
+    monkeypatch.setenv("NMM_GEMV_UNROLL", unroll)
     monkeypatch.setenv("NMM_CHAIN_FUSED", "1")
     fused = alloc_chain(step)
-    for _ in range(20):                      # repeated launches: the queue and counters reset
+    for _ in range(20):                      # repeated launches: flags and counters reset
         run_chain(step, fused, workspace=ws)
     torch.cuda.synchronize()
-    sync_words = ws.buf[:32].view(torch.int32).cpu()
-    assert int(sync_words[2]) == 0, "a dependency wait gave up"
-    assert int(sync_words.abs().sum()) == 0, "queue / completion words must return to zero"
+    head = ws.buf[:65536].view(torch.int32).cpu()
+    assert int(head[2]) == 0, "a dependency wait gave up"
+    assert int(head.abs().sum()) == 0, "exit counter, tickets and completion flags must return to zero"
     monkeypatch.setenv("NMM_CHAIN_FUSED", "0")
     sep = alloc_chain(step)
     run_chain(step, sep, workspace=ws)
@@ -219,3 +224,44 @@ def test_fused_chain_matches_separate_launches_and_resets(monkeypatch):
     for k in nmm.CHAIN_BUFFERS[6:]:
         assert torch.equal(fused[k], sep[k]), k
     check_chain_stepwise(step, fused)
+
+
+def test_fused_chain_concurrent_with_attention_and_in_graphs(monkeypatch):
+    step = small_step(9)
+    q, kv, scale = syn.attention_case(8, 128, 4096)
+    qd, kvd = dev16(q, syn.BF16), dev16(kv, syn.BF16)
+    monkeypatch.setenv("NMM_CHAIN_FUSED", "1")
+    ref = alloc_chain(step)
+    run_chain(step, ref)
+    att_ref = torch.empty((128, 512), device="cuda")
+    nmm.nmm_latent_attention(qd, kvd, att_ref, scale)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Stream(), torch.cuda.Stream()
+    ws_a, ws_b = nmm.Workspace(), nmm.Workspace()
+    bufs = alloc_chain(step)
+    att = torch.empty((128, 512), device="cuda")
+    run_chain(step, bufs, stream=a, workspace=ws_a)           # sizes the workspaces
+    nmm.nmm_latent_attention(qd, kvd, att, scale, stream=b, workspace=ws_b)
+    torch.cuda.synchronize()
+    cap = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cap):
+        start = torch.cuda.Event()
+        start.record(cap)
+        a.wait_event(start)
+        b.wait_event(start)
+        run_chain(step, bufs, stream=a, workspace=ws_a)
+        nmm.nmm_latent_attention(qd, kvd, att, scale, stream=b, workspace=ws_b)
+        cap.wait_stream(a)
+        cap.wait_stream(b)
+    for rep in range(4):
+        for k in ("y", "down_f32", "q_f32", "lat_f32", "o_f32"):
+            bufs[k].fill_(float("nan"))
+        att.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for k in nmm.CHAIN_BUFFERS[6:]:
+            assert torch.equal(bufs[k], ref[k]), (rep, k)
+        assert torch.equal(att, att_ref), rep
+        assert int(ws_a.buf[:65536].view(torch.int32).abs().sum()) == 0, rep
