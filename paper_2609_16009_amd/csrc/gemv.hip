@@ -138,8 +138,11 @@ __device__ __forceinline__ void prefetch(i32x4 (&buf)[U], const Stream& st) {
 }
 
 // Consume `nsteps` row-steps (a multiple of U, the first U already in `buf`), keeping U loads in
-// flight: the load for step s+U is issued right after step s's data is taken.  The steady-state
-// loop has no branches, so the compiler's wait counters track each load individually.
+// flight: step s is multiplied and its register then takes the load for step s+U.  Consuming a
+// slot before reloading it lets every slot stay in one register across iterations (a load into
+// a fresh register would have to be copied back at the end of the iteration, which waits for
+// it), and a scheduling barrier keeps each reload next to its multiply.  The steady-state loop
+// has no branches, so the wait counters track each load.
 template <int DT, int MT, int U, bool GUARD>
 __device__ __forceinline__ void stream_rows(float (&acc)[MT][8], i32x4 (&buf)[U], const Stream& st,
                                             int nsteps, const float* __restrict__ xs, int xs_step) {
@@ -147,10 +150,12 @@ __device__ __forceinline__ void stream_rows(float (&acc)[MT][8], i32x4 (&buf)[U]
     for (; s + U < nsteps; s += U) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const i32x4 cur = buf[u];
+            fma_chunk<DT, MT>(acc, buf[u], xs + (s + u) * xs_step);
             const int sn = s + U + u;
             buf[u] = load_chunk<GUARD>(st.rsrc, st.off + sn * st.step_bytes, st.row + sn * st.rstep < st.K);
-            fma_chunk<DT, MT>(acc, cur, xs + (s + u) * xs_step);
+            // keep the reload here: sunk to the end of the iteration it would leave nothing in
+            // flight while the other slots are multiplied
+            __builtin_amdgcn_sched_barrier(0);
         }
     }
 #pragma unroll

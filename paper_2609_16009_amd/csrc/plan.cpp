@@ -145,26 +145,29 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     const int64_t chunks = cdiv(N, 8);
     const int64_t mats = std::max<int64_t>(batch, 1) * q.mblocks;
     const int64_t w_bytes = mats * K * chunks * 16;
-    // Measured on MI355X over the decode shapes: for 1- and 2-row tiles and weights up to
-    // 100 MB, 16 row-steps in flight per lane with about one workgroup per compute unit and as
-    // few K-slices as the panel count allows (the split-K gather is a serial tail); larger
-    // weights stream best with 4 in flight and more, split workgroups.
-    const bool deep = q.mt <= 2 && w_bytes <= int64_t(100) << 20;
-    q.unroll = unroll > 0 ? unroll : static_cast<int>(env_int("NMM_GEMV_UNROLL", deep ? 16 : 4));
+    // Measured on MI355X over the decode shapes: 1- and 2-row tiles stream best with about one
+    // workgroup per compute unit -- for weights up to 100 MB with 16 row-steps in flight per lane
+    // and as few K-slices as the panel count allows (the split-K gather is a serial tail), for
+    // larger weights with 8 in flight and panels up to 512 columns.  Taller tiles keep 4 in
+    // flight and more workgroups.
+    const bool narrow_m = q.mt <= 2;
+    const bool deep = narrow_m && w_bytes <= int64_t(100) << 20;
+    q.unroll = unroll > 0 ? unroll : static_cast<int>(env_int("NMM_GEMV_UNROLL", deep ? 16 : narrow_m ? 8 : 4));
     if (q.unroll != 2 && q.unroll != 4 && q.unroll != 8 && q.unroll != 16) q.unroll = 8;
     if (q.unroll == 16 && q.mt > 2) q.unroll = 8;                  // 16 only for 1- and 2-row tiles
     const int U = q.unroll;
     // Panel width (measured on MI355X over the decode shapes): as wide as possible, up to 32
-    // chunks (64 for 16-row tiles), while the launch still has >= 24 panels in total and every
-    // row is split into >= 2 panels; never narrower than 8 chunks (128-byte row segments).
+    // chunks (64 for 16-row tiles and for 1-2-row tiles of weights over 100 MB), while the launch
+    // still has >= 24 panels in total and every row is split into >= 2 panels; never narrower
+    // than 8 chunks (128-byte row segments).
     int min_cw = static_cast<int>(env_int("NMM_GEMV_MINCW", 8));
     if (min_cw > kPanelChunks || (min_cw & (min_cw - 1))) min_cw = 8;
-    int cw = static_cast<int>(env_int("NMM_GEMV_MAXCW", q.mt >= 16 ? 64 : 32));
+    int cw = static_cast<int>(env_int("NMM_GEMV_MAXCW", (q.mt >= 16 || (narrow_m && !deep)) ? 64 : 32));
     if (cw > kPanelChunks || (cw & (cw - 1)) || cw < min_cw) cw = std::max(min_cw, 32);
     // Workgroups wanted: one per ~100 KB of W, between 256 and 768 (fewer leave HBM idle; more
     // only add split-K gather work); 256 for the deep-prefetch plans.
     const int64_t want = env_int("NMM_GEMV_TARGET",
-                                 deep ? 256 : std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
+                                 narrow_m ? 256 : std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
     while (cw > min_cw && (mats * cdiv(chunks, cw) < 24 || chunks < 2 * cw)) cw /= 2;
     // deep plans trade K-slices for narrower panels while twice the panels still fit the target
     if (deep && U == 16 && !std::getenv("NMM_GEMV_MAXCW"))
@@ -198,8 +201,12 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     int64_t ks_want = 1;
     {
         const double ratio = double(want) / double(std::max<int64_t>(panels_all, 1));
-        while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;   // nearest power of two
-        ks_want = std::min(ks_want, ks_cap);
+        if (env_int("NMM_GEMV_KS_ANY", 0) > 0) {
+            ks_want = std::max<int64_t>(1, std::min<int64_t>(ks_cap, int64_t(ratio + 0.5)));
+        } else {
+            while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;   // nearest power of two
+            ks_want = std::min(ks_want, ks_cap);
+        }
     }
 
     auto slice = [&](int64_t rstep, int& ks, int& rows) {
