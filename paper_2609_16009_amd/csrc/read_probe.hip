@@ -1,5 +1,6 @@
 // Read-bandwidth calibration: stream a buffer once with the GEMV's load instruction (16-byte,
-// non-temporal buffer loads, U in flight per lane) and fold it into one checksum per workgroup.
+// non-temporal buffer loads, U in flight per lane, U in {1, 2, 4, 8, 16}) and fold it into one
+// checksum per workgroup.
 // It measures how fast this GPU can read HBM with that access pattern, the practical ceiling
 // the GEMV roofline fractions are compared against.
 #include <hip/hip_runtime.h>
@@ -26,12 +27,25 @@ __global__ __launch_bounds__(256) void read_probe_kernel(const uint8_t* buf, uin
         const uint64_t wn = (chunks - w0 < kWin) ? chunks - w0 : kWin;
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<uint8_t*>(buf + w0 * 16), (short)0, int(wn * 16), kRsrcWord3);
-        for (uint64_t c = t; c < wn; c += nthreads * U) {
+        // this thread's chunks of the window are t, t + nthreads, ...; U of them stay in flight:
+        // a slot is folded in and then reloaded in place (no register copies, no drain)
+        const uint64_t n_t = (t < wn) ? (wn - t + nthreads - 1) / nthreads : 0;
+        const uint64_t groups = ((wn + nthreads - 1) / nthreads + U - 1) / U;   // the same for every lane
+        auto load = [&](uint64_t j) {
+            return __builtin_amdgcn_raw_buffer_load_b128(r, j < n_t ? uint32_t((t + j * nthreads) * 16) : 0x80000000u, 0,
+                                                         kLoadNT);
+        };
+        if (groups) {
             i32x4 v[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint64_t cc = c + u * nthreads;
-                v[u] = __builtin_amdgcn_raw_buffer_load_b128(r, cc < wn ? uint32_t(cc * 16) : 0x80000000u, 0, kLoadNT);
+            for (int u = 0; u < U; ++u) v[u] = load(u);
+            for (uint64_t g = 1; g < groups; ++g) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    acc ^= uint32_t(v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3]);
+                    v[u] = load(g * U + u);
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) acc ^= uint32_t(v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3]);
@@ -65,6 +79,7 @@ extern "C" nmm_status nmm_read_probe(const void* buf, size_t bytes, uint32_t* ou
         case 2: hipLaunchKernelGGL(nmm::read_probe_kernel<2>, g, blk, 0, s, b, chunks, out); break;
         case 4: hipLaunchKernelGGL(nmm::read_probe_kernel<4>, g, blk, 0, s, b, chunks, out); break;
         case 8: hipLaunchKernelGGL(nmm::read_probe_kernel<8>, g, blk, 0, s, b, chunks, out); break;
+        case 16: hipLaunchKernelGGL(nmm::read_probe_kernel<16>, g, blk, 0, s, b, chunks, out); break;
         default: return NMM_ERR_ARG;
     }
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
