@@ -105,10 +105,10 @@ typedef __attribute__((address_space(3))) void lds_void;
 // chunk is viewed as CH rows of cpr + 1 slots (one slot of padding per row); slot s of the
 // chunk holds piece (s / (cpr + 1), s % (cpr + 1)) of the rows c0 .. c0 + CH - 1, and padding
 // slots and positions past the span read zeros.  Wave w issues instructions w, w + 4, ...
-template <int CH>
+template <int CH, int SPR>
 __device__ __forceinline__ void stage_chunk(uint16_t* buf, __amdgpu_buffer_rsrc_t kvr, const AttnParams& p, int c0,
                                             int s_end, int wave, int lane) {
-    const int spr = p.cols / 8 + 1;            // slots per row
+    const int spr = SPR ? SPR : p.cols / 8 + 1;   // slots per row (a constant for the fixed shape)
     const int slots = CH * spr;
     for (int ins = wave; ins * 64 < slots; ins += 4) {
         const int sl = ins * 64 + lane;
@@ -130,6 +130,7 @@ __global__ __launch_bounds__(kAThreads) __attribute__((amdgpu_waves_per_eu(1, 1)
 void attention_kernel(const AttnParams p) {
     __shared__ __attribute__((aligned(16))) uint16_t kv_a[CH * PMAX];
     __shared__ __attribute__((aligned(16))) uint16_t kv_b[CH * PMAX];
+    constexpr int SPR = EXACT ? (KS * 32 > NT * 16 ? KS * 32 : NT * 16) / 8 + 1 : 0;   // LDS slots per row
     constexpr int CT = CH / 16;            // score tiles per chunk
     constexpr int PK = CH / 32;            // P.V k-steps per chunk
 
@@ -165,7 +166,7 @@ void attention_kernel(const AttnParams p) {
         for (int u = 0; u < KS; ++u)
             qf[u] = __builtin_amdgcn_raw_buffer_load_b128(qr, (ok && u < ksteps) ? base + 64 * u : kOutOfRange, 0, 0);
     }
-    stage_chunk<CH>(kv_a, kvr, p, s_begin, s_end, wave, lane);
+    stage_chunk<CH, SPR>(kv_a, kvr, p, s_begin, s_end, wave, lane);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
@@ -175,10 +176,9 @@ void attention_kernel(const AttnParams p) {
     float m_run = -INFINITY, l_run = 0.f;   // this lane's head (column j), in log2 units
     const int a4 = j >> 2, b4 = j & 3;
 
-    // one chunk: the next chunk streams into `nxt` while `cur` is computed
+    // one chunk: computed from `cur`; the next chunk streams into `nxt` meanwhile
     auto chunk = [&](const uint16_t* cur, uint16_t* nxt, int ck) {
         const int c0 = s_begin + ck * CH;
-        if (ck + 1 < nchunks) stage_chunk<CH>(nxt, kvr, p, c0 + CH, s_end, wave, lane);
 
         // ---- S^T[CH positions][16 heads] = K . Q^T: lane (g, j) gets positions 16t + 4g + i of
         // head j.  The K fragments of step u + 1 are read while step u multiplies.
@@ -202,6 +202,10 @@ void attention_kernel(const AttnParams p) {
                     s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[u & 1][t]), as_bf16x8(qf[u]), s[t], 0, 0, 0);
             }
         }
+
+        // the next chunk's rows stream into the other buffer during the softmax and P.V (every
+        // wave finished reading that buffer before the last barrier)
+        if (ck + 1 < nchunks) stage_chunk<CH, SPR>(nxt, kvr, p, c0 + CH, s_end, wave, lane);
 
         // ---- online softmax of head j over the chunk
         float mx = -INFINITY;
@@ -292,56 +296,54 @@ void attention_kernel(const AttnParams p) {
 
 // Merge the spans of each head in span order:
 //   out = sum_s w_s O_s,  w_s = 2^(m_s - M) / sum_q 2^(m_q - M) l_q,  M = max_s m_s.
-// A workgroup owns one head block (64 heads) and 16 output columns.  It stages the block's
-// (max, sum) pairs of every span in LDS and turns them into weights (one thread per head); then
-// each thread combines 4 columns of one head, issuing the loads of up to 16 spans at once.
-constexpr int kMergeCols = 16;
+// One output per thread: a workgroup owns 4 heads x 64 columns, so 64 threads read one
+// 256-byte segment of a (head, span) row.  The 4 heads' weights are computed once (one thread
+// per head) into LDS; every thread then issues the loads of up to 16 spans at once.
+constexpr int kMergeCols = 64;
+constexpr int kMergeHeads = kAThreads / kMergeCols;   // 4
 constexpr int kMergeBatch = 16;
 constexpr int kMergeMaxSpans = 64;
 __global__ __launch_bounds__(kAThreads) void attention_merge_kernel(const AttnParams p) {
-    __shared__ float mls[kMergeMaxSpans * kHB * 2];   // [span][head][m, l]; m becomes the weight
-    const int n_cb = p.dv / kMergeCols;
-    const int hb = blockIdx.x / n_cb, cb = blockIdx.x - hb * n_cb;
+    __shared__ float wgt[kMergeMaxSpans * kMergeHeads];   // [span][head of the group]
+    const int n_cb = (p.dv + kMergeCols - 1) / kMergeCols;
+    const int hq = blockIdx.x / n_cb, cb = blockIdx.x - hq * n_cb;
     const int tid = threadIdx.x;
-    const float* ml = p.part_ml + int64_t(hb) * p.nsp * (kHB * 2);
-    const int n_ml = p.nsp * kHB * 2;
-    for (int i0 = 0; i0 < n_ml; i0 += kAThreads * 8) {
-        float v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = (i0 + u * kAThreads + tid < n_ml) ? ml[i0 + u * kAThreads + tid] : 0.f;
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (i0 + u * kAThreads + tid < n_ml) mls[i0 + u * kAThreads + tid] = v[u];
-    }
-    __syncthreads();
-    if (tid < kHB) {
+    const int h0 = hq * kMergeHeads;                      // a multiple of 4: never crosses a head block
+    const int hb = h0 / kHB, r0 = h0 - hb * kHB;
+    if (tid < kMergeHeads) {
+        const float* ml = p.part_ml + (int64_t(hb) * p.nsp * kHB + r0 + tid) * 2;
+        const int64_t st = kHB * 2;
         float M = -INFINITY;
-        for (int q = 0; q < p.nsp; ++q) M = fmaxf(M, mls[(q * kHB + tid) * 2]);
+#pragma unroll 8
+        for (int q = 0; q < p.nsp; ++q) M = fmaxf(M, ml[q * st]);
         float den = 0.f;
+#pragma unroll 8
         for (int q = 0; q < p.nsp; ++q) {
-            const float mq = mls[(q * kHB + tid) * 2];
+            const float mq = ml[q * st];
             const float w = (mq == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mq - M);
-            den += w * mls[(q * kHB + tid) * 2 + 1];
-            mls[(q * kHB + tid) * 2] = w;
+            den += w * ml[q * st + 1];
+            wgt[q * kMergeHeads + tid] = w;
         }
-        for (int q = 0; q < p.nsp; ++q) mls[(q * kHB + tid) * 2] /= den;
+        const float inv = 1.f / den;
+#pragma unroll 8
+        for (int q = 0; q < p.nsp; ++q) wgt[q * kMergeHeads + tid] *= inv;
     }
     __syncthreads();
-    const int r = tid >> 2, n = cb * kMergeCols + 4 * (tid & 3);   // head r of the block, 4 columns
-    const float* src = p.part_o + (int64_t(hb) * p.nsp * kHB + r) * p.dv + n;
+    const int i = tid / kMergeCols, n = cb * kMergeCols + (tid % kMergeCols);
+    const int h = h0 + i;
+    if (h >= p.heads || n >= p.dv) return;
+    const float* src = p.part_o + (int64_t(hb) * p.nsp * kHB + r0 + i) * p.dv + n;
     const int64_t step = int64_t(kHB) * p.dv;
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    float acc = 0.f;
     for (int q0 = 0; q0 < p.nsp; q0 += kMergeBatch) {
-        f32x4 v[kMergeBatch];
+        float v[kMergeBatch];
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) v[u] = (q0 + u < p.nsp) ? src[(q0 + u) * step] : 0.f;
 #pragma unroll
         for (int u = 0; u < kMergeBatch; ++u)
-            v[u] = (q0 + u < p.nsp) ? *reinterpret_cast<const f32x4*>(src + (q0 + u) * step) : f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int u = 0; u < kMergeBatch; ++u)
-            if (q0 + u < p.nsp) acc += mls[((q0 + u) * kHB + r) * 2] * v[u];
+            if (q0 + u < p.nsp) acc += wgt[(q0 + u) * kMergeHeads + i] * v[u];
     }
-    const int h = hb * kHB + r;
-    if (h < p.heads) *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + n) = acc;
+    p.out[int64_t(h) * p.ldo + n] = acc;
 }
 
 struct AttnPlan {
@@ -460,7 +462,8 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
         st = launch_attention<32, 32, 32, 1032, false>(p, grid, s);
     if (st != NMM_OK) return st;
     if (a.nsp > 1) {
-        hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(a.n_hb * (d_v / kMergeCols))),
+        const int64_t merge_grid = ((heads + kMergeHeads - 1) / kMergeHeads) * ((d_v + kMergeCols - 1) / kMergeCols);
+        hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(merge_grid)),
                            dim3(kAThreads), 0, s, p);
         if (hipGetLastError() != hipSuccess) return NMM_ERR_HIP;
     }
