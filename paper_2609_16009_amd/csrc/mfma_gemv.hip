@@ -7,12 +7,15 @@
 // Section III-A; Conditions 4-5, Section V) are about where the split between the two units
 // lies; on MI355X it is measured, and nmm_gemv's AUTO path switches here above it.
 //
-//  * A workgroup (4 waves) owns one 128-column panel of W and one K-slice.  It stages its x
-//    rows (bf16/fp16, row-major, the MFMA A operand) in LDS once.
-//  * W streams in stages of 64 rows x 128 columns (16 KB): each thread loads four 16-byte chunks
-//    one stage ahead, stores them to a double-buffered LDS tile, and the waves read their
-//    v_mfma_f32_16x16x32 B operands back with ds_read_b64_tr_b16, the gfx950 transposing LDS
-//    read (the B operand needs 8 consecutive k of one column; W rows hold consecutive columns).
+//  * A workgroup (4 waves) owns one 128-column panel of W and one K-slice.
+//  * W streams in stages of 64 rows x 128 columns (16 KB) together with the stage's 64 k of the
+//    x tile (the MFMA A operand, 2-4 KB): each thread keeps two stages of 16-byte chunks in
+//    flight, stores the oldest to a double-buffered LDS stage and reloads its registers in
+//    place.  The waves read their v_mfma_f32_16x16x32 B operands back with ds_read_b64_tr_b16,
+//    the gfx950 transposing LDS read (the B operand needs 8 consecutive k of one column; W rows
+//    hold consecutive columns).  x travels with W instead of being staged for the whole slice
+//    up front, so no workgroup waits for its x before its W stream starts and the slice length
+//    is not bounded by LDS.
 //  * Wave w owns the column tiles 2w and 2w+1 of the panel, so no cross-wave reduction is needed.
 //  * K-slices are combined exactly like the GEMV's: device-scope atomic partial stores, a
 //    ticket per panel, and the last workgroup sums the slices in order.
@@ -39,6 +42,8 @@ constexpr int kRsrcWord3 = 0x00020000;
 constexpr int kLoadNT = 2;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kWStride = kMfmaPanelCols + 8;   // LDS row stride of a W stage (elements)
+constexpr int kXStride = kMfmaStageRows + 8;   // LDS row stride of an x stage (elements)
+constexpr int kMfmaDepth = 2;                  // stages in flight per thread (2-4 measured alike)
 
 struct MParams {
     const uint16_t* x;
@@ -51,7 +56,6 @@ struct MParams {
     int M, K, N;
     uint32_t row_bytes, w_extent;
     int panels, ks, rows, items, mblocks;
-    int x_stride;   // LDS row stride of the staged x (elements)
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
@@ -82,12 +86,15 @@ __device__ __forceinline__ i32x4 load_b(const uint16_t* wst, int row0, int col0,
     return i32x4{int(lo.x), int(lo.y), int(hi.x), int(hi.y)};
 }
 
-template <int DT, int MT>
+template <int DT, int MT, int D>
 __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
+    // two stage buffers, each a W tile [64][kWStride] followed by an x tile [MT][kXStride]
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
     __shared__ int s_last;
     constexpr int MTILES = MT / 16;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int kStage = kMfmaStageRows * kWStride + MT * kXStride;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = lane >> 4, j = lane & 15;
 
     const uint32_t bid = blockIdx.x;
@@ -95,53 +102,40 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
     const int mb = static_cast<int>(bid / uint32_t(p.items));
     const int panel = item / p.ks, slice = item - panel * p.ks;
     const int m0 = mb * MT, k0 = slice * p.rows, n0 = panel * kMfmaPanelCols;
-    const int stages = p.rows / kMfmaStageRows;
+    const int stages = (min(p.rows, p.K - k0) + kMfmaStageRows - 1) / kMfmaStageRows;
+    const int mrows = min(MT, p.M - m0);
 
-    uint16_t* x_lds = smem;                                   // [MT][x_stride]
-    uint16_t* w_lds = smem + MT * p.x_stride;                 // 2 x [64][kWStride]
-
-    // ---- W stage loads: thread t takes chunk t%16 of rows t/16 + 16q (q < 4)
+    // ---- W: thread t takes chunk t%16 of rows t/16 + 16q (q < 4) of a stage.
     const __amdgpu_buffer_rsrc_t wr = make_rsrc(p.w, p.w_extent);
     const int wc = tid & 15, wr0 = tid >> 4;
     const int chunks_valid = min(16, (p.N - n0 + 7) / 8);
-    auto w_off = [&](int stage, int q) -> uint32_t {
-        const int row = k0 + stage * kMfmaStageRows + wr0 + 16 * q;
-        return (row < p.K && wc < chunks_valid) ? uint32_t(row) * p.row_bytes + uint32_t(n0 / 8 + wc) * 16u : kOutOfRange;
+    auto w_off = [&](int st, int q) -> uint32_t {
+        const int row = k0 + st * kMfmaStageRows + wr0 + 16 * q;
+        return (st < stages && row < p.K && wc < chunks_valid) ? uint32_t(row) * p.row_bytes + uint32_t(n0 / 8 + wc) * 16u
+                                                              : kOutOfRange;
     };
-    i32x4 wreg[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) wreg[q] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off(0, q), 0, kLoadNT);
+    // ---- x: thread t takes chunk t%8 (8 k) of row t/8 of the stage's 64 k; rows past M or
+    // chunks past K read zeros, and elements past K inside the last chunk are cleared on the way
+    // to LDS (the padding of a row is read but never used).
+    const int xm = tid >> 3, xc = tid & 7;
+    const __amdgpu_buffer_rsrc_t xr =
+        make_rsrc(p.x + int64_t(m0) * p.ldx, uint32_t(((mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2));
+    const int xk_left = p.K - (k0 + 8 * xc);   // elements of this thread's chunk of stage 0 inside K
+    auto x_off = [&](int st) -> uint32_t {
+        const int left = xk_left - st * kMfmaStageRows;
+        return (st < stages && xm < mrows && left > 0) ? uint32_t((xm * p.ldx + k0 + st * kMfmaStageRows + 8 * xc) * 2)
+                                                      : kOutOfRange;
+    };
 
-    // ---- x rows m0.. (zero past M or K), staged once as the A operand; every load is issued
-    // before any is used
-    {
-        const int cpr = p.rows / 8;
-        const int mrows = min(MT, p.M - m0);
-        const __amdgpu_buffer_rsrc_t xr =
-            make_rsrc(p.x + int64_t(m0) * p.ldx, uint32_t(((mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2));
-        constexpr int kPer = kMfmaXChunks / kThreads;    // x chunks per thread (upper bound)
-        i32x4 v[kPer];
+    // D stages in flight: the registers of stage s go to LDS and are then reloaded with stage
+    // s + D in place (no register copies, so the stream never drains); past the slice they read
+    // zeros without touching memory.
+    i32x4 wreg[D][4], xreg[D];
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int i = tid + u * kThreads;
-            const int m = i / cpr, c = i - m * cpr, k = k0 + 8 * c;
-            const bool ok = i < MT * cpr && m < mrows && k < p.K;
-            v[u] = __builtin_amdgcn_raw_buffer_load_b128(xr, ok ? uint32_t((int64_t(m) * p.ldx + k) * 2) : kOutOfRange, 0, 0);
-        }
+    for (int d = 0; d < D; ++d) {
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int i = tid + u * kThreads;
-            if (i < MT * cpr) {
-                const int m = i / cpr, c = i - m * cpr, k = k0 + 8 * c;
-                i32x4 val = v[u];
-                if (k + 8 > p.K) {   // zero the elements past K within the last chunk
-#pragma unroll
-                    for (int t = 0; t < 8; ++t)
-                        if (k + t >= p.K) val[t >> 1] &= (t & 1) ? 0x0000FFFF : 0xFFFF0000;
-                }
-                *reinterpret_cast<i32x4*>(x_lds + m * p.x_stride + 8 * c) = val;
-            }
-        }
+        for (int q = 0; q < 4; ++q) wreg[d][q] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off(d, q), 0, kLoadNT);
+        xreg[d] = __builtin_amdgcn_raw_buffer_load_b128(xr, x_off(d), 0, 0);
     }
 
     f32x4 acc[MTILES][2];
@@ -150,23 +144,35 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int s = 0; s < stages; ++s) {
-        uint16_t* wst = w_lds + (s & 1) * (kMfmaStageRows * kWStride);
+    // one stage: registers to LDS buffer (s & 1), reload with stage s + D, then the MFMAs.  A
+    // wave that writes buffer (s & 1) has passed the barrier of stage s - 1, so every wave has
+    // finished reading stage s - 2 from it.
+    auto stage = [&](int s, i32x4 (&wd)[4], i32x4& xd) {
+        uint16_t* wst = smem + (s & 1) * kStage;
+        uint16_t* xst = wst + kMfmaStageRows * kWStride;
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            *reinterpret_cast<i32x4*>(wst + (wr0 + 16 * q) * kWStride + 8 * wc) = wreg[q];
-        if (s + 1 < stages) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) wreg[q] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off(s + 1, q), 0, kLoadNT);
+        for (int q = 0; q < 4; ++q) {
+            *reinterpret_cast<i32x4*>(wst + (wr0 + 16 * q) * kWStride + 8 * wc) = wd[q];
+            wd[q] = __builtin_amdgcn_raw_buffer_load_b128(wr, w_off(s + D, q), 0, kLoadNT);
         }
+        if (tid < MT * 8) {
+            i32x4 v = xd;
+            if (p.K & 7) {
+                const int left = xk_left - s * kMfmaStageRows;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] &= (2 * e + 1 < left) ? -1 : (2 * e < left ? 0x0000FFFF : 0);
+            }
+            *reinterpret_cast<i32x4*>(xst + xm * kXStride + 8 * xc) = v;
+        }
+        xd = __builtin_amdgcn_raw_buffer_load_b128(xr, x_off(s + D), 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
 #pragma unroll
         for (int kk = 0; kk < kMfmaStageRows / 32; ++kk) {
-            const int kx = s * kMfmaStageRows + 32 * kk;   // k offset within the slice
             i32x4 a[MTILES];
 #pragma unroll
             for (int mt = 0; mt < MTILES; ++mt)
-                a[mt] = *reinterpret_cast<const i32x4*>(x_lds + (16 * mt + j) * p.x_stride + kx + 8 * g);
+                a[mt] = *reinterpret_cast<const i32x4*>(xst + (16 * mt + j) * kXStride + 32 * kk + 8 * g);
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const i32x4 b = load_b<DT>(wst, 32 * kk, 16 * (2 * wave + t), g, j);
@@ -174,7 +180,15 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
                 for (int mt = 0; mt < MTILES; ++mt) acc[mt][t] = mfma<DT>(a[mt], b, acc[mt][t]);
             }
         }
+    };
+    int s0 = 0;
+    for (; s0 + D <= stages; s0 += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) stage(s0 + d, wreg[d], xreg[d]);
     }
+#pragma unroll
+    for (int d = 0; d + 1 < D; ++d)
+        if (s0 + d < stages) stage(s0 + d, wreg[d], xreg[d]);
 
     // ---- outputs: lane (g, j) holds rows 4g+i of its tiles, column j
     const int64_t pbase = ((int64_t(mb) * p.panels + panel) * p.ks) * (int64_t(MT) * kMfmaPanelCols);
@@ -247,13 +261,13 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
 
 template <int DT, int MT>
 void launch_mt(const MParams& mp, int64_t grid, size_t lds, hipStream_t s) {
-    hipLaunchKernelGGL((mfma_gemv_kernel<DT, MT>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, mp);
+    hipLaunchKernelGGL((mfma_gemv_kernel<DT, MT, kMfmaDepth>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, mp);
 }
 
 }  // namespace
 
 size_t mfma_lds_bytes(const GemvPlan& p) {
-    return (size_t(p.mt) * (p.rows_full + 8) + 2 * kMfmaStageRows * kWStride) * 2;
+    return size_t(2) * (kMfmaStageRows * kWStride + p.mt * kXStride) * 2;
 }
 
 nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream) {
@@ -275,7 +289,6 @@ nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
     mp.rows = p.rows_full;
     mp.items = p.items;
     mp.mblocks = p.mblocks;
-    mp.x_stride = p.rows_full + 8;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const size_t lds = mfma_lds_bytes(p);
     if (a.dt == NMM_BF16) {

@@ -36,8 +36,8 @@ constexpr int64_t kTicketBytes = kMaxTickets * 4;
 // Matrix-core path (mfma_gemv.hip): 128-column panels, W staged 64 rows at a time.
 constexpr int kMfmaPanelCols = 128;
 constexpr int kMfmaStageRows = 64;
-constexpr int kMfmaXChunks = 2048;         // staged x chunks per workgroup: MT * rows / 8 <= this
-constexpr int kMfmaMinMDefault = 4;        // AUTO uses the matrix cores from this many rows on
+constexpr int kMfmaTargetGrid = 256;      // the matrix-core plan splits K until about this many workgroups
+constexpr int kMfmaMinMDefault = 3;        // AUTO uses the matrix cores from this many rows on
 
 struct GemvPlan {
     int path = NMM_PATH_GEMV;

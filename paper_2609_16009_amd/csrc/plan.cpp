@@ -76,7 +76,9 @@ nmm_status validate_gemv(const GemvArgs& a, int path) {
 }
 
 // The matrix-core partition: 128-column panels, K-slices of whole 64-row stages, x tiles of
-// 16 or 32 rows.  The split count follows the GEMV's rule (about one workgroup per 100 KB of W).
+// 16 or 32 rows.  Splits are added only until the grid reaches about 256 workgroups: every
+// workgroup pays a fixed start-up latency and split-K tail, so one round of long streams beats
+// more, shorter ones (measured on the W_UQ, W_O and down shapes).
 nmm_status plan_mfma(int64_t M, int64_t K, int64_t N, GemvPlan* p) {
     GemvPlan q;
     q.path = NMM_PATH_MFMA;
@@ -90,22 +92,14 @@ nmm_status plan_mfma(int64_t M, int64_t K, int64_t N, GemvPlan* p) {
         return NMM_OK;
     }
     const int64_t panels = int64_t(q.mblocks) * q.n_full;
-    const int64_t w_bytes = int64_t(q.mblocks) * K * cdiv(N, 8) * 16;
-    const int64_t want = env_int("NMM_GEMV_TARGET", std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
+    const int64_t want = env_int("NMM_GEMV_TARGET", kMfmaTargetGrid);
     const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", 16);
     int64_t ks_want = 1;
     const double ratio = double(want) / double(panels);
     while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;
-    // rows whose x tile fits both the per-thread staging bound and, with the double-buffered W
-    // stage, 64 KB of LDS
-    const int64_t lds_rows = ((32768 - 2 * kMfmaStageRows * (kMfmaPanelCols + 8)) / q.mt - 8) / kMfmaStageRows * kMfmaStageRows;
-    const int64_t cap = std::min<int64_t>(kMfmaXChunks * 8 / q.mt, lds_rows);
-    int64_t r = std::min<int64_t>(rup(cdiv(K, ks_want), kMfmaStageRows), cap);
+    int64_t r = rup(cdiv(K, ks_want), kMfmaStageRows);
     int64_t k = cdiv(K, r);
-    r = std::min<int64_t>(cap, rup(cdiv(K, k), kMfmaStageRows));
-    k = cdiv(K, r);
     if (panels > kMaxTickets) {
-        if (rup(K, kMfmaStageRows) > cap) return NMM_ERR_SHAPE;
         k = 1;
         r = rup(K, kMfmaStageRows);
     }

@@ -112,12 +112,26 @@ def test_mfma_launch_stays_in_bounds(M, K, N, ldx, ldw):
     mt, rows, ks, panels = p["m_tile"], p["rows_full"], p["split_k_full"], p["n_full_panels"]
     assert mt in (16, 32) and rows % 64 == 0 and ks * rows >= K and (ks - 1) * rows < K
     assert panels * 128 >= N and (panels - 1) * 128 < N
-    # LDS: x tile [mt][rows + 8] + two W stages [64][136], bf16
-    assert (mt * (rows + 8) + 2 * 64 * 136) * 2 <= 65536
-    assert mt * rows // 8 <= 2048
+    # LDS: two stage buffers, each a W tile [64][136] and an x tile [mt][72], 16-bit elements
+    assert 2 * (64 * 136 + mt * 72) * 2 <= 65536
     extent = ((K - 1) * ldw + (N + 7) // 8 * 8) * 2
     tid = np.arange(256)
     wc, wr0 = tid & 15, tid >> 4
+    xm, xc = tid >> 3, tid & 7
+    for mb in {0, p["m_blocks"] - 1}:
+        m0 = mb * mt
+        mrows = min(mt, M - m0)
+        x_extent = ((mrows - 1) * ldx + (K + 7) // 8 * 8) * 2
+        for sl in {0, ks - 1}:
+            k0 = sl * rows
+            stages = (min(rows, K - k0) + 63) // 64
+            for st in range(stages):
+                k = k0 + st * 64 + 8 * xc
+                ok = (xm < mrows) & (k < K)
+                off = (xm * ldx + k) * 2
+                assert np.all(off[ok] + 16 <= x_extent)
+                # the LDS x tile row of every loading thread exists
+                assert np.all(xm[tid < mt * 8] < mt)
     for panel in {0, panels - 1}:
         n0 = panel * 128
         valid = min(16, (N - n0 + 7) // 8)
