@@ -33,6 +33,7 @@ namespace {
 
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 // Buffer-resource word 3 for raw (unswizzled) gfx9 buffers; out-of-range reads return zero.
@@ -293,20 +294,52 @@ __device__ __forceinline__ int64_t part_base(const KParams& p, const Item& it) {
     return (((it.b * p.mblocks + it.mb) * p.n_panels + it.panel) * int64_t(p.ks_max)) * (int64_t(MT) * kPanelCols);
 }
 
-// Gather, part 1: each wave folds its row groups with a fixed butterfly of cross-lane exchanges
-// (lanes r*cw + c and (r^j)*cw + c hold the same columns), then the four waves are summed
-// through LDS in wave order.  A panel with one K-slice writes y; otherwise the slice's partial
+// A workgroup barrier that orders LDS only.  __syncthreads() also releases global memory, which
+// makes every wave wait for its outstanding stores first.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Row-group butterfly without LDS.  Within each 16-lane row, DPP rotations by 1, 2, 4 and 8 add
+// lane l - off (mod 16) to lane l; applied for off = cw, 2cw, .. 8 they leave in every lane the sum
+// of the row's lanes congruent to it mod cw (for off = 8 the partner is lane l ^ 8).  Across rows,
+// v_permlane16_swap and v_permlane32_swap exchange 16-lane rows (permlane16_swap(x, x) gives the
+// rows [x0 x0 x2 x2] and [x1 x1 x3 x3], permlane32_swap(x, x) gives [x0 x1 x0 x1] and
+// [x2 x3 x2 x3], so the two halves add up to the pair sums x[l] + x[l ^ 16], x[l] + x[l ^ 32]).
+template <int OFF>
+__device__ __forceinline__ float add_ror(float x) {
+    return x + __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x120 + OFF /* row_ror:OFF */, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float add_xor16(float x) {
+    const u32x2 r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r.x) + __uint_as_float(r.y);
+}
+__device__ __forceinline__ float add_xor32(float x) {
+    const u32x2 r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r.x) + __uint_as_float(r.y);
+}
+
+// Gather, part 1: each wave folds its row groups with the butterfly above (lanes r*cw + c and
+// r'*cw + c hold the same columns), then the four waves are summed through LDS in wave order.  A panel with one K-slice writes y; otherwise the slice's partial
 // sums go to the workspace with device-scope stores (coherent past the per-XCD L2 caches).
 template <int MT, bool CHAIN>
 __device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, float (&acc)[MT][8], float* lds,
                                             int tid) {
     const int lane = tid & 63, wave = tid >> 6;
-    for (int off = it.cw; off < 64; off <<= 1) {
-#pragma unroll
-        for (int m = 0; m < MT; ++m)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) acc[m][j] += __shfl_xor(acc[m][j], off);
+#define NMM_FOLD(COND, OP)                                                   \
+    if (COND) {                                                              \
+        _Pragma("unroll") for (int m = 0; m < MT; ++m)                       \
+            _Pragma("unroll") for (int j = 0; j < 8; ++j) acc[m][j] = OP(acc[m][j]); \
     }
+    NMM_FOLD(it.cw <= 1, add_ror<1>)   // narrow tail panels only
+    NMM_FOLD(it.cw <= 2, add_ror<2>)
+    NMM_FOLD(it.cw <= 4, add_ror<4>)
+    NMM_FOLD(it.cw <= 8, add_ror<8>)
+    NMM_FOLD(it.cw <= 16, add_xor16)
+    NMM_FOLD(it.cw <= 32, add_xor32)
+#undef NMM_FOLD
     constexpr int MG = MT < 4 ? MT : 4;
     const int pcols = it.cw * 8;
     const int64_t pbase = part_base<MT>(p, it);
@@ -320,7 +353,7 @@ __device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, fl
                 *reinterpret_cast<f32x4*>(dst + 4) = f32x4{acc[g + mm][4], acc[g + mm][5], acc[g + mm][6], acc[g + mm][7]};
             }
         }
-        __syncthreads();
+        lds_barrier();
         for (int o = tid; o < MG * pcols; o += kThreads) {
             const int mm = o / pcols, col = o - mm * pcols;
             float v = lds[mm * pcols + col];
@@ -335,7 +368,7 @@ __device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, fl
                                    v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
         }
-        __syncthreads();
+        lds_barrier();
     }
 }
 
