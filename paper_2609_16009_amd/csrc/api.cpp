@@ -31,15 +31,24 @@ bool chain_fused_requested() {
     return fe && fe[0] == '1';
 }
 
+}  // namespace
+
+// Compute units of the current device (256 on MI355X; also the answer when no device is visible).
+int nmm::device_cus() {
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    return cus;
+}
+
+namespace {
+
 int chain_workgroups() {
     if (const char* s = std::getenv("NMM_CHAIN_WGS")) {
         const long v = std::strtol(s, nullptr, 10);
         if (v > 0 && v < (1 << 20)) return static_cast<int>(v);
     }
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-        cus = 256;
-    return cus;
+    return device_cus();
 }
 
 nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, void* stream) {

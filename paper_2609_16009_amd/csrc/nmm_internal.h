@@ -95,6 +95,7 @@ int chain_flags(const GemvArgs* a, const GemvPlan* p, int n);
 bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n);
 nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 size_t mfma_lds_bytes(const GemvPlan& p);
+int device_cus();   // compute units of the current device
 nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
                         unsigned* const* tickets, float* const* part, int grid, void* stream);
 
