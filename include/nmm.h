@@ -132,7 +132,11 @@ nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_
  * Every buffer is caller-owned device memory.  The fp32 and bf16 intermediates are outputs so
  * that each step can be checked on its own.  `events`, if not NULL, points to n_events >= 6
  * hipEvent_t handles; event i is recorded on `stream` before step i (i < 5) and event 5 after
- * the last step -- optional instrumentation for per-step timing.
+ * the last step -- optional instrumentation for per-step timing.  When kv_lora = 512,
+ * v_head = 128 and nope is a multiple of 64 up to 512, the two per-head steps run as one
+ * launch (one workgroup per head; the environment variable NMM_CHAIN_PAIR=0 keeps two) and
+ * events 2 and 3 are both recorded before it.  Either way every output is the fp32 sum of the
+ * same products; only the order of the additions differs between the two forms.
  */
 typedef struct {
     int64_t hidden, q_lora, kv_lora, rope, heads, nope, v_head;   /* 7168,1536,512,64,128,128,128 */

@@ -26,6 +26,11 @@ int chain_unroll() {
     return 16;
 }
 
+bool chain_pair_enabled() {
+    const char* e = std::getenv("NMM_CHAIN_PAIR");
+    return !(e && e[0] == '0');
+}
+
 bool chain_fused_requested() {
     const char* fe = std::getenv("NMM_CHAIN_FUSED");
     return fe && fe[0] == '1';
@@ -256,9 +261,19 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
         }
         return NMM_OK;
     }
+    // W_UK and W_UV run as one launch, one workgroup per head, where the dimensions allow it
+    // (NMM_CHAIN_PAIR=0 keeps two launches); events 2 and 3 are then recorded together before it
+    const bool pair = chain_pair_enabled() && head_pair_ok(c.heads, c.nope, c.kv_lora, c.v_head);
     for (int i = 0; i < 5; ++i) {
         if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess)
             return NMM_ERR_HIP;
+        if (pair && i == 2) continue;
+        if (pair && i == 3) {
+            st = launch_head_pair(c.heads, c.nope, c.qnope_bf16, c.w_uk, c.w_uv, c.lat_f32, c.lat_bf16, c.o_f32, c.o_bf16,
+                                  stream);
+            if (st != NMM_OK) return st;
+            continue;
+        }
         unsigned* tickets = nullptr;
         float* part = nullptr;
         if (ch.plan[i].split()) {

@@ -811,6 +811,156 @@ nmm_status launch_chain_u(const ChainArgs& ca, int grid, size_t lds, hipStream_t
     return last_launch_status();
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// The decode chain's per-head pair W_UK -> W_UV in one launch (bf16, M = 1).  Head h's two
+// products depend only on each other, so one workgroup runs both:
+//   lat_h = q_nope_h . W_UK[h]  ([nope] x [nope, 512]),  lat'_h = bf16(lat_h)
+//   o_h   = lat'_h . W_UV[h]    ([512] x [512, 128]),    o'_h   = bf16(o_h)
+// It streams W_UK[h] and then W_UV[h] as one sequence of row-steps with U steps in flight, so
+// W_UV's first loads are out while W_UK's sums are reduced; no second launch, no split-K.
+//  * W_UK step t: wave w reads row 4t + w (1 KB, 16 bytes per lane).
+//  * W_UV step t: wave w reads rows 16t + 4w .. + 3 (256 bytes each, 16 lanes per row).
+// One workgroup per head leaves the rest of the device to the other stream's work.
+// ---------------------------------------------------------------------------------------------
+constexpr int kPairLat = 512;     // kv_lora
+constexpr int kPairV = 128;       // v_head
+constexpr int kPairMaxNope = 512;
+
+struct PairParams {
+    const uint16_t* q;    // q_nope bf16, head h at q + h * sq
+    int64_t sq;
+    const uint16_t* wuk;  // [heads][nope][512]
+    const uint16_t* wuv;  // [heads][512][128]
+    float* lat;           // [heads][512]
+    uint16_t* latb;
+    float* o;             // [heads][128]
+    uint16_t* ob;
+    int nope;
+};
+
+template <int U>
+__global__ __launch_bounds__(kThreads) void head_pair_kernel(const PairParams p) {
+    __shared__ __attribute__((aligned(16))) float xs[kPairMaxNope];   // q_nope of the head
+    __shared__ __attribute__((aligned(16))) float red[kWaves * kPairLat];
+    __shared__ float lat_s[kPairLat];                                 // lat'_h, widened
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t h = blockIdx.x;
+    const int ta = p.nope / 4;                          // W_UK row-steps (a multiple of U)
+    constexpr int kTb = kPairLat / 16;                  // W_UV row-steps
+    const __amdgpu_buffer_rsrc_t uk =
+        make_rsrc(p.wuk + h * int64_t(p.nope) * kPairLat, uint32_t(p.nope) * kPairLat * 2);
+    const __amdgpu_buffer_rsrc_t uv = make_rsrc(p.wuv + h * int64_t(kPairLat) * kPairV, kPairLat * kPairV * 2);
+    auto off_a = [&](int t) { return uint32_t((4 * t + wave) * (kPairLat * 2) + lane * 16); };
+    auto off_b = [&](int t) {
+        return t < kTb ? uint32_t((16 * t + 4 * wave + (lane >> 4)) * (kPairV * 2) + (lane & 15) * 16) : kOutOfRange;
+    };
+
+    // q_nope_h first (8 values per lane), then the first U row-steps, then q to LDS
+    i32x4 qv = __builtin_amdgcn_raw_buffer_load_b128(make_rsrc(p.q + h * p.sq, uint32_t(p.nope) * 2),
+                                                    tid * 8 < p.nope ? uint32_t(tid * 16) : kOutOfRange, 0, 0);
+    i32x4 buf[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uk, off_a(u), 0, kLoadNT);
+    if (tid * 8 < p.nope) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t w = static_cast<uint32_t>(qv[i]);
+            xs[tid * 8 + 2 * i] = __uint_as_float(w << 16);
+            xs[tid * 8 + 2 * i + 1] = __uint_as_float(w & 0xFFFF0000u);
+        }
+    }
+    __syncthreads();
+
+    // ---- lat_h: row 4t + wave, columns 8 lane .. + 7
+    float acc[1][8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[0][e] = 0.f;
+    int t0 = 0;
+    for (; t0 + U < ta; t0 += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            fma_chunk<NMM_BF16, 1>(acc, buf[u], xs + 4 * (t0 + u) + wave);
+            buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uk, off_a(t0 + u + U), 0, kLoadNT);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {   // the last U steps reload with W_UV's first U
+        fma_chunk<NMM_BF16, 1>(acc, buf[u], xs + 4 * (t0 + u) + wave);
+        buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uv, off_b(u), 0, kLoadNT);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // the four waves' row sums, in wave order; lat and its bf16 rounding out, lat' to LDS
+    *reinterpret_cast<f32x4*>(red + wave * kPairLat + 8 * lane) = f32x4{acc[0][0], acc[0][1], acc[0][2], acc[0][3]};
+    *reinterpret_cast<f32x4*>(red + wave * kPairLat + 8 * lane + 4) = f32x4{acc[0][4], acc[0][5], acc[0][6], acc[0][7]};
+    lds_barrier();
+    for (int c = tid; c < kPairLat; c += kThreads) {
+        float v = red[c];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) v += red[w * kPairLat + c];
+        const uint16_t b = to_bf16_bits(v);
+        p.lat[h * kPairLat + c] = v;
+        p.latb[h * kPairLat + c] = b;
+        lat_s[c] = __uint_as_float(uint32_t(b) << 16);
+    }
+    lds_barrier();
+
+    // ---- o_h: rows 16t + 4 wave + lane / 16, columns 8 (lane % 16) .. + 7
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[0][e] = 0.f;
+    const int rsub = 4 * wave + (lane >> 4);
+    for (int t = 0; t < kTb; t += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            fma_chunk<NMM_BF16, 1>(acc, buf[u], lat_s + 16 * (t + u) + rsub);
+            buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uv, off_b(t + u + U), 0, kLoadNT);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    // fold the wave's four row groups (lanes c, c + 16, c + 32, c + 48), then the waves in order
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[0][e] = add_xor32(add_xor16(acc[0][e]));
+    if (lane < 16) {
+        *reinterpret_cast<f32x4*>(red + wave * kPairV + 8 * lane) = f32x4{acc[0][0], acc[0][1], acc[0][2], acc[0][3]};
+        *reinterpret_cast<f32x4*>(red + wave * kPairV + 8 * lane + 4) = f32x4{acc[0][4], acc[0][5], acc[0][6], acc[0][7]};
+    }
+    lds_barrier();
+    if (tid < kPairV) {
+        float v = red[tid];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) v += red[w * kPairV + tid];
+        p.o[h * kPairV + tid] = v;
+        p.ob[h * kPairV + tid] = to_bf16_bits(v);
+    }
+}
+
+}  // namespace
+
+bool head_pair_ok(int64_t heads, int64_t nope, int64_t kv_lora, int64_t v_head) {
+    return heads >= 1 && heads < (int64_t(1) << 31) && kv_lora == kPairLat && v_head == kPairV && nope >= 4 * kPairUnroll &&
+           nope <= kPairMaxNope && nope % (4 * kPairUnroll) == 0;
+}
+
+nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
+                            float* lat, void* lat_bf16, float* o, void* o_bf16, void* stream) {
+    PairParams pp{};
+    pp.q = static_cast<const uint16_t*>(q_nope);
+    pp.sq = nope;
+    pp.wuk = static_cast<const uint16_t*>(w_uk);
+    pp.wuv = static_cast<const uint16_t*>(w_uv);
+    pp.lat = lat;
+    pp.latb = static_cast<uint16_t*>(lat_bf16);
+    pp.o = o;
+    pp.ob = static_cast<uint16_t*>(o_bf16);
+    pp.nope = static_cast<int>(nope);
+    hipLaunchKernelGGL(head_pair_kernel<kPairUnroll>, dim3(static_cast<uint32_t>(heads)), dim3(kThreads), 0,
+                       static_cast<hipStream_t>(stream), pp);
+    return last_launch_status();
+}
+
+namespace {
 }  // namespace
 
 nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,

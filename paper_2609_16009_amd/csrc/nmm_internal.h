@@ -96,6 +96,13 @@ bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n);
 nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 size_t mfma_lds_bytes(const GemvPlan& p);
 int device_cus();   // compute units of the current device
+
+// The decode chain's W_UK -> W_UV pair in one launch, one workgroup per head (bf16, M = 1):
+// usable for kv_lora 512, v_head 128 and nope a multiple of 4 * kPairUnroll up to 512.
+constexpr int kPairUnroll = 16;
+bool head_pair_ok(int64_t heads, int64_t nope, int64_t kv_lora, int64_t v_head);
+nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
+                            float* lat, void* lat_bf16, float* o, void* o_bf16, void* stream);
 nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
                         unsigned* const* tickets, float* const* part, int grid, void* stream);
 

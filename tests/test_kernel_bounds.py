@@ -201,3 +201,32 @@ def test_chain_dependencies_cover_every_input(dims, unroll, monkeypatch):
                 assert 0 <= qa <= qb < flags[s - 1]
                 needed = {producer_panel(pp, group, keep, sb, b * sx + k)[0] for k in range(k0, k1)}
                 assert needed <= set(range(qa, qb + 1))
+
+
+@pytest.mark.parametrize("nope", [64, 128, 192, 512])
+def test_head_pair_loads_stay_in_bounds(nope):
+    # head_pair_kernel: W_UK[h] is nope rows of 1 KB, W_UV[h] 512 rows of 256 B; 16 row-steps
+    # in flight, W_UK's last 16 steps reload with W_UV's first 16, W_UV's last reload past the end
+    U, lat, v = 16, 512, 128
+    assert nope % (4 * U) == 0
+    tid = np.arange(256)
+    lane, wave = tid & 63, tid >> 6
+    ta, tb = nope // 4, lat // 16
+    uk_bytes, uv_bytes = nope * lat * 2, lat * v * 2
+    off_a = lambda t: (4 * t + wave) * lat * 2 + lane * 16
+    off_b = lambda t: (16 * t + 4 * wave + (lane >> 4)) * v * 2 + (lane & 15) * 16 if t < tb else None
+    issued_a = list(range(U)) + [t0 + u + U for t0 in range(0, ta - U, U) for u in range(U)]
+    assert sorted(issued_a) == list(range(ta))                 # every W_UK step exactly once
+    for t in issued_a:
+        assert np.all(off_a(t) + 16 <= uk_bytes) and np.all(off_a(t) >= 0)
+    issued_b = list(range(U)) + [t + u + U for t in range(0, tb, U) for u in range(U)]
+    assert sorted(x for x in issued_b if x < tb) == list(range(tb))   # every W_UV step once
+    for t in issued_b:
+        o = off_b(t)
+        if o is not None:
+            assert np.all(o + 16 <= uv_bytes)
+    # rows used by the multiply-adds: x of W_UK and the latent of W_UV
+    assert max(4 * t + 3 for t in range(ta)) < nope
+    assert max(16 * t + 15 for t in range(tb)) < lat
+    # q_nope: 8 values per lane, lanes with tid * 8 < nope
+    assert np.all((tid * 16 + 16)[tid * 8 < nope] <= nope * 2)
