@@ -297,48 +297,57 @@ void attention_kernel(const AttnParams p) {
 // Merge the spans of each head in span order:
 //   out = sum_s w_s O_s,  w_s = 2^(m_s - M) / sum_q 2^(m_q - M) l_q,  M = max_s m_s.
 // One output per thread: a workgroup owns 4 heads x 64 columns, so 64 threads read one
-// 256-byte segment of a (head, span) row.  The 4 heads' weights are computed once (one thread
-// per head) into LDS; every thread then issues the loads of up to 16 spans at once.
+// 256-byte segment of a (head, span) row.  The partial outputs' loads go out first; the spans'
+// (max, sum) pairs follow, one pair per thread, into LDS, where one thread per head forms the
+// weights -- so the whole merge waits for about one memory round trip.
 constexpr int kMergeCols = 64;
 constexpr int kMergeHeads = kAThreads / kMergeCols;   // 4
-constexpr int kMergeBatch = 16;
+constexpr int kMergeBatch = 32;
 constexpr int kMergeMaxSpans = 64;
 __global__ __launch_bounds__(kAThreads) void attention_merge_kernel(const AttnParams p) {
-    __shared__ float wgt[kMergeMaxSpans * kMergeHeads];   // [span][head of the group]
+    __shared__ float wgt[kMergeMaxSpans * kMergeHeads];      // [span][head of the group]
+    __shared__ float mls[kMergeMaxSpans * kMergeHeads * 2];  // [span][head][max, sum]
     const int n_cb = (p.dv + kMergeCols - 1) / kMergeCols;
     const int hq = blockIdx.x / n_cb, cb = blockIdx.x - hq * n_cb;
     const int tid = threadIdx.x;
     const int h0 = hq * kMergeHeads;                      // a multiple of 4: never crosses a head block
     const int hb = h0 / kHB, r0 = h0 - hb * kHB;
+    const int i = tid / kMergeCols, n = cb * kMergeCols + (tid % kMergeCols);
+    const int h = h0 + i;
+    const bool active = h < p.heads && n < p.dv;
+    const float* src = p.part_o + (int64_t(hb) * p.nsp * kHB + r0 + i) * p.dv + n;
+    const int64_t step = int64_t(kHB) * p.dv;
+    float v[kMergeBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) v[u] = (active && u < p.nsp) ? src[u * step] : 0.f;
+    for (int t = tid; t < p.nsp * kMergeHeads; t += kAThreads) {
+        const int q = t / kMergeHeads, hh = t - q * kMergeHeads;
+        const float* ml = p.part_ml + ((int64_t(hb) * p.nsp + q) * kHB + r0 + hh) * 2;
+        mls[2 * t] = ml[0];
+        mls[2 * t + 1] = ml[1];
+    }
+    __syncthreads();
     if (tid < kMergeHeads) {
-        const float* ml = p.part_ml + (int64_t(hb) * p.nsp * kHB + r0 + tid) * 2;
-        const int64_t st = kHB * 2;
         float M = -INFINITY;
-#pragma unroll 8
-        for (int q = 0; q < p.nsp; ++q) M = fmaxf(M, ml[q * st]);
+        for (int q = 0; q < p.nsp; ++q) M = fmaxf(M, mls[2 * (q * kMergeHeads + tid)]);
         float den = 0.f;
-#pragma unroll 8
         for (int q = 0; q < p.nsp; ++q) {
-            const float mq = ml[q * st];
+            const float mq = mls[2 * (q * kMergeHeads + tid)];
             const float w = (mq == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mq - M);
-            den += w * ml[q * st + 1];
+            den += w * mls[2 * (q * kMergeHeads + tid) + 1];
             wgt[q * kMergeHeads + tid] = w;
         }
         const float inv = 1.f / den;
-#pragma unroll 8
         for (int q = 0; q < p.nsp; ++q) wgt[q * kMergeHeads + tid] *= inv;
     }
     __syncthreads();
-    const int i = tid / kMergeCols, n = cb * kMergeCols + (tid % kMergeCols);
-    const int h = h0 + i;
-    if (h >= p.heads || n >= p.dv) return;
-    const float* src = p.part_o + (int64_t(hb) * p.nsp * kHB + r0 + i) * p.dv + n;
-    const int64_t step = int64_t(kHB) * p.dv;
+    if (!active) return;
     float acc = 0.f;
     for (int q0 = 0; q0 < p.nsp; q0 += kMergeBatch) {
-        float v[kMergeBatch];
+        if (q0 > 0) {
 #pragma unroll
-        for (int u = 0; u < kMergeBatch; ++u) v[u] = (q0 + u < p.nsp) ? src[(q0 + u) * step] : 0.f;
+            for (int u = 0; u < kMergeBatch; ++u) v[u] = (q0 + u < p.nsp) ? src[(q0 + u) * step] : 0.f;
+        }
 #pragma unroll
         for (int u = 0; u < kMergeBatch; ++u)
             if (q0 + u < p.nsp) acc += wgt[(q0 + u) * kMergeHeads + i] * v[u];
