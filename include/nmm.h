@@ -39,8 +39,9 @@
  *    device-side fault surfaces at the caller's next synchronisation.
  *  - Empty problems: M == 0 or N == 0 is a no-op returning NMM_OK; K == 0 writes zeros (the
  *    empty sum).
- *  - Limits: every size and leading dimension must be < 2^31, and each W matrix's extent must
- *    be < 2^31 bytes (buffer-resource offsets are 32-bit); otherwise NMM_ERR_SHAPE.
+ *  - Limits: every size and leading dimension must be < 2^31, each W matrix's extent must be
+ *    < 2^31 bytes, and so must the x rows of one 32-row block, (min(M, 32) - 1) * ldx +
+ *    roundup(K, 8) elements (buffer-resource offsets are 32-bit); otherwise NMM_ERR_SHAPE.
  */
 #ifndef NMM_H
 #define NMM_H

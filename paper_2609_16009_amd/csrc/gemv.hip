@@ -199,15 +199,16 @@ __device__ __forceinline__ void stage_x_issue(i32x4 (&v)[kXPer], const KParams& 
     const int cpr = rows / 8;                       // chunks per x row of the slice
     const int total = cpr * MT;
     const int mrows = min(MT, p.M - m0);
-    // x's extent reaches the 16-byte chunk holding each row's last element (ABI rule)
-    const uint32_t x_extent = uint32_t(((int64_t(m0) + mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2);
-    const __amdgpu_buffer_rsrc_t xr = make_rsrc(p.x + b * p.sx, x_extent);
+    // the row block's x: its extent reaches the 16-byte chunk holding each row's last element
+    // (ABI rule; below 2 GiB by validation)
+    const uint32_t x_extent = uint32_t((int64_t(mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2);
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(p.x + b * p.sx + int64_t(m0) * p.ldx, x_extent);
 #pragma unroll
     for (int j = 0; j < kXPer; ++j) {
         const int i = tid + j * kThreads;
         const int m = i / cpr, q = i - m * cpr;
         const bool ok = i < total && m < mrows;
-        const uint32_t off = ok ? uint32_t(((int64_t(m0) + m) * p.ldx + k0 + 8 * q) * 2) : kOutOfRange;
+        const uint32_t off = ok ? uint32_t((int64_t(m) * p.ldx + k0 + 8 * q) * 2) : kOutOfRange;
         v[j] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, AUX);
     }
 }

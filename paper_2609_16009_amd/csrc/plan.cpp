@@ -71,6 +71,9 @@ nmm_status validate_gemv(const GemvArgs& a, int path) {
     if ((reinterpret_cast<uintptr_t>(a.y) & 3u) != 0) return NMM_ERR_ALIGN;
     const int64_t extent = ((a.K - 1) * a.ldw + rup(a.N, 8)) * 2;    // bytes of one W
     if (extent >= kLimit) return NMM_ERR_SHAPE;
+    // bytes of x one row block reads (blocks are at most 32 rows)
+    const int64_t x_extent = ((std::min<int64_t>(a.M, 32) - 1) * a.ldx + rup(a.K, 8)) * 2;
+    if (x_extent >= kLimit) return NMM_ERR_SHAPE;
     if (a.ybf && (a.ybf_group <= 0 || a.ybf_keep <= 0 || a.ybf_keep > a.ybf_group)) return NMM_ERR_ARG;
     return NMM_OK;
 }

@@ -66,6 +66,8 @@ def gemv(**kw):
     (dict(y=ALIGNED + 2), nmm.NMM_ERR_ALIGN),
     (dict(M=1, K=1 << 31), nmm.NMM_ERR_SHAPE),
     (dict(K=40000, N=40000, ldw=40000, ldy=40000, ldx=40000), nmm.NMM_ERR_SHAPE),  # W > 2 GiB
+    (dict(M=2, ldx=1 << 30), nmm.NMM_ERR_SHAPE),    # two x rows 2 GiB apart: one block > 2 GiB
+    (dict(M=40, ldx=1 << 26), nmm.NMM_ERR_SHAPE),   # a 32-row block of x spans > 2 GiB
     (dict(K=4096, N=4096, ldw=4096, ldy=4096, ldx=4096, ws=None), nmm.NMM_ERR_WORKSPACE),
     (dict(K=4096, N=4096, ldw=4096, ldy=4096, ldx=4096, wsb=16), nmm.NMM_ERR_WORKSPACE),
     (dict(K=4096, N=4096, ldw=4096, ldy=4096, ldx=4096, ws=ALIGNED + 64), nmm.NMM_ERR_WORKSPACE),
