@@ -9,7 +9,10 @@ Functions (each cites the passage it follows in ``nmm_oracle.c``):
 * ``gemv``            -- y = x . W and sum |x_k W_kn| in fp64 (problem statement, Section II-E;
                          Condition 2, Section III-A; eq. 4, Section IV-B).
 * ``batched_gemv``    -- the same per batch index (per-head absorbed MLA matmuls).
-* ``round_bf16``      -- fp32 -> bf16 ties-to-even (Algorithm 2's final cast, Section IV-E).
+* ``round_bf16``      -- fp32 -> bf16, ties to even or away (Algorithm 2's final cast, Section IV-E).
+* ``round_bf16_exact``-- the same for fp64 values, rounded once.
+* ``rmsnorm``, ``rope``, ``kv_entry``, ``mla_kv_update`` -- MatMul 2 of Section IV-A and the
+                         vector work behind it (RMSNorm, RoPE, the cache entry).
 * ``latent_attention``-- textbook softmax attention in fp64 (the decode step's independent work).
 * ``mla_chain``       -- the decode step's narrow chain composed from the above.
 
@@ -61,6 +64,16 @@ def lib() -> ctypes.CDLL:
         L.nmmo_round_bf16_rne.restype = ctypes.c_uint16
         L.nmmo_round_bf16_rne.argtypes = [ctypes.c_float]
         L.nmmo_round_bf16_rne_array.argtypes = [_p, _p, _i64]
+        L.nmmo_round_bf16_array.argtypes = [_p, _p, _i64, ctypes.c_int]
+        L.nmmo_rmsnorm.argtypes = [_i64, _p, _p, ctypes.c_double, _p]
+        L.nmmo_rope.argtypes = [_i64, _p, _i64, ctypes.c_double, _p]
+        L.nmmo_kv_entry.restype = ctypes.c_int
+        L.nmmo_kv_entry.argtypes = [_i64, _i64, _p, _p, ctypes.c_double, ctypes.c_double, _i64,
+                                    ctypes.c_int, _p, _p]
+        L.nmmo_mla_kv_update.restype = ctypes.c_int
+        L.nmmo_mla_kv_update.argtypes = [_i64, _i64, _i64, _p, _p, _i64, _p, ctypes.c_double,
+                                         ctypes.c_double, _i64, ctypes.c_int, _p, _p, _p, _p,
+                                         ctypes.c_int]
         L.nmmo_decode_array.argtypes = [ctypes.c_int, _p, _p, _i64]
         L.nmmo_max_threads.restype = ctypes.c_int
         L.nmmo_gemv.restype = ctypes.c_int
@@ -101,12 +114,85 @@ def decode(bits, dt: int) -> np.ndarray:
     return out
 
 
-def round_bf16(values) -> np.ndarray:
-    """Round float32 values to bf16 bit patterns, ties to even (the paper's output cast)."""
-    v = np.ascontiguousarray(values, dtype=np.float32)
+ROUND_EVEN, ROUND_AWAY = 0, 1
+
+
+def round_bf16(values, mode: int = ROUND_EVEN) -> np.ndarray:
+    """Round values, first narrowed to float32, to bf16 bit patterns (the paper's output cast);
+    ties to even (mode 0) or away from zero (mode 1)."""
+    v = np.ascontiguousarray(np.asarray(values, dtype=np.float32), dtype=np.float64)
     out = np.empty(v.shape, dtype=np.uint16)
-    lib().nmmo_round_bf16_rne_array(_ptr(v), _ptr(out), v.size)
+    lib().nmmo_round_bf16_array(_ptr(v), _ptr(out), v.size, int(mode))
     return out
+
+
+def round_bf16_exact(values, mode: int = ROUND_EVEN) -> np.ndarray:
+    """Round float64 values to bf16 bit patterns with one rounding (no float32 step)."""
+    v = np.ascontiguousarray(values, dtype=np.float64)
+    out = np.empty(v.shape, dtype=np.uint16)
+    lib().nmmo_round_bf16_array(_ptr(v), _ptr(out), v.size, int(mode))
+    return out
+
+
+def rmsnorm(c, gamma, eps: float) -> np.ndarray:
+    """c / sqrt(mean(c^2) + eps) * gamma in float64 (gamma: bf16 bits)."""
+    c = np.ascontiguousarray(c, dtype=np.float64)
+    g = _u16(gamma)
+    if g.size != c.size:
+        raise ValueError("gamma must match c")
+    out = np.empty(c.shape, dtype=np.float64)
+    lib().nmmo_rmsnorm(c.size, _ptr(c), _ptr(g), float(eps), _ptr(out))
+    return out
+
+
+def rope(k, t: int, theta: float) -> np.ndarray:
+    """RoFormer rotation of adjacent pairs of k at position t, base theta, in float64."""
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    if k.size % 2:
+        raise ValueError("RoPE needs an even width")
+    out = np.empty(k.shape, dtype=np.float64)
+    lib().nmmo_rope(k.size, _ptr(k), int(t), float(theta), _ptr(out))
+    return out
+
+
+def kv_entry(mm, gamma, kv_lora: int, eps: float, theta: float, t: int,
+             mode: int = ROUND_EVEN) -> tuple[np.ndarray, np.ndarray]:
+    """The cache entry [RMSNorm(mm[:kv_lora]) | RoPE(mm[kv_lora:], t)]: (float64 row, bf16 bits)."""
+    mm = np.ascontiguousarray(mm, dtype=np.float64).reshape(-1)
+    g = _u16(gamma)
+    rope_w = mm.size - kv_lora
+    row = np.empty(mm.size, dtype=np.float64)
+    bits = np.empty(mm.size, dtype=np.uint16)
+    rc = lib().nmmo_kv_entry(kv_lora, rope_w, _ptr(mm), _ptr(g), float(eps), float(theta), int(t),
+                             int(mode), _ptr(row), _ptr(bits))
+    if rc:
+        raise ValueError(f"oracle kv_entry rejected its arguments ({rc})")
+    return row, bits
+
+
+def mla_kv_update(h, W, gamma, kv_lora: int, rope_w: int, eps: float, theta: float, t: int,
+                  mode: int = ROUND_EVEN, threads: int = 0):
+    """MatMul 2 (h[1, hidden] . W[hidden, >= kv_lora + rope_w]) and the cache entry behind it.
+
+    Returns (mm, mm_abs, row, row_bits): the product and sum |h_k W_kn| in float64, the float64
+    entry before rounding, and its bf16 bits."""
+    h = _u16(h).reshape(-1)
+    W = _u16(W)
+    g = _u16(gamma)
+    hidden, ldw = W.shape
+    n = kv_lora + rope_w
+    if h.size != hidden or g.size != kv_lora or ldw < n:
+        raise ValueError("MatMul 2 operand shapes do not match")
+    mm = np.empty(n, dtype=np.float64)
+    mm_abs = np.empty(n, dtype=np.float64)
+    row = np.empty(n, dtype=np.float64)
+    bits = np.empty(n, dtype=np.uint16)
+    rc = lib().nmmo_mla_kv_update(hidden, kv_lora, rope_w, _ptr(h), _ptr(W), ldw, _ptr(g), float(eps),
+                                  float(theta), int(t), int(mode), _ptr(mm), _ptr(mm_abs), _ptr(row),
+                                  _ptr(bits), threads)
+    if rc:
+        raise ValueError(f"oracle mla_kv_update rejected its arguments ({rc})")
+    return mm, mm_abs, row, bits
 
 
 def gemv(x, W, dt: int, M: int | None = None, K: int | None = None, N: int | None = None,

@@ -16,9 +16,15 @@
  *    Issue") and computes the same product, so the plain product is the reference.  A product
  *    of two 16-bit floats is exact in fp64; only the K-term summation rounds, at ~K*2^-53.
  *  - The same per batch index (the per-head absorbed MLA matmuls).
- *  - The output narrowing fp32 -> bf16 with round-to-nearest-even (Algorithm 2's final cast,
- *    Section IV-E).  The paper names the mode CAST_ROUND without defining it; ties-to-even
- *    is the reading taken here.
+ *  - The output narrowing to bf16 (Algorithm 2's final cast, Section IV-E).  The paper names
+ *    the mode CAST_ROUND without defining it, so both nearest modes are provided: ties to even
+ *    (the default reading, used between the chain's steps) and ties away from zero.
+ *  - The vector work the paper places behind MatMul 2 (Section IV-A, eq. 1-3: c^KV = W^DKV h,
+ *    k^R = RoPE(W^KR h), computed as one product, followed by RMSNorm, RoPE and caching):
+ *        c' = c / sqrt(mean(c^2) + eps) * gamma      RMSNorm (Zhang and Sennrich, 2019)
+ *        k' = RoPE(k, t)                             RoPE (Su et al., RoFormer), adjacent pairs
+ *        cache[t] = bf16(c' | k')
+ *    The paper gives neither formula in full; these are the cited methods' own definitions.
  *  - Latent attention for the decode step's independent stream: fp64 scores, softmax with
  *    the maximum subtracted, then times V.  Not a formula of the paper (its MLA figure is
  *    lost); the plain textbook definition.
@@ -77,21 +83,25 @@ double nmmo_dec_bf16(uint16_t b) {
 
 static double dec(int dt, uint16_t b) { return dt == NMMO_F16 ? nmmo_dec_f16(b) : nmmo_dec_bf16(b); }
 
-/* ------------------------------------------------------------------ fp32 -> bf16 (RNE) */
+/* ------------------------------------------------------------------ rounding to bf16 */
 
-/* Round half to even of a non-negative double that is an integer plus a fraction. */
-static double rne_nonneg(double s) {
+#define NMMO_ROUND_EVEN 0
+#define NMMO_ROUND_AWAY 1
+
+/* Round a non-negative double s < 2^53 to an integer, nearest, ties to even or away from 0. */
+static double round_nonneg(double s, int mode) {
     double fl = floor(s);
     double frac = s - fl;                 /* exact: s < 2^53 here */
     if (frac > 0.5) return fl + 1.0;
     if (frac < 0.5) return fl;
+    if (mode == NMMO_ROUND_AWAY) return fl + 1.0;
     return (fmod(fl, 2.0) == 0.0) ? fl : fl + 1.0;
 }
 
-/* Nearest bf16 to the float v, ties to even.  Returns the bit pattern.  NaN maps to a quiet
- * NaN with v's sign; results beyond the largest finite bf16 (after rounding) become inf. */
-uint16_t nmmo_round_bf16_rne(float v) {
-    double a = (double)v;
+/* Nearest bf16 to the double a (one rounding), ties per mode.  Returns the bit pattern.  NaN
+ * maps to a quiet NaN with a's sign; results beyond the largest finite bf16 (after rounding)
+ * become inf. */
+uint16_t nmmo_round_bf16(double a, int mode) {
     uint16_t sign = signbit(a) ? 0x8000u : 0u;
     if (isnan(a)) return (uint16_t)(sign | 0x7FC0u);
     a = fabs(a);
@@ -102,12 +112,12 @@ uint16_t nmmo_round_bf16_rne(float v) {
     int unb = e - 1;                      /* a in [2^unb, 2^(unb+1)) */
     if (unb < -126) {
         /* subnormal range: the grid step is 2^-133 */
-        double r = rne_nonneg(ldexp(a, 133));   /* 0..128 */
+        double r = round_nonneg(ldexp(a, 133), mode);   /* 0..128 */
         if (r >= 128.0) return (uint16_t)(sign | (1u << 7));   /* rounds up to 2^-126 */
         return (uint16_t)(sign | (uint16_t)r);
     }
     /* normal: 8 significant bits; the grid step is 2^(unb-7) */
-    double r = rne_nonneg(ldexp(a, 7 - unb));   /* in [128, 256] */
+    double r = round_nonneg(ldexp(a, 7 - unb), mode);   /* in [128, 256] */
     if (r >= 256.0) { r = 128.0; unb += 1; }
     if (unb > 127) return (uint16_t)(sign | 0x7F80u);
     uint16_t ebits = (uint16_t)(unb + 127);
@@ -115,8 +125,15 @@ uint16_t nmmo_round_bf16_rne(float v) {
     return (uint16_t)(sign | (ebits << 7) | fbits);
 }
 
+/* The float v to bf16, ties to even (exact widening, then one rounding). */
+uint16_t nmmo_round_bf16_rne(float v) { return nmmo_round_bf16((double)v, NMMO_ROUND_EVEN); }
+
 void nmmo_round_bf16_rne_array(const float* v, uint16_t* out, int64_t n) {
     for (int64_t i = 0; i < n; ++i) out[i] = nmmo_round_bf16_rne(v[i]);
+}
+
+void nmmo_round_bf16_array(const double* v, uint16_t* out, int64_t n, int mode) {
+    for (int64_t i = 0; i < n; ++i) out[i] = nmmo_round_bf16(v[i], mode);
 }
 
 void nmmo_decode_array(int dt, const uint16_t* b, double* out, int64_t n) {
@@ -292,4 +309,67 @@ int nmmo_mla_chain(int64_t hidden, int64_t q_lora, int64_t kv_lora, int64_t rope
 done:
     free(buf); free(a); free(b);
     return rc;
+}
+
+/* ------------------------------------------------------------------ behind MatMul 2 */
+
+/*
+ * RMSNorm of the compressed latent c (Section IV-A names it among the vector work fed by
+ * MatMul 2; the definition is Zhang and Sennrich's root-mean-square layer normalisation):
+ *   out[i] = c[i] / sqrt((1/n) * sum_j c[j]^2 + eps) * gamma[i]          (gamma bf16)
+ */
+void nmmo_rmsnorm(int64_t n, const double* c, const uint16_t* gamma, double eps, double* out) {
+    double ss = 0.0;
+    for (int64_t j = 0; j < n; ++j) ss += c[j] * c[j];
+    double inv = 1.0 / sqrt(ss / (double)n + eps);
+    for (int64_t i = 0; i < n; ++i) out[i] = c[i] * inv * nmmo_dec_bf16(gamma[i]);
+}
+
+/*
+ * Rotary position embedding of the decoupled key k^R at position t (eq. 2 of Section IV-A; the
+ * definition is RoFormer's, Su et al.): the d values form d/2 adjacent pairs (k[2i], k[2i+1]),
+ * and pair i turns by the angle t * theta^(-2i/d):
+ *   out[2i]   = k[2i] cos(a_i) - k[2i+1] sin(a_i)
+ *   out[2i+1] = k[2i] sin(a_i) + k[2i+1] cos(a_i)
+ */
+void nmmo_rope(int64_t d, const double* k, int64_t t, double theta, double* out) {
+    for (int64_t i = 0; i < d / 2; ++i) {
+        double a = (double)t * pow(theta, -2.0 * (double)i / (double)d);
+        double cs = cos(a), sn = sin(a);
+        out[2 * i] = k[2 * i] * cs - k[2 * i + 1] * sn;
+        out[2 * i + 1] = k[2 * i] * sn + k[2 * i + 1] * cs;
+    }
+}
+
+/*
+ * The cache entry built from MatMul 2's product mm = [c^KV | k^R] (kv_lora + rope values):
+ *   row[:kv_lora] = RMSNorm(mm[:kv_lora]),  row[kv_lora:] = RoPE(mm[kv_lora:], t),
+ *   row_bf16 = bf16(row) (one rounding, ties per mode).
+ * row may be NULL.  Returns 0 or a negative error.
+ */
+int nmmo_kv_entry(int64_t kv_lora, int64_t rope, const double* mm, const uint16_t* gamma, double eps,
+                  double theta, int64_t t, int mode, double* row, uint16_t* row_bf16) {
+    if (kv_lora < 1 || rope < 0 || (rope & 1) || !mm || !gamma || !row_bf16) return -1;
+    double* r = row ? row : (double*)malloc((size_t)(kv_lora + rope) * sizeof(double));
+    if (!r) return -2;
+    nmmo_rmsnorm(kv_lora, mm, gamma, eps, r);
+    nmmo_rope(rope, mm + kv_lora, t, theta, r + kv_lora);
+    nmmo_round_bf16_array(r, row_bf16, kv_lora + rope, mode);
+    if (!row) free(r);
+    return 0;
+}
+
+/*
+ * MatMul 2 for one token and the cache entry behind it (Section IV-A, eq. 3 and 4):
+ *   mm = h . W,  W = (W^DKV | W^KR)^T  [hidden, kv_lora + rope] (row pitch ldw),
+ * then nmmo_kv_entry.  mm (fp64, kv_lora + rope values) is an output too, and mm_abs (may be
+ * NULL) receives sum_k |h_k W_kn|.
+ */
+int nmmo_mla_kv_update(int64_t hidden, int64_t kv_lora, int64_t rope, const uint16_t* h, const uint16_t* w,
+                       int64_t ldw, const uint16_t* gamma, double eps, double theta, int64_t t, int mode,
+                       double* mm, double* mm_abs, double* row, uint16_t* row_bf16, int nthreads) {
+    int64_t n = kv_lora + rope;
+    int rc = nmmo_gemv(1, hidden, n, NMMO_BF16, h, hidden, w, ldw, mm, mm_abs, n, nthreads);
+    if (rc) return rc;
+    return nmmo_kv_entry(kv_lora, rope, mm, gamma, eps, theta, t, mode, row, row_bf16);
 }

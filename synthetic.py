@@ -191,3 +191,33 @@ def attention_case(seed: int, heads: int, seq: int, dqk: int = ATTN_DQK, dv: int
     if ldkv is not None and ldkv != dqk:
         kv = padded(kv, ldkv)
     return q, kv, 1.0 / math.sqrt(QK_HEAD)
+
+
+# MatMul 2 of the paper (one token times (W^DKV | W^KR)^T) and the cache entry behind it.
+KV_EPS, ROPE_THETA = 1e-6, 10000.0      # DeepSeek-V3's RMSNorm epsilon; RoFormer's RoPE base
+
+
+@dataclass
+class KvUpdateCase:
+    """MatMul 2 [1, hidden] . [hidden, kv_lora + rope] and the RMSNorm / RoPE / cache-append behind it."""
+    h: np.ndarray          # [1, hidden] token
+    w: np.ndarray          # [hidden, ldw]: columns 0..kv_lora-1 are W^DKV^T, then rope columns of W^KR^T
+    gamma: np.ndarray      # [kv_lora] RMSNorm weight
+    kv_lora: int
+    rope: int
+    position: int          # the token's position: its RoPE angle and its cache row
+    eps: float = KV_EPS
+    theta: float = ROPE_THETA
+
+
+def kv_update_case(seed: int = 5, hidden: int = HIDDEN, kv_lora: int = KV_LORA, rope: int = ROPE,
+                   position: int = ATTN_SEQ, ldw: int | None = None) -> KvUpdateCase:
+    """Seed 5. h ~ N(0,1), W ~ N(0, 1/hidden), gamma ~ 1 + 0.1 N(0,1) (a trained norm weight sits
+    near 1); bf16 throughout.  The default position appends after a 4096-row cache."""
+    rng = np.random.default_rng(seed)
+    h = normal_bits(rng, (1, hidden), 1.0, BF16)
+    w = normal_bits(rng, (hidden, kv_lora + rope), 1 / math.sqrt(hidden), BF16)
+    gamma = bits_from_f32((1.0 + 0.1 * rng.standard_normal(kv_lora, dtype=np.float32)).astype(np.float32), BF16)
+    if ldw is not None and ldw != kv_lora + rope:
+        w = padded(w, ldw)
+    return KvUpdateCase(h, w, gamma, kv_lora, rope, position)

@@ -33,6 +33,19 @@ MUTANTS = {
     "attention_unnormalised": ("out[h * ldo + n] = o / l;", "out[h * ldo + n] = o;"),
     "attention_v_shifted": ("double v = nmmo_dec_bf16(kv[j * ldkv + n]);",
                             "double v = nmmo_dec_bf16(kv[j * ldkv + (n + 1) % dv]);"),
+    "round_away_ignored": ("    if (mode == NMMO_ROUND_AWAY) return fl + 1.0;\n", ""),
+    "round_away_breaks_down": ("    if (mode == NMMO_ROUND_AWAY) return fl + 1.0;", "    if (mode == NMMO_ROUND_AWAY) return fl;"),
+    "rmsnorm_sum_not_mean": ("double inv = 1.0 / sqrt(ss / (double)n + eps);", "double inv = 1.0 / sqrt(ss + eps);"),
+    "rmsnorm_drops_eps": ("double inv = 1.0 / sqrt(ss / (double)n + eps);", "double inv = 1.0 / sqrt(ss / (double)n);"),
+    "rmsnorm_ignores_gamma": ("out[i] = c[i] * inv * nmmo_dec_bf16(gamma[i]);", "out[i] = c[i] * inv;"),
+    "rope_turns_backwards": ("out[2 * i] = k[2 * i] * cs - k[2 * i + 1] * sn;\n        out[2 * i + 1] = k[2 * i] * sn + k[2 * i + 1] * cs;",
+                             "out[2 * i] = k[2 * i] * cs + k[2 * i + 1] * sn;\n        out[2 * i + 1] = -k[2 * i] * sn + k[2 * i + 1] * cs;"),
+    "rope_half_exponent": ("pow(theta, -2.0 * (double)i / (double)d)", "pow(theta, -(double)i / (double)d)"),
+    "rope_rotates_halves": ("out[2 * i] = k[2 * i] * cs - k[2 * i + 1] * sn;\n        out[2 * i + 1] = k[2 * i] * sn + k[2 * i + 1] * cs;",
+                            "out[i] = k[i] * cs - k[i + d / 2] * sn;\n        out[i + d / 2] = k[i] * sn + k[i + d / 2] * cs;"),
+    "kv_entry_rope_on_latent": ("nmmo_rope(rope, mm + kv_lora, t, theta, r + kv_lora);", "nmmo_rope(rope, mm, t, theta, r + kv_lora);"),
+    "kv_entry_fixed_mode": ("nmmo_round_bf16_array(r, row_bf16, kv_lora + rope, mode);", "nmmo_round_bf16_array(r, row_bf16, kv_lora + rope, 0);"),
+    "kv_update_wrong_pitch": ("h, hidden, w, ldw, mm, mm_abs, n, nthreads);", "h, hidden, w, n, mm, mm_abs, n, nthreads);"),
     "chain_takes_rope_slice": ("b[h * nope + d] = nmmo_round_bf16_rne((float)buf[h * (nope + rope) + d]);",
                                "b[h * nope + d] = nmmo_round_bf16_rne((float)buf[h * (nope + rope) + rope + d]);"),
 }

@@ -11,6 +11,14 @@ What pins what:
   * Latent attention: seq = 1, uniform scores, a two-key case whose softmax is (3/4, 1/4) by
     construction, a dominant key, permutation invariance.
   * Decode chain: permutation-matrix weights make the chain a closed-form gather of x.
+  * Ties away from zero and the single rounding of fp64 values: constructed ties and a
+    neighbour search over the decoded bf16 grid.
+  * RMSNorm: a 3-4-5 closed form, eps on a one-element vector, unit RMS and scale invariance.
+  * RoPE: identity at t = 0, a quarter turn, the relative-position property of RoFormer
+    (<R_m q, R_n k> depends on m - n only), composition, the pair frequency ladder, and the
+    rotation's direction.
+  * MatMul 2 and the cache entry: a one-hot token selects a row of W, and the entry splits
+    into RMSNorm of the first kv_lora values and RoPE of the rest.
 """
 from __future__ import annotations
 
@@ -353,3 +361,178 @@ def test_chain_rounds_intermediates_to_bf16():
     expect = oracle.decode(oracle.round_bf16(np.array([exact], np.float32)), syn.BF16)[0]
     assert expect != exact and expect == 3 + 2 ** -5
     assert y[0, 1] == expect and y[0, 0] == 0.0
+
+
+# ---------------------------------------------------------------- rounding modes
+
+def _neighbour_search(v: float, away: bool) -> int:
+    """Nearest bf16 to v by searching the decoded grid (independent of the oracle's arithmetic)."""
+    sign = 0x8000 if math.copysign(1.0, v) < 0 else 0
+    a = abs(v)
+    grid = oracle.decode(np.arange(0, 0x7F81, dtype=np.uint16), syn.BF16)   # 0 .. inf, ascending
+    hi = int(np.searchsorted(grid, a, side="left"))
+    if grid[hi] == a:
+        return sign | hi
+    lo = hi - 1
+    dlo, dhi = a - grid[lo], grid[hi] - a
+    if dlo < dhi:
+        return sign | lo
+    if dhi < dlo:
+        return sign | hi
+    return sign | (hi if away or (hi & 1) == 0 else lo)
+
+
+def test_round_bf16_ties_away_from_zero():
+    b = np.arange(0x0000, 0x7F7F, dtype=np.uint32)
+    mid = ((b << 16) | 0x8000).view(np.float32)
+    assert np.array_equal(oracle.round_bf16(mid, oracle.ROUND_AWAY), (b + 1).astype(np.uint16))
+    assert np.array_equal(oracle.round_bf16(-mid, oracle.ROUND_AWAY), (b + 1).astype(np.uint16) | 0x8000)
+    below = ((b << 16) | 0x7FFF).view(np.float32)
+    assert np.array_equal(oracle.round_bf16(below, oracle.ROUND_AWAY), b.astype(np.uint16))
+    # integers: 257 and 259 are ties on the bf16 grid of step 2 above 256
+    ints = np.array([257.0, 259.0, -257.0, 258.0], np.float32)
+    assert oracle.round_bf16(ints, oracle.ROUND_EVEN).tolist() == [0x4380, 0x4382, 0xC380, 0x4381]
+    assert oracle.round_bf16(ints, oracle.ROUND_AWAY).tolist() == [0x4381, 0x4382, 0xC381, 0x4381]
+    # the largest finite bf16 plus half a step rounds away to infinity
+    top = np.array([(2 - 2 ** -8) * 2.0 ** 127], np.float64)
+    assert oracle.round_bf16_exact(top, oracle.ROUND_AWAY).tolist() == [0x7F80]
+    assert oracle.round_bf16_exact(top, oracle.ROUND_EVEN).tolist() == [0x7F80]
+
+
+@pytest.mark.parametrize("away", [False, True])
+def test_round_bf16_exact_matches_neighbour_search(away):
+    rng = random.Random(7 + away)
+    vals = []
+    for _ in range(400):
+        e = rng.randint(-140, 127)
+        vals.append(rng.choice([-1, 1]) * rng.random() * 2.0 ** e)
+    # exact ties and values a hair off them, in the normal and subnormal ranges
+    for b in (0x0001, 0x0042, 0x3F80, 0x4380, 0x7F00):
+        lo = float(oracle.decode(np.array([b], np.uint16), syn.BF16)[0])
+        hi = float(oracle.decode(np.array([b + 1], np.uint16), syn.BF16)[0])
+        m = (lo + hi) / 2
+        vals += [m, -m, math.nextafter(m, 0), math.nextafter(m, math.inf)]
+    mode = oracle.ROUND_AWAY if away else oracle.ROUND_EVEN
+    got = oracle.round_bf16_exact(np.array(vals), mode).tolist()
+    assert got == [_neighbour_search(v, away) for v in vals]
+
+
+def test_round_bf16_exact_rounds_once():
+    # 257 + 2^-20 lies above the tie 257 (so rounds to 258), but narrowing it to float32 first
+    # lands on the tie, which then rounds to even (256)
+    v = np.array([257.0 + 2.0 ** -20])
+    assert oracle.round_bf16_exact(v).tolist() == [0x4381]
+    assert oracle.round_bf16(v).tolist() == [0x4380]
+
+
+# ---------------------------------------------------------------- RMSNorm and RoPE
+
+def _gamma(vals):
+    return exact_bits(np.asarray(vals, np.float32), syn.BF16)
+
+
+def test_rmsnorm_closed_forms():
+    # mean of squares of (3, 4) is 12.5; each value divides by sqrt(12.5) = 5 / sqrt(2)
+    out = oracle.rmsnorm([3.0, 4.0], _gamma([1.0, 1.0]), 0.0)
+    assert np.allclose(out, [3 * math.sqrt(2) / 5, 4 * math.sqrt(2) / 5], rtol=1e-15, atol=0)
+    # eps enters under the root: 2 / sqrt(4 + 5) = 2/3
+    assert np.allclose(oracle.rmsnorm([2.0], _gamma([1.0]), 5.0), [2.0 / 3.0], rtol=1e-15)
+    # gamma scales each output on its own
+    g = oracle.rmsnorm([3.0, 4.0], _gamma([2.0, -0.5]), 0.0)
+    assert np.allclose(g, out * np.array([2.0, -0.5]), rtol=1e-15)
+
+
+def test_rmsnorm_unit_rms_and_scale_invariance():
+    rng = np.random.default_rng(11)
+    c = rng.standard_normal(512) * 7.0
+    ones = _gamma(np.ones(512))
+    out = oracle.rmsnorm(c, ones, 0.0)
+    assert abs(math.sqrt(np.mean(out ** 2)) - 1.0) < 1e-13
+    assert np.allclose(oracle.rmsnorm(c * 1000.0, ones, 0.0), out, rtol=1e-13)
+    # with eps > 0 the output's RMS falls below 1 by exactly sqrt(ms / (ms + eps))
+    ms = np.mean(c ** 2)
+    out_e = oracle.rmsnorm(c, ones, ms)
+    assert abs(math.sqrt(np.mean(out_e ** 2)) - math.sqrt(0.5)) < 1e-13
+
+
+def test_rope_identity_at_position_zero():
+    k = np.random.default_rng(3).standard_normal(64)
+    assert np.array_equal(oracle.rope(k, 0, 10000.0), k)
+
+
+def test_rope_quarter_turn_and_direction():
+    # d = 4: pair 1 turns at theta^(-1/2); theta = (2/pi)^2 makes that pi/2 per position
+    th = (2 / math.pi) ** 2
+    out = oracle.rope([0.0, 0.0, 1.0, 0.0], 1, th)
+    assert np.allclose(out, [0.0, 0.0, 0.0, 1.0], atol=1e-15)
+    out = oracle.rope([0.0, 0.0, 0.0, 1.0], 1, th)
+    assert np.allclose(out, [0.0, 0.0, -1.0, 0.0], atol=1e-15)
+    # pair 0 always turns by t radians: a small t moves (1, 0) towards +second component
+    small = oracle.rope([1.0, 0.0], 1, 10000.0)
+    assert small[1] > 0.8 and 0.5 < small[0] < 0.6
+
+
+def test_rope_relative_position_property():
+    rng = np.random.default_rng(5)
+    q, k = rng.standard_normal(64), rng.standard_normal(64)
+    for m, n in [(7, 3), (4100, 4096), (12, 0), (300, 450)]:
+        lhs = float(np.dot(oracle.rope(q, m, 10000.0), oracle.rope(k, n, 10000.0)))
+        rhs = float(np.dot(oracle.rope(q, m - n, 10000.0), k))
+        assert abs(lhs - rhs) < 1e-10 * (1 + abs(rhs))
+
+
+def test_rope_composes_and_preserves_pair_norms():
+    rng = np.random.default_rng(6)
+    k = rng.standard_normal(64)
+    two = oracle.rope(oracle.rope(k, 100, 10000.0), 23, 10000.0)
+    assert np.allclose(two, oracle.rope(k, 123, 10000.0), rtol=0, atol=1e-12)
+    r = oracle.rope(k, 4096, 10000.0)
+    assert np.allclose(np.hypot(r[0::2], r[1::2]), np.hypot(k[0::2], k[1::2]), rtol=1e-14)
+
+
+def test_rope_frequency_ladder():
+    # pair i turns theta^(2/d) times slower than pair i-1: with d = 8 and theta = 16, pair 2 at
+    # t = 16 turns as far as pair 0 at t = 4 (16 * 16^(-4/8) = 4)
+    e = np.zeros(8); e[4] = 1.0
+    r = oracle.rope(e, 16, 16.0)
+    r0 = oracle.rope([1.0, 0.0] + [0.0] * 6, 4, 16.0)
+    assert np.allclose(r[4:6], r0[0:2], atol=1e-14)
+    assert np.array_equal(r[:4], np.zeros(4)) and np.array_equal(r[6:], np.zeros(2))
+
+
+# ---------------------------------------------------------------- MatMul 2 and the cache entry
+
+def test_kv_entry_splits_into_rmsnorm_and_rope():
+    rng = np.random.default_rng(9)
+    mm = rng.standard_normal(12)
+    gamma = syn.normal_bits(rng, (8,), 1.0, syn.BF16)
+    row, bits = oracle.kv_entry(mm, gamma, 8, 1e-6, 10000.0, 37)
+    assert np.array_equal(row[:8], oracle.rmsnorm(mm[:8], gamma, 1e-6))
+    assert np.array_equal(row[8:], oracle.rope(mm[8:], 37, 10000.0))
+    assert np.array_equal(bits, oracle.round_bf16_exact(row))
+
+
+def test_kv_entry_rounding_mode_reaches_the_cache():
+    # c = (257, 0, 0, -257): mean square 33024.5, and eps = 32511.5 makes the root 256, so with
+    # gamma = 256 the normalised values are the bf16 ties +-257; the RoPE part at t = 0 passes
+    # the ties 259 (even and away agree: 260) and -257 through unchanged
+    mm = np.array([257.0, 0.0, 0.0, -257.0, 259.0, -257.0])
+    g = exact_bits(np.array([256.0, 1.0, 1.0, 256.0], np.float32), syn.BF16)
+    row, even = oracle.kv_entry(mm, g, 4, 32511.5, 10000.0, 0, oracle.ROUND_EVEN)
+    _, away = oracle.kv_entry(mm, g, 4, 32511.5, 10000.0, 0, oracle.ROUND_AWAY)
+    assert row.tolist() == [257.0, 0.0, 0.0, -257.0, 259.0, -257.0]
+    assert even.tolist() == [0x4380, 0x0000, 0x0000, 0xC380, 0x4382, 0xC380]
+    assert away.tolist() == [0x4381, 0x0000, 0x0000, 0xC381, 0x4382, 0xC381]
+
+
+def test_mla_kv_update_one_hot_token_selects_a_row():
+    rng = np.random.default_rng(10)
+    hidden, kv, rp = 24, 8, 4
+    W = syn.padded(syn.normal_bits(rng, (hidden, kv + rp), 0.2, syn.BF16), kv + rp + 4)
+    gamma = syn.normal_bits(rng, (kv,), 1.0, syn.BF16)
+    h = np.zeros(hidden, np.uint16); h[13] = ONE[syn.BF16]
+    mm, mm_abs, row, bits = oracle.mla_kv_update(h, W, gamma, kv, rp, 1e-6, 10000.0, 5)
+    w13 = oracle.decode(W[13, :kv + rp], syn.BF16)
+    assert np.array_equal(mm, w13) and np.array_equal(mm_abs, np.abs(w13))
+    row2, bits2 = oracle.kv_entry(w13, gamma, kv, 1e-6, 10000.0, 5)
+    assert np.array_equal(row, row2) and np.array_equal(bits, bits2)
