@@ -112,6 +112,77 @@ nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_
                             float* y, int64_t ldy, int64_t stride_y, nmm_path path,
                             void* workspace, size_t workspace_bytes, void* stream);
 
+/* Rounding of bf16 outputs: nearest with ties to even, or nearest with ties away from zero.
+ * The paper's output cast (Algorithm 2, Section IV-E) is named CAST_ROUND without a definition,
+ * so both nearest modes are offered; ties to even is the default reading. */
+typedef enum { NMM_ROUND_EVEN = 0, NMM_ROUND_AWAY = 1 } nmm_round;
+
+/*
+ * nmm_gemv_bf16 -- y_bf16[M,N] = bf16(x[M,K] . W[K,N]): nmm_gemv's fp32 sums, rounded once to
+ * bf16 in the same launch (Algorithm 2's output cast, Section IV-E; Alg. 2 returns C in bf16).
+ *
+ *   y_bf16, ldyb  bf16 output, y_bf16[m * ldyb + n]; 2-byte aligned, ldyb >= N (elements).
+ *   round         NMM_ROUND_EVEN or NMM_ROUND_AWAY (anything else: NMM_ERR_ARG).
+ *   y, ldy        optional fp32 copy of the same sums (NULL for none; ldy is then ignored).
+ *
+ * Everything else is as for nmm_gemv, including the workspace (nmm_gemv_workspace_size of the
+ * same shape) and both kernel families.  K == 0 writes +0.
+ */
+nmm_status nmm_gemv_bf16(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                         const void* x, int64_t ldx, const void* W, int64_t ldw,
+                         void* y_bf16, int64_t ldyb, nmm_round round,
+                         float* y, int64_t ldy, nmm_path path,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * nmm_mla_kv_update -- DeepSeek-V3 MLA's MatMul 2 for one token and the vector work the paper
+ * places behind it (Section IV-A: eq. 1 c^KV = W^DKV h, eq. 2 k^R = RoPE(W^KR h), eq. 3 the two
+ * as one product; then RMSNorm, RoPE and caching), in one launch:
+ *
+ *   mm       = h . W                  W = (W^DKV | W^KR)^T  [hidden, kv_lora + rope]  (eq. 4)
+ *   c'       = c / sqrt(mean(c^2) + eps) * gamma,      c = mm[:kv_lora]              (RMSNorm)
+ *   k'[2i]   = k[2i] cos(a_i) - k[2i+1] sin(a_i)       k = mm[kv_lora:]              (RoPE on
+ *   k'[2i+1] = k[2i] sin(a_i) + k[2i+1] cos(a_i)       a_i = position * theta^(-2i/rope)  adjacent
+ *   cache[position, 0 : kv_lora + rope] = bf16([c' | k'])                              pairs)
+ *
+ * RMSNorm follows Zhang and Sennrich's definition and RoPE RoFormer's (the paper names both
+ * without formulas).  W streams as in nmm_gemv (fp32 sums, K-slices added in slice order); the
+ * last workgroup to finish gathers the slices of every column and builds the entry in fp32 (RoPE
+ * angles formed and reduced modulo 2*pi in fp64) and rounds each value once to bf16 per `round`.  The layout of the entry is the latent cache that
+ * nmm_latent_attention reads (V = its first kv_lora columns).
+ *
+ * Fields (NMM_ERR_SHAPE, _ALIGN, _ARG or _NULL before any launch):
+ *   hidden, kv_lora, rope  > 0, > 0, even in [0, 512]; kv_lora + rope <= 4096.
+ *   h          [hidden] bf16 token, 16-byte aligned; the kernel reads whole 16-byte chunks up to
+ *              roundup(hidden, 8) elements (values past hidden are not used).
+ *   w, ldw     W above, bf16, 16-byte aligned, ldw >= kv_lora + rope and a multiple of 8.
+ *   gamma      [kv_lora] bf16 RMSNorm weight (2-byte aligned).
+ *   eps        finite, >= 0.          rope_theta   finite, > 0.
+ *   position   the token's position (its RoPE angle and its cache row), 0 <= position < cache_rows.
+ *   mm         [kv_lora + rope] fp32: MatMul 2's product, an output.
+ *   cache      bf16 latent cache [cache_rows, ld_cache], 2-byte aligned, ld_cache >= kv_lora +
+ *              rope; only row `position`, columns [0, kv_lora + rope), is written.
+ *   round      NMM_ROUND_EVEN or NMM_ROUND_AWAY.
+ * The workspace (nmm_mla_kv_update_workspace_size) holds the split-K partials and the arrival
+ * counters, the epilogue's among them; zeroed once at allocation, it is left zeroed.
+ */
+typedef struct {
+    int64_t hidden, kv_lora, rope;   /* DeepSeek-V3: 7168, 512, 64 */
+    const void* h;
+    const void* w;
+    int64_t ldw;
+    const void* gamma;
+    float eps, rope_theta;
+    int64_t position;
+    float* mm;
+    void* cache;
+    int64_t ld_cache, cache_rows;
+    nmm_round round;
+} nmm_mla_kv;
+
+nmm_status nmm_mla_kv_update(const nmm_mla_kv* kv, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
 /*
  * One DeepSeek-V3 MLA single-token decode chain of narrow MatMuls, all bf16 row-major [K,N]:
  *
@@ -185,6 +256,7 @@ size_t nmm_batched_gemv_workspace_size(int64_t batch, int64_t M, int64_t K, int6
                                        nmm_dtype dt, nmm_path path);
 size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain);
 size_t nmm_latent_attention_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v);
+size_t nmm_mla_kv_update_workspace_size(const nmm_mla_kv* kv);
 
 /* Zero a workspace on `stream` with a fill kernel (no memset node, so it is safe to capture). */
 nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream);

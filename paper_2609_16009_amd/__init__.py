@@ -21,6 +21,7 @@ NMM_OK, NMM_ERR_NULL, NMM_ERR_SHAPE, NMM_ERR_DTYPE, NMM_ERR_ALIGN, NMM_ERR_WORKS
     NMM_ERR_HIP, NMM_ERR_PATH, NMM_ERR_ARG = range(9)
 NMM_F16, NMM_BF16 = 1, 2
 NMM_PATH_AUTO, NMM_PATH_GEMV, NMM_PATH_MFMA = 0, 1, 2
+NMM_ROUND_EVEN, NMM_ROUND_AWAY = 0, 1
 
 _i64 = ctypes.c_int64
 _p = ctypes.c_void_p
@@ -55,11 +56,21 @@ class nmm_mla_chain(ctypes.Structure):
                                   "o_bf16", "events")] + [("n_events", ctypes.c_int)]
 
 
+class nmm_mla_kv(ctypes.Structure):
+    _fields_ = [("hidden", _i64), ("kv_lora", _i64), ("rope", _i64), ("h", _p), ("w", _p), ("ldw", _i64),
+                ("gamma", _p), ("eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("position", _i64),
+                ("mm", _p), ("cache", _p), ("ld_cache", _i64), ("cache_rows", _i64), ("round", ctypes.c_int)]
+
+
 EXPORTS = {
     "nmm_gemv": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
                                 ctypes.c_int, _p, _sz, _p]),
     "nmm_batched_gemv": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_int, _p, _i64, _i64, _p,
                                         _i64, _i64, _p, _i64, _i64, ctypes.c_int, _p, _sz, _p]),
+    "nmm_gemv_bf16": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
+                                     ctypes.c_int, _p, _i64, ctypes.c_int, _p, _sz, _p]),
+    "nmm_mla_kv_update": (ctypes.c_int, [ctypes.POINTER(nmm_mla_kv), _p, _sz, _p]),
+    "nmm_mla_kv_update_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_kv)]),
     "nmm_mla_decode_chain": (ctypes.c_int, [ctypes.POINTER(nmm_mla_chain), _p, _sz, _p]),
     "nmm_latent_attention": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64,
                                             ctypes.c_float, _p, _i64, _p, _sz, _p]),
@@ -164,6 +175,47 @@ def nmm_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None
     _check(lib().nmm_gemv(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y.data_ptr(),
                           _ld(y), path, wp, wb, _stream(stream)), "nmm_gemv")
     return y
+
+
+def nmm_gemv_bf16(x: torch.Tensor, W: torch.Tensor, y_bf16: torch.Tensor, *, round: int = NMM_ROUND_EVEN,
+                  y: torch.Tensor | None = None, N: int | None = None, path: int = NMM_PATH_AUTO,
+                  dt: int | None = None, workspace=None, stream=None) -> torch.Tensor:
+    """y_bf16[M,N] = bf16(x[M,K] . W[K,N]) rounded once per ``round``; ``y`` (fp32) optional."""
+    code = _dtype_code(x, dt)
+    M, K = x.shape[0], W.shape[0]
+    N = W.shape[1] if N is None else N
+    need = lib().nmm_gemv_workspace_size(M, K, N, code, path)
+    wp, wb = _workspace(workspace, need, x.device)
+    _check(lib().nmm_gemv_bf16(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y_bf16.data_ptr(),
+                               _ld(y_bf16), round, y.data_ptr() if y is not None else None,
+                               _ld(y) if y is not None else 0, path, wp, wb, _stream(stream)), "nmm_gemv_bf16")
+    return y_bf16
+
+
+def _kv_struct(h, w, gamma, mm, cache, *, kv_lora: int, rope: int, eps: float, theta: float,
+               position: int, round: int):
+    k = nmm_mla_kv()
+    k.hidden = w.shape[0] if w is not None else 0      # h may be padded to a multiple of 8
+    k.kv_lora, k.rope = int(kv_lora), int(rope)
+    for name, t in (("h", h), ("w", w), ("gamma", gamma), ("mm", mm), ("cache", cache)):
+        setattr(k, name, t.data_ptr() if t is not None else None)
+    k.ldw = _ld(w) if w is not None else 0
+    k.eps, k.rope_theta, k.position = float(eps), float(theta), int(position)
+    k.ld_cache = _ld(cache) if cache is not None else 0
+    k.cache_rows = cache.shape[0] if cache is not None else 0
+    k.round = int(round)
+    return k
+
+
+def nmm_mla_kv_update(h: torch.Tensor, w: torch.Tensor, gamma: torch.Tensor, mm: torch.Tensor,
+                      cache: torch.Tensor, *, kv_lora: int, rope: int, eps: float, theta: float,
+                      position: int, round: int = NMM_ROUND_EVEN, workspace=None, stream=None) -> None:
+    """MatMul 2 (h . w -> mm fp32) and the cache entry cache[position] = bf16([RMSNorm | RoPE])."""
+    k = _kv_struct(h, w, gamma, mm, cache, kv_lora=kv_lora, rope=rope, eps=eps, theta=theta,
+                   position=position, round=round)
+    need = lib().nmm_mla_kv_update_workspace_size(ctypes.byref(k))
+    wp, wb = _workspace(workspace, need, h.device)
+    _check(lib().nmm_mla_kv_update(ctypes.byref(k), wp, wb, _stream(stream)), "nmm_mla_kv_update")
 
 
 def nmm_batched_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None = None,

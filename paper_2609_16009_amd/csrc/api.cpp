@@ -14,6 +14,7 @@ using namespace nmm;
 namespace {
 
 size_t rup256(size_t v) { return (v + 255) / 256 * 256; }
+int64_t rup8(int64_t v) { return (v + 7) / 8 * 8; }
 
 // Workgroups of the persistent chain launch: one per compute unit of the current device, so
 // that all of them are resident together even beside other kernels (NMM_CHAIN_WGS overrides).
@@ -148,6 +149,37 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out, int unroll = 0) {
     return NMM_OK;
 }
 
+// MatMul 2 and its cache entry: the GEMV's arguments and plan, and the workspace they need (the
+// counter block always, for the epilogue's panel counter).
+struct KvUpdate {
+    GemvArgs args;
+    GemvPlan plan;
+    size_t ws_bytes = 0;
+};
+
+nmm_status build_kv_update(const nmm_mla_kv& k, KvUpdate* out) {
+    constexpr int64_t kLim = int64_t(1) << 31;
+    if (k.hidden <= 0 || k.kv_lora <= 0 || k.rope < 0 || (k.rope & 1) || k.hidden >= kLim ||
+        k.kv_lora + k.rope > kKvMaxWidth || k.rope > kKvMaxRope)
+        return NMM_ERR_SHAPE;
+    const int64_t n = k.kv_lora + k.rope;
+    if (k.ldw < n || k.ld_cache < n || k.cache_rows <= 0 || k.ld_cache >= kLim) return NMM_ERR_SHAPE;
+    if (k.position < 0 || k.position >= k.cache_rows) return NMM_ERR_SHAPE;
+    if (!std::isfinite(k.eps) || k.eps < 0.f || !std::isfinite(k.rope_theta) || k.rope_theta <= 0.f)
+        return NMM_ERR_ARG;
+    if (k.round != NMM_ROUND_EVEN && k.round != NMM_ROUND_AWAY) return NMM_ERR_ARG;
+    KvUpdate u;
+    GemvArgs& a = u.args;
+    a.M = 1; a.K = k.hidden; a.N = n; a.dt = NMM_BF16;
+    a.x = k.h; a.ldx = rup8(k.hidden); a.w = k.w; a.ldw = k.ldw; a.y = k.mm; a.ldy = n;
+    nmm_status st = plan_gemv(1, 1, a.K, a.N, NMM_BF16, NMM_PATH_GEMV, &u.plan);
+    if (st != NMM_OK) return st;
+    if (u.plan.n_tickets + 1 > kMaxTickets) return NMM_ERR_SHAPE;
+    u.ws_bytes = std::max<size_t>(u.plan.ws_bytes, kTicketBytes);
+    *out = u;
+    return NMM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -171,6 +203,23 @@ nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_
     a.x = x; a.ldx = ldx; a.sx = stride_x;
     a.w = W; a.ldw = ldw; a.sw = stride_w;
     a.y = y; a.ldy = ldy; a.sy = stride_y;
+    return gemv_common(a, path, workspace, workspace_bytes, stream);
+}
+
+nmm_status nmm_gemv_bf16(int64_t M, int64_t K, int64_t N, nmm_dtype dt, const void* x, int64_t ldx,
+                         const void* W, int64_t ldw, void* y_bf16, int64_t ldyb, nmm_round round,
+                         float* y, int64_t ldy, nmm_path path, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+    if (round != NMM_ROUND_EVEN && round != NMM_ROUND_AWAY) return NMM_ERR_ARG;
+    GemvArgs a;
+    a.M = M; a.K = K; a.N = N; a.dt = dt;
+    a.x = x; a.ldx = ldx; a.w = W; a.ldw = ldw;
+    a.y = y; a.ldy = y ? ldy : 0;
+    if (M > 0 && N > 0 && !y_bf16) return NMM_ERR_NULL;
+    if (ldyb < N) return NMM_ERR_SHAPE;
+    // one group spanning every column: ybf[m * ldyb + n]
+    a.ybf = y_bf16; a.ybf_group = std::max<int64_t>(N, 1); a.ybf_keep = a.ybf_group; a.ybf_ldm = ldyb;
+    a.ybf_away = round == NMM_ROUND_AWAY ? 1 : 0;
     return gemv_common(a, path, workspace, workspace_bytes, stream);
 }
 
@@ -286,6 +335,41 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
     if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[5]), s) != hipSuccess)
         return NMM_ERR_HIP;
     return NMM_OK;
+}
+
+size_t nmm_mla_kv_update_workspace_size(const nmm_mla_kv* kv) {
+    if (!kv) return 0;
+    KvUpdate u;
+    return build_kv_update(*kv, &u) == NMM_OK ? u.ws_bytes : 0;
+}
+
+nmm_status nmm_mla_kv_update(const nmm_mla_kv* kv, void* workspace, size_t workspace_bytes, void* stream) {
+    if (!kv) return NMM_ERR_NULL;
+    const nmm_mla_kv& k = *kv;
+    if (!k.h || !k.w || !k.gamma || !k.mm || !k.cache) return NMM_ERR_NULL;
+    KvUpdate u;
+    nmm_status st = build_kv_update(k, &u);
+    if (st != NMM_OK) return st;
+    st = validate_gemv(u.args, NMM_PATH_GEMV);
+    if (st != NMM_OK) return st;
+    if (reinterpret_cast<uintptr_t>(k.gamma) & 1u || reinterpret_cast<uintptr_t>(k.cache) & 1u) return NMM_ERR_ALIGN;
+    st = validate_workspace(workspace, workspace_bytes, u.ws_bytes);
+    if (st != NMM_OK) return st;
+    unsigned* counters = static_cast<unsigned*>(workspace);
+    float* part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes);
+    KvEpilogue e;
+    e.gamma = k.gamma;
+    e.row = static_cast<uint16_t*>(k.cache) + k.position * k.ld_cache;
+    e.done = counters + u.plan.n_tickets;
+    e.eps = k.eps;
+    e.theta = k.rope_theta;
+    e.position = k.position;
+    e.c_off = 0;
+    e.kv = static_cast<int>(k.kv_lora);
+    e.rope = static_cast<int>(k.rope);
+    e.away = k.round == NMM_ROUND_AWAY ? 1 : 0;
+    return launch_gemv_kv(u.args, u.plan, u.plan.split() ? counters : nullptr, u.plan.split() ? part : nullptr, e,
+                          stream);
 }
 
 nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream) {

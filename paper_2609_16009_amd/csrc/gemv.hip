@@ -23,9 +23,11 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstdlib>
 
+#include "bf16_cast.h"
 #include "nmm_internal.h"
 
 namespace nmm {
@@ -50,6 +52,7 @@ struct KParams {
     int64_t ldy, sy;
     uint16_t* ybf;
     int64_t ybf_group, ybf_keep, ybf_ldm, ybf_sb;
+    int ybf_away;          // bf16 rounding of ybf: 0 nearest-even, 1 nearest with ties away from zero
     float* part;
     unsigned* tickets;
     int M, K, N;
@@ -163,26 +166,33 @@ __device__ __forceinline__ void stream_rows(float (&acc)[MT][8], i32x4 (&buf)[U]
     for (int u = 0; u < U; ++u) fma_chunk<DT, MT>(acc, buf[u], xs + (s + u) * xs_step);
 }
 
-__device__ __forceinline__ uint16_t to_bf16_bits(float v) {
-    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
-}
-
 // Cache policy of x loads inside the fused chain: device-coherent (sc1), because x was written
 // by other workgroups of the same launch and this XCD's L2 may hold older copies.
 constexpr int kLoadCoherent = 16;
 
-// y[m, n] (fp32) and its optional bf16 copy.  Inside the fused chain the bf16 copy is the next
-// MatMul's operand, read by other workgroups during the same launch, so it is written with a
-// device-scope atomic store (coherent at memory).
-template <bool CHAIN>
+// How y and its bf16 copy are stored.  Inside the fused chain the bf16 copy is the next
+// MatMul's operand, read by other workgroups during the same launch; after MatMul 2 the fp32 y
+// is read by the launch's last workgroup (the cache-entry epilogue).  Those stores are
+// device-scope atomic stores (coherent at memory).
+constexpr int kStorePlain = 0;   // separate launch: plain stores
+constexpr int kStoreChain = 1;   // the bf16 copy coherent
+constexpr int kStoreEpi = 2;     // y coherent
+constexpr int kStoreNoY = 3;     // separate launch with the bf16 copy only (y is null)
+
+// y[m, n] (fp32) and its optional bf16 copy.
+template <int SM>
 __device__ __forceinline__ void store_out(const KParams& p, int64_t b, int m, int n, float v) {
-    p.y[b * p.sy + int64_t(m) * p.ldy + n] = v;
+    if constexpr (SM != kStoreNoY) {
+        float* yd = p.y + b * p.sy + int64_t(m) * p.ldy + n;
+        if constexpr (SM == kStoreEpi) __hip_atomic_store(yd, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else *yd = v;
+    }
     if (p.ybf) {
         const int64_t g = n / p.ybf_group, r = n - g * p.ybf_group;
         if (r < p.ybf_keep) {
             uint16_t* dst = p.ybf + b * p.ybf_sb + int64_t(m) * p.ybf_ldm + g * p.ybf_keep + r;
-            if constexpr (CHAIN) __hip_atomic_store(dst, to_bf16_bits(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            else *dst = to_bf16_bits(v);
+            if constexpr (SM == kStoreChain) __hip_atomic_store(dst, to_bf16_bits(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            else *dst = to_bf16_mode(v, p.ybf_away);
         }
     }
 }
@@ -325,7 +335,7 @@ __device__ __forceinline__ float add_xor32(float x) {
 // Gather, part 1: each wave folds its row groups with the butterfly above (lanes r*cw + c and
 // r'*cw + c hold the same columns), then the four waves are summed through LDS in wave order.  A panel with one K-slice writes y; otherwise the slice's partial
 // sums go to the workspace with device-scope stores (coherent past the per-XCD L2 caches).
-template <int MT, bool CHAIN>
+template <int MT, int SM>
 __device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, float (&acc)[MT][8], float* lds,
                                             int tid) {
     const int lane = tid & 63, wave = tid >> 6;
@@ -363,7 +373,7 @@ __device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, fl
             const int m = g + mm;
             const int n = it.chunk0 * 8 + col;
             if (it.ks == 1) {
-                if (it.m0 + m < p.M && n < p.N) store_out<CHAIN>(p, it.b, it.m0 + m, n, v);
+                if (it.m0 + m < p.M && n < p.N) store_out<SM>(p, it.b, it.m0 + m, n, v);
             } else {
                 __hip_atomic_store(p.part + pbase + int64_t(it.slice) * (MT * kPanelCols) + m * kPanelCols + col,
                                    v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -375,7 +385,7 @@ __device__ __forceinline__ void reduce_item(const KParams& p, const Item& it, fl
 
 // Gather, part 2 (the panel's last workgroup only): every output of the panel sums its K-slices
 // in slice order; the loads of R outputs x QB slices are all in flight before any is added.
-template <int MT, bool CHAIN>
+template <int MT, int SM>
 __device__ __forceinline__ void gather_panel(const KParams& p, const Item& it, int tid) {
     constexpr int R = (MT * 2 < 8) ? MT * 2 : 8;   // outputs per thread per pass (pcols <= 512)
     constexpr int QB = 32 / R;                      // slices per batch
@@ -411,7 +421,7 @@ __device__ __forceinline__ void gather_panel(const KParams& p, const Item& it, i
             const int o = o0 + r * kThreads;
             const int m = o / pcols, col = o - m * pcols;
             const int n = it.chunk0 * 8 + col;
-            if (o < n_out && it.m0 + m < p.M && n < p.N) store_out<CHAIN>(p, it.b, it.m0 + m, n, sum[r]);
+            if (o < n_out && it.m0 + m < p.M && n < p.N) store_out<SM>(p, it.b, it.m0 + m, n, sum[r]);
         }
     }
 }
@@ -422,12 +432,10 @@ __device__ __forceinline__ unsigned* ticket_of(const KParams& p, const Item& it)
     return p.tickets + (it.b * p.mblocks + it.mb) * p.n_panels + it.panel;
 }
 
-// One work item of a separate GEMV launch.
+// A work item's stream: stage its x slice, then multiply its K-slice of the panel into acc.
 template <int DT, int MT, int U>
-__device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float* lds, int* s_last) {
-    const int tid = threadIdx.x;
-    const Item it = item_of<MT>(p, bid, tid);
-
+__device__ __forceinline__ void stream_item(const KParams& p, const Item& it, float* lds, float (&acc)[MT][8],
+                                            int tid) {
     // ---- init: issue x's loads, then the first U loads of W, then commit x to LDS while the W
     // loads are still in flight
     const Stream st = stream_of(p, it);
@@ -439,7 +447,6 @@ __device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float*
     __syncthreads();
 
     // ---- compute: stream this workgroup's rows of the panel
-    float acc[MT][8];
 #pragma unroll
     for (int m = 0; m < MT; ++m)
 #pragma unroll
@@ -450,10 +457,14 @@ __device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float*
         stream_rows<DT, MT, U, true>(acc, buf, st, nsteps, xs, it.rstep * MT);
     }
     __syncthreads();   // x slice no longer needed: LDS becomes the reduction buffer
+}
 
-    // ---- gather
-    reduce_item<MT, false>(p, it, acc, lds, tid);
-    if (it.ks == 1) return;
+// The gather of one panel (reduce_item has run): a single K-slice has written y already;
+// otherwise the slice takes the panel's ticket and the last to arrive sums the slices.  Returns
+// whether this workgroup wrote the panel's final outputs.
+template <int MT, int SM>
+__device__ __forceinline__ bool finish_panel(const KParams& p, const Item& it, int* s_last, int tid) {
+    if (it.ks == 1) return true;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
@@ -464,14 +475,140 @@ __device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float*
         *s_last = last;
     }
     __syncthreads();
-    if (*s_last) gather_panel<MT, false>(p, it, tid);
+    if (!*s_last) return false;
+    gather_panel<MT, SM>(p, it, tid);
+    return true;
 }
 
-template <int DT, int MT, int U>
+// One work item of a separate GEMV launch (SM: kStorePlain or kStoreNoY).
+template <int DT, int MT, int U, int SM>
+__device__ __forceinline__ void gemv_item(const KParams& p, uint32_t bid, float* lds, int* s_last) {
+    const int tid = threadIdx.x;
+    const Item it = item_of<MT>(p, bid, tid);
+    float acc[MT][8];
+    stream_item<DT, MT, U>(p, it, lds, acc, tid);
+    reduce_item<MT, SM>(p, it, acc, lds, tid);
+    (void)finish_panel<MT, SM>(p, it, s_last, tid);
+}
+
+template <int DT, int MT, int U, int SM>
 __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
     extern __shared__ float lds[];
     __shared__ int s_last;
-    gemv_item<DT, MT, U>(p, blockIdx.x, lds, &s_last);
+    gemv_item<DT, MT, U, SM>(p, blockIdx.x, lds, &s_last);
+}
+
+// ---------------------------------------------------------------------------------------------
+// MatMul 2 and the vector work behind it (Section IV-A, eq. 1-3): y = [c^KV | k^R] = h . W, then
+// the cache entry [RMSNorm(c^KV) | RoPE(k^R, t)] in bf16.  The GEMV runs as above, except that
+// y is stored device-coherently; every workgroup that writes the final outputs of a panel
+// covering [c_off, c_off + kv + rope) counts the panel in on one counter, and the one that
+// counts in last builds the entry from y.  No workgroup waits for another, so the launch cannot
+// deadlock whatever else is resident.
+// ---------------------------------------------------------------------------------------------
+struct KvParams {
+    const uint16_t* gamma;   // [kv] bf16 RMSNorm weight
+    uint16_t* row;           // the cache row (bf16, kv + rope values)
+    unsigned* done;          // the panel counter (zero before and after the launch)
+    float eps;
+    double freq_step;        // theta^(-2/rope): pair j turns freq_step^j radians per position
+    int64_t position;
+    int c_off, kv, rope, away;
+    int first_panel, n_panels;   // the panels covering the entry's columns
+};
+
+constexpr double kTwoPiHi = 6.283185307179586;          // 2*pi rounded to double
+constexpr double kTwoPiLo = 2.4492935982947064e-16;     // 2*pi - kTwoPiHi
+constexpr double kInvTwoPi = 0.15915494309189535;
+
+// Sine and cosine of RoPE pair j's angle a = t * theta^(-2j/rope) = t * freq_step^j.  The power
+// is taken by binary powering and a formed in fp64 (relative error a few units of 2^-53), then a
+// is reduced to [-pi, pi] by a two-term Cody-Waite step with fused multiply-adds (k * kTwoPiHi
+// is exact for |k| < 2^30, i.e. positions below 2^31); the sine and cosine of the reduced angle
+// are taken in fp32.
+__device__ __forceinline__ void rope_angle(const KvParams& e, int j, float* sn, float* cs) {
+    double f = 1.0, b = e.freq_step;
+    for (int n = j; n; n >>= 1) {
+        if (n & 1) f *= b;
+        b *= b;
+    }
+    const double a = double(e.position) * f;
+    const double k = rint(a * kInvTwoPi);
+    const double r = fma(-k, kTwoPiLo, fma(-k, kTwoPiHi, a));
+    sincosf(float(r), sn, cs);
+}
+
+// The entry, built by the workgroup that counts the last panel in: y[c_off ..] and gamma are
+// staged in LDS in one pass (one round trip), then RMSNorm and RoPE (sn, cs: this thread's
+// pair, taken earlier).
+__device__ __forceinline__ void kv_entry(const KParams& p, const KvParams& e, float* lds, float sn, float cs) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int n_all = e.kv + e.rope;
+    float* vals = lds;                  // [n_all]
+    float* gam = lds + n_all;           // [kv]
+    float* red = gam + e.kv;            // [kWaves]
+    float ss = 0.f;
+    for (int i = tid; i < n_all; i += kThreads) {
+        const float v = __hip_atomic_load(p.y + e.c_off + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        vals[i] = v;
+        if (i < e.kv) {
+            gam[i] = __uint_as_float(uint32_t(e.gamma[i]) << 16);
+            ss += v * v;
+        }
+    }
+    // mean of squares: a fixed butterfly inside each wave, then the waves in order
+    ss = add_ror<1>(ss);
+    ss = add_ror<2>(ss);
+    ss = add_ror<4>(ss);
+    ss = add_ror<8>(ss);
+    ss = add_xor16(ss);
+    ss = add_xor32(ss);
+    if (lane == 0) red[wave] = ss;
+    __syncthreads();
+    float tot = red[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) tot += red[w];
+    const float inv = 1.0f / __builtin_sqrtf(tot / float(e.kv) + e.eps);
+    for (int i = tid; i < e.kv; i += kThreads) e.row[i] = to_bf16_mode(vals[i] * inv * gam[i], e.away);
+    if (tid < e.rope / 2) {
+        const float k0 = vals[e.kv + 2 * tid], k1 = vals[e.kv + 2 * tid + 1];
+        e.row[e.kv + 2 * tid] = to_bf16_mode(k0 * cs - k1 * sn, e.away);
+        e.row[e.kv + 2 * tid + 1] = to_bf16_mode(k0 * sn + k1 * cs, e.away);
+    }
+}
+
+template <int U>
+__global__ __launch_bounds__(kThreads) void gemv_kv_kernel(const KParams p, const KvParams e) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    const int tid = threadIdx.x;
+    const Item it = item_of<1>(p, blockIdx.x, tid);
+    const bool counted = it.panel >= e.first_panel && it.panel < e.first_panel + e.n_panels;
+    float acc[1][8];
+    stream_item<NMM_BF16, 1, U>(p, it, lds, acc, tid);
+    if (!counted) {
+        reduce_item<1, kStorePlain>(p, it, acc, lds, tid);
+        (void)finish_panel<1, kStorePlain>(p, it, &s_last, tid);
+        return;
+    }
+    reduce_item<1, kStoreEpi>(p, it, acc, lds, tid);
+    if (!finish_panel<1, kStoreEpi>(p, it, &s_last, tid)) return;
+    // each workgroup that completes a panel takes the RoPE sines and cosines while its last
+    // stores complete (the empty asm keeps the computation here); the last to count in uses them
+    float sn = 0.f, cs = 1.f;
+    if (tid < e.rope / 2) rope_angle(e, tid, &sn, &cs);
+    asm volatile("" : "+v"(sn), "+v"(cs));
+    // the panel's outputs are final: let their stores complete, then count the panel in
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        const unsigned prev = __hip_atomic_fetch_add(e.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int last = prev == unsigned(e.n_panels - 1);
+        if (last) __hip_atomic_store(e.done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = last;
+    }
+    __syncthreads();
+    if (s_last) kv_entry(p, e, lds, sn, cs);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -587,7 +724,7 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(const ChainArgs a) {
         for (int j = 0; j < 8; ++j) acc[0][j] = 0.f;
         stream_rows<NMM_BF16, 1, U, true>(acc, buf, ss, it.rows / it.rstep, lds + it.rin, it.rstep);
         __syncthreads();
-        reduce_item<1, true>(p, it, acc, lds, tid);
+        reduce_item<1, kStoreChain>(p, it, acc, lds, tid);
         __builtin_amdgcn_s_waitcnt(0);   // this item's stores are complete
         __syncthreads();
         unsigned prev = 0;
@@ -614,7 +751,7 @@ __global__ __launch_bounds__(kThreads) void chain_kernel(const ChainArgs a) {
             }
             __syncthreads();
             if (s_last) {
-                gather_panel<1, true>(p, it, tid);
+                gather_panel<1, kStoreChain>(p, it, tid);
                 __builtin_amdgcn_s_waitcnt(0);
                 __syncthreads();
                 if (tid == 0) raise_flag(a, st, it);
@@ -651,7 +788,7 @@ __global__ void zero_output_kernel(float* y, int64_t ldy, int64_t sy, uint16_t* 
     for (int64_t i = blockIdx.x * int64_t(blockDim.x) + threadIdx.x; i < total;
          i += int64_t(gridDim.x) * blockDim.x) {
         const int64_t n = i % N, m = (i / N) % M, b = i / (N * M);
-        y[b * sy + m * ldy + n] = 0.f;
+        if (y) y[b * sy + m * ldy + n] = 0.f;
         if (ybf) {
             const int64_t g = n / group, r = n - g * group;
             if (r < keep) ybf[b * sb + m * ldm + g * keep + r] = 0;
@@ -670,7 +807,10 @@ __global__ void zero_bytes_kernel(uint8_t* p, size_t bytes) {
 
 template <int DT, int MT, int U>
 void launch_t(const KParams& kp, int64_t grid, size_t lds, hipStream_t s) {
-    hipLaunchKernelGGL((gemv_kernel<DT, MT, U>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, kp);
+    if (kp.y)
+        hipLaunchKernelGGL((gemv_kernel<DT, MT, U, kStorePlain>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, kp);
+    else
+        hipLaunchKernelGGL((gemv_kernel<DT, MT, U, kStoreNoY>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, kp);
 }
 
 template <int DT, int MT>
@@ -728,6 +868,7 @@ KParams make_params(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, flo
     kp.ybf_keep = a.ybf_keep;
     kp.ybf_ldm = a.ybf_ldm;
     kp.ybf_sb = a.ybf_sb;
+    kp.ybf_away = a.ybf_away;
     kp.M = static_cast<int>(a.M);
     kp.K = static_cast<int>(a.K);
     kp.N = static_cast<int>(a.N);
@@ -777,6 +918,39 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
     if (a.dt == NMM_BF16) launch_m<NMM_BF16>(kp, p.grid, lds, p.mt, p.unroll, s);
     else launch_m<NMM_F16>(kp, p.grid, lds, p.mt, p.unroll, s);
     return last_launch_status();
+}
+
+nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
+                          const KvEpilogue& e, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const KParams kp = make_params(a, p, tickets, part);
+    KvParams kv{};
+    kv.gamma = static_cast<const uint16_t*>(e.gamma);
+    kv.row = static_cast<uint16_t*>(e.row);
+    kv.done = e.done;
+    kv.eps = e.eps;
+    kv.freq_step = e.rope > 0 ? std::pow(double(e.theta), -2.0 / double(e.rope)) : 1.0;
+    kv.position = e.position;
+    kv.c_off = static_cast<int>(e.c_off);
+    kv.kv = e.kv;
+    kv.rope = e.rope;
+    kv.away = e.away;
+    const int64_t pcols = int64_t(p.cw_full) * 8;
+    kv.first_panel = static_cast<int>(e.c_off / pcols);
+    kv.n_panels = static_cast<int>((e.c_off + e.kv + e.rope - 1) / pcols) - kv.first_panel + 1;
+    const size_t lds = gemv_kv_lds_bytes(p, e.kv, e.rope);
+    const dim3 grid(static_cast<uint32_t>(p.grid)), block(kThreads);
+    switch (p.unroll) {
+        case 16: hipLaunchKernelGGL(gemv_kv_kernel<16>, grid, block, lds, s, kp, kv); break;
+        case 8: hipLaunchKernelGGL(gemv_kv_kernel<8>, grid, block, lds, s, kp, kv); break;
+        case 4: hipLaunchKernelGGL(gemv_kv_kernel<4>, grid, block, lds, s, kp, kv); break;
+        default: hipLaunchKernelGGL(gemv_kv_kernel<2>, grid, block, lds, s, kp, kv); break;
+    }
+    return last_launch_status();
+}
+
+size_t gemv_kv_lds_bytes(const GemvPlan& p, int kv, int rope) {
+    return std::max(gemv_lds_bytes(p), size_t(2 * kv + rope + kWaves) * 4);
 }
 
 bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n) {

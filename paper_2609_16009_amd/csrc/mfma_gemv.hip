@@ -24,6 +24,7 @@
 #include <algorithm>
 #include <cstdint>
 
+#include "bf16_cast.h"
 #include "nmm_internal.h"
 
 namespace nmm {
@@ -49,8 +50,11 @@ struct MParams {
     const uint16_t* x;
     int64_t ldx;
     const uint16_t* w;
-    float* y;
+    float* y;              // fp32 output (may be null when ybf is set)
     int64_t ldy;
+    uint16_t* ybf;         // optional bf16 output, ybf[m * ldyb + n]
+    int64_t ldyb;
+    int away;              // bf16 rounding: 0 nearest-even, 1 ties away from zero
     float* part;
     unsigned* tickets;
     int M, K, N;
@@ -60,6 +64,17 @@ struct MParams {
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+// An output: fp32 y only (BF false), or the bf16 copy and, when y is not null, y as well.
+template <bool BF>
+__device__ __forceinline__ void put_y(const MParams& p, int m, int n, float v) {
+    if constexpr (BF) {
+        if (p.y) p.y[int64_t(m) * p.ldy + n] = v;
+        p.ybf[int64_t(m) * p.ldyb + n] = to_bf16_mode(v, p.away);
+    } else {
+        p.y[int64_t(m) * p.ldy + n] = v;
+    }
 }
 
 template <int DT>
@@ -86,7 +101,7 @@ __device__ __forceinline__ i32x4 load_b(const uint16_t* wst, int row0, int col0,
     return i32x4{int(lo.x), int(lo.y), int(hi.x), int(hi.y)};
 }
 
-template <int DT, int MT, int D>
+template <int DT, int MT, int D, bool BF>
 __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
     // two stage buffers, each a W tile [64][kWStride] followed by an x tile [MT][kXStride]
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
@@ -200,7 +215,7 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int m = m0 + 16 * mt + 4 * g + i, n = n0 + 16 * (2 * wave + t) + j;
-                    if (m < p.M && n < p.N) p.y[int64_t(m) * p.ldy + n] = acc[mt][t][i];
+                    if (m < p.M && n < p.N) put_y<BF>(p, m, n, acc[mt][t][i]);
                 }
         return;
     }
@@ -255,13 +270,16 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
     for (int r = 0; r < PER; ++r) {
         const int o = tid + r * kThreads;
         const int m = m0 + o / kMfmaPanelCols, n = n0 + o % kMfmaPanelCols;
-        if (m < p.M && n < p.N) p.y[int64_t(m) * p.ldy + n] = sum[r];
+        if (m < p.M && n < p.N) put_y<BF>(p, m, n, sum[r]);
     }
 }
 
 template <int DT, int MT>
 void launch_mt(const MParams& mp, int64_t grid, size_t lds, hipStream_t s) {
-    hipLaunchKernelGGL((mfma_gemv_kernel<DT, MT, kMfmaDepth>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, mp);
+    if (mp.ybf)
+        hipLaunchKernelGGL((mfma_gemv_kernel<DT, MT, kMfmaDepth, true>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, mp);
+    else
+        hipLaunchKernelGGL((mfma_gemv_kernel<DT, MT, kMfmaDepth, false>), dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, mp);
 }
 
 }  // namespace
@@ -277,6 +295,9 @@ nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
     mp.w = static_cast<const uint16_t*>(a.w);
     mp.y = a.y;
     mp.ldy = a.ldy;
+    mp.ybf = static_cast<uint16_t*>(a.ybf);
+    mp.ldyb = a.ybf_ldm;
+    mp.away = a.ybf_away;
     mp.part = part;
     mp.tickets = tickets;
     mp.M = static_cast<int>(a.M);

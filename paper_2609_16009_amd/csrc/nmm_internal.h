@@ -70,7 +70,22 @@ struct GemvArgs {
     //   ybf[b*ybf_sb + m*ybf_ldm + (n / ybf_group) * ybf_keep + (n % ybf_group)]
     // when (n % ybf_group) < ybf_keep.
     void* ybf = nullptr; int64_t ybf_group = 0, ybf_keep = 0, ybf_ldm = 0, ybf_sb = 0;
+    int ybf_away = 0;   // rounding of ybf: 0 nearest-even, 1 nearest with ties away from zero
 };
+
+// The cache entry behind MatMul 2 (gemv.hip): y[c_off .. c_off + kv + rope) of an M = 1 bf16 GEMV
+// becomes row = bf16([RMSNorm(c) * gamma | RoPE(k, position)]).  `done` is a counter in the
+// workspace's counter block, zero before and after the launch.
+struct KvEpilogue {
+    const void* gamma = nullptr;
+    void* row = nullptr;
+    unsigned* done = nullptr;
+    float eps = 0.f, theta = 0.f;
+    int64_t position = 0, c_off = 0;
+    int kv = 0, rope = 0, away = 0;
+};
+constexpr int kKvMaxWidth = 4096;   // kv + rope values the epilogue stages in LDS
+constexpr int kKvMaxRope = 512;     // RoPE width: one pair per thread of a 256-thread workgroup
 
 // Pure host functions (no HIP calls): argument checks and the partition.
 nmm_status validate_gemv(const GemvArgs& a, int path);
@@ -85,6 +100,11 @@ nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
 // plan does not split K).
 nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
+// The GEMV of a validated M = 1 bf16 plan (path GEMV) followed in the same launch by the cache
+// entry of `e` (K > 0).
+nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
+                          const KvEpilogue& e, void* stream);
+size_t gemv_kv_lds_bytes(const GemvPlan& p, int kv, int rope);
 
 // The fused decode chain: n (<= 5) M = 1 bf16 GEMVs in one persistent launch.  `sync` points to
 // the chain's words in the counter block: [1] exited workgroups, [2] error word (sticky);

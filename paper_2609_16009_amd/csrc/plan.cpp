@@ -61,20 +61,23 @@ nmm_status validate_gemv(const GemvArgs& a, int path) {
         return NMM_ERR_SHAPE;
     if (a.sx < 0 || a.sw < 0 || a.sy < 0) return NMM_ERR_SHAPE;
     if (a.batch == 0 || a.M == 0 || a.N == 0) return NMM_OK;          // nothing is touched
-    if (!a.y) return NMM_ERR_NULL;
-    if (a.ldy < a.N) return NMM_ERR_SHAPE;
+    if (!a.y && !a.ybf) return NMM_ERR_NULL;                         // some output is required
+    if (a.y && a.ldy < a.N) return NMM_ERR_SHAPE;
+    if (a.ybf && (a.ybf_ldm < 0 || a.ybf_ldm >= kLimit)) return NMM_ERR_SHAPE;
+    if (a.ybf && (a.ybf_group <= 0 || a.ybf_keep <= 0 || a.ybf_keep > a.ybf_group)) return NMM_ERR_ARG;
+    if (a.ybf_away != 0 && a.ybf_away != 1) return NMM_ERR_ARG;
+    if ((a.y && (reinterpret_cast<uintptr_t>(a.y) & 3u)) || (reinterpret_cast<uintptr_t>(a.ybf) & 1u))
+        return NMM_ERR_ALIGN;
     if (a.K == 0) return NMM_OK;                                      // y = 0; x and W unused
     if (!a.x || !a.w) return NMM_ERR_NULL;
     if (a.ldx < a.K || a.ldw < a.N) return NMM_ERR_SHAPE;
     if (!aligned16(a.x) || !aligned16(a.w) || a.ldx % 8 || a.ldw % 8 || a.sx % 8 || a.sw % 8)
         return NMM_ERR_ALIGN;
-    if ((reinterpret_cast<uintptr_t>(a.y) & 3u) != 0) return NMM_ERR_ALIGN;
     const int64_t extent = ((a.K - 1) * a.ldw + rup(a.N, 8)) * 2;    // bytes of one W
     if (extent >= kLimit) return NMM_ERR_SHAPE;
     // bytes of x one row block reads (blocks are at most 32 rows)
     const int64_t x_extent = ((std::min<int64_t>(a.M, 32) - 1) * a.ldx + rup(a.K, 8)) * 2;
     if (x_extent >= kLimit) return NMM_ERR_SHAPE;
-    if (a.ybf && (a.ybf_group <= 0 || a.ybf_keep <= 0 || a.ybf_keep > a.ybf_group)) return NMM_ERR_ARG;
     return NMM_OK;
 }
 

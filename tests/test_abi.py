@@ -155,3 +155,94 @@ def test_plan_rejects_unavailable_path_and_bad_dtype():
     assert L.nmm_gemv_plan(1, 1, 64, 64, 7, 0, ctypes.byref(info)) == nmm.NMM_ERR_DTYPE
     assert L.nmm_gemv_plan(1, 1, 64, 64, nmm.NMM_BF16, 5, ctypes.byref(info)) == nmm.NMM_ERR_PATH
     assert L.nmm_gemv_plan(1, 1, 64, 64, nmm.NMM_BF16, 0, None) == nmm.NMM_ERR_NULL
+
+
+def gemv_bf16(**kw):
+    a = dict(M=1, K=64, N=64, dt=nmm.NMM_BF16, x=ALIGNED, ldx=64, W=ALIGNED, ldw=64, yb=ALIGNED, ldyb=64,
+             round=nmm.NMM_ROUND_EVEN, y=None, ldy=0, path=nmm.NMM_PATH_AUTO, ws=ALIGNED, wsb=1 << 30,
+             stream=None)
+    a.update(kw)
+    return L.nmm_gemv_bf16(a["M"], a["K"], a["N"], a["dt"], a["x"], a["ldx"], a["W"], a["ldw"], a["yb"],
+                           a["ldyb"], a["round"], a["y"], a["ldy"], a["path"], a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(yb=None), nmm.NMM_ERR_NULL),
+    (dict(round=2), nmm.NMM_ERR_ARG),
+    (dict(round=-1), nmm.NMM_ERR_ARG),
+    (dict(ldyb=63), nmm.NMM_ERR_SHAPE),
+    (dict(yb=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+    (dict(y=ALIGNED, ldy=32), nmm.NMM_ERR_SHAPE),
+    (dict(y=ALIGNED + 2, ldy=64), nmm.NMM_ERR_ALIGN),
+    (dict(x=None), nmm.NMM_ERR_NULL),
+    (dict(M=-1), nmm.NMM_ERR_SHAPE),
+    (dict(K=4096, N=4096, ldw=4096, ldyb=4096, ldx=4096, ws=None), nmm.NMM_ERR_WORKSPACE),
+])
+def test_gemv_bf16_rejects_invalid_arguments(kw, status):
+    assert gemv_bf16(**kw) == status
+
+
+@pytest.mark.parametrize("kw", [dict(M=0), dict(N=0, ldyb=0), dict(M=0, yb=None, x=None)])
+def test_gemv_bf16_empty_problems_are_noops(kw):
+    assert gemv_bf16(**kw) == nmm.NMM_OK
+
+
+def kv_struct(**kw):
+    k = nmm.nmm_mla_kv()
+    vals = dict(hidden=7168, kv_lora=512, rope=64, h=ALIGNED, w=ALIGNED, ldw=576, gamma=ALIGNED, eps=1e-6,
+                rope_theta=10000.0, position=4096, mm=ALIGNED, cache=ALIGNED, ld_cache=576, cache_rows=4097,
+                round=nmm.NMM_ROUND_EVEN)
+    vals.update(kw)
+    for name, v in vals.items():
+        setattr(k, name, v)
+    return k
+
+
+def test_kv_update_workspace_covers_the_counter_block():
+    k = kv_struct()
+    need = L.nmm_mla_kv_update_workspace_size(ctypes.byref(k))
+    plan = nmm.nmm_gemv_plan(1, 7168, 576, path=nmm.NMM_PATH_GEMV)
+    assert need >= 64 * 1024 and need >= plan["workspace_bytes"]
+    assert L.nmm_mla_kv_update_workspace_size(ctypes.byref(kv_struct(rope=63))) == 0
+    assert L.nmm_mla_kv_update_workspace_size(None) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(h=None), nmm.NMM_ERR_NULL),
+    (dict(w=None), nmm.NMM_ERR_NULL),
+    (dict(gamma=None), nmm.NMM_ERR_NULL),
+    (dict(mm=None), nmm.NMM_ERR_NULL),
+    (dict(cache=None), nmm.NMM_ERR_NULL),
+    (dict(hidden=0), nmm.NMM_ERR_SHAPE),
+    (dict(kv_lora=0), nmm.NMM_ERR_SHAPE),
+    (dict(rope=63, ldw=576), nmm.NMM_ERR_SHAPE),
+    (dict(rope=-2), nmm.NMM_ERR_SHAPE),
+    (dict(rope=514, ldw=1032, ld_cache=1032), nmm.NMM_ERR_SHAPE),
+    (dict(kv_lora=4096, rope=64, ldw=4160, ld_cache=4160), nmm.NMM_ERR_SHAPE),
+    (dict(ldw=568), nmm.NMM_ERR_SHAPE),
+    (dict(ld_cache=575), nmm.NMM_ERR_SHAPE),
+    (dict(position=4097), nmm.NMM_ERR_SHAPE),
+    (dict(position=-1), nmm.NMM_ERR_SHAPE),
+    (dict(cache_rows=0, position=0), nmm.NMM_ERR_SHAPE),
+    (dict(eps=-1.0), nmm.NMM_ERR_ARG),
+    (dict(eps=float("nan")), nmm.NMM_ERR_ARG),
+    (dict(rope_theta=0.0), nmm.NMM_ERR_ARG),
+    (dict(rope_theta=float("inf")), nmm.NMM_ERR_ARG),
+    (dict(round=5), nmm.NMM_ERR_ARG),
+    (dict(ldw=580), nmm.NMM_ERR_ALIGN),
+    (dict(h=ALIGNED + 8), nmm.NMM_ERR_ALIGN),
+    (dict(gamma=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+    (dict(cache=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+    (dict(mm=ALIGNED + 2), nmm.NMM_ERR_ALIGN),
+])
+def test_kv_update_rejects_invalid_arguments(kw, status):
+    k = kv_struct(**kw)
+    assert L.nmm_mla_kv_update(ctypes.byref(k), ALIGNED, 1 << 30, None) == status
+
+
+def test_kv_update_rejects_small_or_missing_workspace():
+    k = kv_struct()
+    need = L.nmm_mla_kv_update_workspace_size(ctypes.byref(k))
+    assert L.nmm_mla_kv_update(ctypes.byref(k), None, 0, None) == nmm.NMM_ERR_WORKSPACE
+    assert L.nmm_mla_kv_update(ctypes.byref(k), ALIGNED, need - 1, None) == nmm.NMM_ERR_WORKSPACE
+    assert L.nmm_mla_kv_update(None, ALIGNED, need, None) == nmm.NMM_ERR_NULL

@@ -230,3 +230,32 @@ def test_head_pair_loads_stay_in_bounds(nope):
     assert max(16 * t + 15 for t in range(tb)) < lat
     # q_nope: 8 values per lane, lanes with tid * 8 < nope
     assert np.all((tid * 16 + 16)[tid * 8 < nope] <= nope * 2)
+
+
+KV_SHAPES = [  # hidden, kv_lora, rope, ldw
+    (7168, 512, 64, 576), (200, 48, 16, 64), (77, 5, 2, 8), (4100, 1000, 88, 1088), (33, 4096, 0, 4096),
+    (1536, 128, 64, 200), (9, 1, 0, 8), (64, 8, 512, 520),
+]
+
+
+@pytest.mark.parametrize("hidden,kv,rope,ldw", KV_SHAPES)
+def test_kv_update_launch_stays_in_bounds(hidden, kv, rope, ldw):
+    """MatMul 2 with its cache-entry epilogue (gemv_kv_kernel): the GEMV part is the plain
+    launch; the epilogue counts every panel of [0, kv + rope) exactly once, keeps its counter in
+    the counter block, and stages kv + rope values, kv gamma values and one word per wave in the
+    launch's LDS."""
+    n = kv + rope
+    ldx = (hidden + 7) // 8 * 8
+    check_launch(1, 1, hidden, n, ldx, ldw, ldy=n)
+    p = nmm.nmm_gemv_plan(1, hidden, n, nmm.NMM_BF16, nmm.NMM_PATH_GEMV)
+    pcols = p["panel_width"] * 8
+    panels_total = p["n_full_panels"] + (1 if p["tail_chunks"] else 0)
+    first, last = 0, (n - 1) // pcols
+    assert first == 0 and last == panels_total - 1     # every panel of the launch counts in once
+    n_tickets = panels_total if max(p["split_k_full"], p["split_k_tail"]) > 1 else 0
+    assert panels_total + 1 <= 16384 and n_tickets < 16384   # the panel counter sits after the tickets
+    rows_max = max(p["rows_full"], p["rows_tail"])
+    lds_floats = max(rows_max * p["m_tile"], min(p["m_tile"], 4) * THREADS * 8, n + kv + WAVES)
+    assert n + kv + WAVES <= lds_floats and lds_floats * 4 <= 64 * 1024   # y values, gamma, per-wave sums
+    assert rope // 2 <= THREADS                         # one RoPE pair per thread
+
