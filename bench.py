@@ -142,6 +142,34 @@ def crossover_sweep(nmm, torch, dev) -> dict:
     return out
 
 
+def matmul2_section(nmm, torch, dev) -> dict:
+    """The paper's MatMul 2 alone, x[1,7168] . (W^DKV | W^KR)^T [7168, 576] bf16: the plain fp32
+    product, the bf16 output, and the product with its cache entry (RMSNorm, RoPE, one bf16 row
+    of a 4097-row latent cache) in one launch; W rotated over copies totalling > 1 GiB."""
+    import numpy as np
+    import synthetic as syn
+    c = syn.kv_update_case()
+    K, n = c.w.shape[0], c.kv_lora + c.rope
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    nbytes = K * 2 + K * n * 2 + n * 4
+    Ws = [up(c.w) for _ in range(max(2, int(1.2e9 // (K * n * 2))))]
+    h, gamma = up(c.h), up(c.gamma)
+    y = torch.empty((1, n), dtype=torch.float32, device=dev)
+    yb = torch.empty((1, n), dtype=torch.bfloat16, device=dev)
+    cache = torch.zeros((c.position + 1, n), dtype=torch.bfloat16, device=dev)
+    ws = nmm.Workspace(dev)
+    nw = len(Ws)
+    t_plain = graph_time_us(torch, lambda r: nmm.nmm_gemv(h, Ws[r % nw], y, workspace=ws))
+    t_bf16 = graph_time_us(torch, lambda r: nmm.nmm_gemv_bf16(h, Ws[r % nw], yb, workspace=ws))
+    t_kv = graph_time_us(torch, lambda r: nmm.nmm_mla_kv_update(
+        h, Ws[r % nw], gamma, y.view(-1), cache, kv_lora=c.kv_lora, rope=c.rope, eps=c.eps, theta=c.theta,
+        position=c.position, workspace=ws))
+    log(f"[bench] MatMul 2 [{K},{n}]: fp32 {t_plain:.2f} us, bf16 out {t_bf16:.2f} us, "
+        f"with RMSNorm + RoPE + cache entry {t_kv:.2f} us")
+    return {"bytes": nbytes, "fp32_us": round(t_plain, 2), "bf16_out_us": round(t_bf16, 2),
+            "with_cache_entry_us": round(t_kv, 2), "fp32_gbps": round(nbytes / t_plain / 1e3, 1)}
+
+
 def cpu_baseline(step, target_s: float, bytes_per_step: int) -> dict:
     import oracle
     threads = oracle.max_threads()
@@ -304,6 +332,19 @@ def main() -> int:
     t_b = timed(alone["attention"], K)
     timed(alone["serial"], W)
     t_serial = timed(alone["serial"], K)
+    # the chain with the cache entry behind its down-projection (RMSNorm, RoPE, one row of a
+    # latent cache), timed right after the chain alone
+    kvc = syn.kv_update_case()
+    kv_cache = torch.zeros((seq + 1, syn.ATTN_DQK), dtype=torch.bfloat16, device=dev)
+    kv_args = dict(gamma=up(kvc.gamma), cache=kv_cache, eps=kvc.eps, theta=kvc.theta, position=seq)
+    chains_kv = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a, kv=kv_args) for c in range(args.copies)]
+    with torch.cuda.stream(cap):
+        chains_kv[0].launch(stream=cap)
+    torch.cuda.synchronize()
+    kv_graphs = [capture(lambda s: chains_kv[s % args.copies].launch(stream=cap), s) for s in range(args.copies)]
+    timed(kv_graphs, W)
+    t_a_kv = timed(kv_graphs, K)
+    log(f"[bench] chain with the cache entry {t_a_kv * 1e3:.1f} us (without: {t_a * 1e3:.1f} us)")
     gain = mean_gain(step_ms, t_serial)
     bound = 1.0 - max(t_a, t_b) / (t_a + t_b)
     log(f"[bench] chain alone {t_a * 1e3:.1f} us, attention alone {t_b * 1e3:.1f} us, serial "
@@ -351,6 +392,8 @@ def main() -> int:
     log(f"[bench] device copy of {half >> 20} MiB: {copy_gbps:.0f} GB/s (read + write)")
     achieved = cb["w_o"] / (wo_us * 1e-6) / 1e9
     chain_gbps = chain_total / (t_a * 1e-3) / 1e9
+
+    matmul2 = matmul2_section(nmm, torch, dev)
 
     crossover = None if args.no_crossover else crossover_sweep(nmm, torch, dev)
 
@@ -400,6 +443,8 @@ def main() -> int:
             "overlap_gain": round(gain, 4),
             "overlap_gain_bound": round(bound, 4),
             "per_matmul_us": {n: round(t, 2) for n, t in per_matmul.items()},
+            "chain_with_cache_entry_us": round(t_a_kv * 1e3, 2),
+            "matmul2": matmul2,
             "per_matmul_gbps": {n: round(cb[n] / t / 1e3, 1) for n, t in per_matmul.items()},
             "hbm_read_probe_gbps": probe,
             "hbm_copy_gbps": round(copy_gbps, 1),

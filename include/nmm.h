@@ -209,6 +209,14 @@ nmm_status nmm_mla_kv_update(const nmm_mla_kv* kv, void* workspace, size_t works
  * launch (one workgroup per head; the environment variable NMM_CHAIN_PAIR=0 keeps two) and
  * events 2 and 3 are both recorded before it.  Either way every output is the fp32 sum of the
  * same products; only the order of the additions differs between the two forms.
+ *
+ * Optionally (kv_cache not NULL) the chain also builds the latent cache entry from the
+ * down-projection's kv_lora | rope columns, computed as nmm_mla_kv_update computes it:
+ *   kv_cache[position, :kv_lora + rope] = bf16([RMSNorm(down[q_lora : q_lora + kv_lora]) |
+ *                                               RoPE(down[q_lora + kv_lora :], position)])
+ * with kv_gamma, kv_eps, rope_theta and round as there (same limits, NMM_ERR_* before any
+ * launch).  One extra workgroup of the W_UQ launch builds it (down is complete by then), so no
+ * step of the chain waits for it; the chain then always runs as separate launches.
  */
 typedef struct {
     int64_t hidden, q_lora, kv_lora, rope, heads, nope, v_head;   /* 7168,1536,512,64,128,128,128 */
@@ -224,6 +232,13 @@ typedef struct {
     void *o_bf16;      /* [heads*v_head]       bf16 */
     void *const *events;
     int n_events;
+    /* optional cache entry behind the down-projection (see above) */
+    const void* kv_gamma;          /* [kv_lora] bf16 RMSNorm weight */
+    float kv_eps, rope_theta;
+    int64_t position;
+    void* kv_cache;                /* bf16 [cache_rows, ld_cache], or NULL for no entry */
+    int64_t ld_cache, cache_rows;
+    nmm_round round;
 } nmm_mla_chain;
 
 nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,

@@ -53,7 +53,10 @@ class nmm_mla_chain(ctypes.Structure):
     _fields_ = [(n, _i64) for n in ("hidden", "q_lora", "kv_lora", "rope", "heads", "nope", "v_head")] + \
                [(n, _p) for n in ("x", "w_down", "w_uq", "w_uk", "w_uv", "w_o", "down_f32", "q_f32",
                                   "lat_f32", "o_f32", "y", "cq_bf16", "qnope_bf16", "lat_bf16",
-                                  "o_bf16", "events")] + [("n_events", ctypes.c_int)]
+                                  "o_bf16", "events")] + [("n_events", ctypes.c_int)] + \
+               [("kv_gamma", _p), ("kv_eps", ctypes.c_float), ("rope_theta", ctypes.c_float),
+                ("position", _i64), ("kv_cache", _p), ("ld_cache", _i64), ("cache_rows", _i64),
+                ("round", ctypes.c_int)]
 
 
 class nmm_mla_kv(ctypes.Structure):
@@ -258,13 +261,23 @@ CHAIN_BUFFERS = ("x", "w_down", "w_uq", "w_uk", "w_uv", "w_o", "down_f32", "q_f3
                  "o_f32", "y", "cq_bf16", "qnope_bf16", "lat_bf16", "o_bf16")
 
 
-def _chain_struct(dims: dict, bufs: dict, events=None):
+def _chain_struct(dims: dict, bufs: dict, events=None, kv: dict | None = None):
+    """``kv`` (optional): the cache entry behind the down-projection, a dict with the tensors
+    ``gamma`` and ``cache`` and the numbers ``eps``, ``theta``, ``position`` and ``round``."""
     c = nmm_mla_chain()
     for k in CHAIN_DIMS:
         setattr(c, k, int(dims[k]))
     for k in CHAIN_BUFFERS:
         t = bufs.get(k)
         setattr(c, k, t.data_ptr() if t is not None else None)
+    if kv is not None:
+        cache = kv["cache"]
+        c.kv_gamma = kv["gamma"].data_ptr()
+        c.kv_eps, c.rope_theta = float(kv["eps"]), float(kv["theta"])
+        c.position = int(kv["position"])
+        c.kv_cache = cache.data_ptr()
+        c.ld_cache, c.cache_rows = _ld(cache), cache.shape[0]
+        c.round = int(kv.get("round", NMM_ROUND_EVEN))
     keep = None
     if events is not None:
         for e in events:
@@ -282,11 +295,12 @@ class PreparedChain:
     (for tight loops where Python overhead would otherwise show).  ``events`` is an optional
     list of event lists, one per slot; ``launch(slot)`` uses slot ``slot``'s events."""
 
-    def __init__(self, dims: dict, bufs: dict, workspace=None, events=None):
+    def __init__(self, dims: dict, bufs: dict, workspace=None, events=None, kv: dict | None = None):
         self._bufs = bufs                       # keep the tensors alive
+        self._kv = kv
         self._slots = []
         for evs in (events or [None]):
-            c, keep = _chain_struct(dims, bufs, evs)
+            c, keep = _chain_struct(dims, bufs, evs, kv)
             self._slots.append((c, keep))
         need = lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(self._slots[0][0]))
         self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
@@ -302,10 +316,12 @@ def nmm_mla_decode_chain_workspace_size(dims: dict) -> int:
     return int(lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(c)))
 
 
-def nmm_mla_decode_chain(dims: dict, bufs: dict, *, workspace=None, stream=None, events=None) -> None:
+def nmm_mla_decode_chain(dims: dict, bufs: dict, *, workspace=None, stream=None, events=None,
+                         kv: dict | None = None) -> None:
     """One decode chain (see nmm.h).  ``bufs`` maps the nmm_mla_chain field names to tensors;
-    ``events`` is an optional list of >= 6 torch.cuda.Event(enable_timing=True)."""
-    c, keep = _chain_struct(dims, bufs, events)
+    ``events`` is an optional list of >= 6 torch.cuda.Event(enable_timing=True); ``kv`` the
+    optional cache entry (see _chain_struct)."""
+    c, keep = _chain_struct(dims, bufs, events, kv)
     need = lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(c))
     wp, wb = _workspace(workspace, need, bufs["x"].device)
     _check(lib().nmm_mla_decode_chain(ctypes.byref(c), wp, wb, _stream(stream)), "nmm_mla_decode_chain")

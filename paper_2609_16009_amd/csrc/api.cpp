@@ -157,17 +157,43 @@ struct KvUpdate {
     size_t ws_bytes = 0;
 };
 
+// The cache entry's own arguments (shared by nmm_mla_kv_update and the chain).
+nmm_status validate_kv_entry(int64_t kv_lora, int64_t rope, float eps, float theta, int64_t position,
+                             int64_t ld_cache, int64_t cache_rows, int round) {
+    constexpr int64_t kLim = int64_t(1) << 31;
+    if (kv_lora <= 0 || rope < 0 || (rope & 1) || kv_lora + rope > kKvMaxWidth || rope > kKvMaxRope)
+        return NMM_ERR_SHAPE;
+    if (ld_cache < kv_lora + rope || cache_rows <= 0 || ld_cache >= kLim) return NMM_ERR_SHAPE;
+    if (position < 0 || position >= cache_rows) return NMM_ERR_SHAPE;
+    if (!std::isfinite(eps) || eps < 0.f || !std::isfinite(theta) || theta <= 0.f) return NMM_ERR_ARG;
+    if (round != NMM_ROUND_EVEN && round != NMM_ROUND_AWAY) return NMM_ERR_ARG;
+    return NMM_OK;
+}
+
+KvEpilogue kv_epilogue(const void* gamma, float eps, float theta, int64_t position, void* cache, int64_t ld_cache,
+                       int64_t c_off, int64_t kv_lora, int64_t rope, int round, unsigned* done) {
+    KvEpilogue e;
+    e.gamma = gamma;
+    e.row = static_cast<uint16_t*>(cache) + position * ld_cache;
+    e.done = done;
+    e.eps = eps;
+    e.theta = theta;
+    e.position = position;
+    e.c_off = c_off;
+    e.kv = static_cast<int>(kv_lora);
+    e.rope = static_cast<int>(rope);
+    e.away = round == NMM_ROUND_AWAY ? 1 : 0;
+    return e;
+}
+
 nmm_status build_kv_update(const nmm_mla_kv& k, KvUpdate* out) {
     constexpr int64_t kLim = int64_t(1) << 31;
-    if (k.hidden <= 0 || k.kv_lora <= 0 || k.rope < 0 || (k.rope & 1) || k.hidden >= kLim ||
-        k.kv_lora + k.rope > kKvMaxWidth || k.rope > kKvMaxRope)
-        return NMM_ERR_SHAPE;
+    if (k.hidden <= 0 || k.hidden >= kLim) return NMM_ERR_SHAPE;
+    nmm_status vst = validate_kv_entry(k.kv_lora, k.rope, k.eps, k.rope_theta, k.position, k.ld_cache, k.cache_rows,
+                                       k.round);
+    if (vst != NMM_OK) return vst;
     const int64_t n = k.kv_lora + k.rope;
-    if (k.ldw < n || k.ld_cache < n || k.cache_rows <= 0 || k.ld_cache >= kLim) return NMM_ERR_SHAPE;
-    if (k.position < 0 || k.position >= k.cache_rows) return NMM_ERR_SHAPE;
-    if (!std::isfinite(k.eps) || k.eps < 0.f || !std::isfinite(k.rope_theta) || k.rope_theta <= 0.f)
-        return NMM_ERR_ARG;
-    if (k.round != NMM_ROUND_EVEN && k.round != NMM_ROUND_AWAY) return NMM_ERR_ARG;
+    if (k.ldw < n) return NMM_ERR_SHAPE;
     KvUpdate u;
     GemvArgs& a = u.args;
     a.M = 1; a.K = k.hidden; a.N = n; a.dt = NMM_BF16;
@@ -284,6 +310,14 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
     }
     st = validate_workspace(workspace, workspace_bytes, ch.ws_total);
     if (st != NMM_OK) return st;
+    if (c.kv_cache) {
+        if (!c.kv_gamma) return NMM_ERR_NULL;
+        st = validate_kv_entry(c.kv_lora, c.rope, c.kv_eps, c.rope_theta, c.position, c.ld_cache, c.cache_rows,
+                               c.round);
+        if (st != NMM_OK) return st;
+        if (reinterpret_cast<uintptr_t>(c.kv_gamma) & 1u || reinterpret_cast<uintptr_t>(c.kv_cache) & 1u)
+            return NMM_ERR_ALIGN;
+    }
     if (c.events) {
         if (c.n_events < 6) return NMM_ERR_ARG;
         for (int i = 0; i < 6; ++i)
@@ -292,7 +326,7 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
     hipStream_t s = static_cast<hipStream_t>(stream);
     // One launch per MatMul by default; NMM_CHAIN_FUSED=1 selects the persistent launch that runs
     // all five MatMuls with per-panel dependencies.
-    const bool fused = want_fused && chain_fusable(ch.step, ch.plan, 5);
+    const bool fused = want_fused && !c.kv_cache && chain_fusable(ch.step, ch.plan, 5);
     if (fused) {
         unsigned* sync = static_cast<unsigned*>(workspace);
         unsigned* tickets[5];
@@ -329,7 +363,15 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
             tickets = static_cast<unsigned*>(workspace) + ch.tick_off[i];
             part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ch.part_off[i]);
         }
-        st = launch_gemv(ch.step[i], ch.plan[i], tickets, part, stream);
+        if (i == 1 && c.kv_cache) {
+            // the cache entry of the down-projection's kv_lora | rope columns, built by one extra
+            // workgroup of the W_UQ launch (down is complete by then)
+            const KvEpilogue e = kv_epilogue(c.kv_gamma, c.kv_eps, c.rope_theta, c.position, c.kv_cache, c.ld_cache,
+                                             c.q_lora, c.kv_lora, c.rope, c.round, nullptr);
+            st = launch_gemv_entry(ch.step[1], ch.plan[1], tickets, part, e, c.down_f32 + c.q_lora, stream);
+        } else {
+            st = launch_gemv(ch.step[i], ch.plan[i], tickets, part, stream);
+        }
         if (st != NMM_OK) return st;
     }
     if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[5]), s) != hipSuccess)
@@ -357,17 +399,8 @@ nmm_status nmm_mla_kv_update(const nmm_mla_kv* kv, void* workspace, size_t works
     if (st != NMM_OK) return st;
     unsigned* counters = static_cast<unsigned*>(workspace);
     float* part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes);
-    KvEpilogue e;
-    e.gamma = k.gamma;
-    e.row = static_cast<uint16_t*>(k.cache) + k.position * k.ld_cache;
-    e.done = counters + u.plan.n_tickets;
-    e.eps = k.eps;
-    e.theta = k.rope_theta;
-    e.position = k.position;
-    e.c_off = 0;
-    e.kv = static_cast<int>(k.kv_lora);
-    e.rope = static_cast<int>(k.rope);
-    e.away = k.round == NMM_ROUND_AWAY ? 1 : 0;
+    const KvEpilogue e = kv_epilogue(k.gamma, k.eps, k.rope_theta, k.position, k.cache, k.ld_cache, 0, k.kv_lora,
+                                     k.rope, k.round, counters + u.plan.n_tickets);
     return launch_gemv_kv(u.args, u.plan, u.plan.split() ? counters : nullptr, u.plan.split() ? part : nullptr, e,
                           stream);
 }

@@ -538,10 +538,10 @@ __device__ __forceinline__ void rope_angle(const KvParams& e, int j, float* sn, 
     sincosf(float(r), sn, cs);
 }
 
-// The entry, built by the workgroup that counts the last panel in: y[c_off ..] and gamma are
-// staged in LDS in one pass (one round trip), then RMSNorm and RoPE (sn, cs: this thread's
-// pair, taken earlier).
-__device__ __forceinline__ void kv_entry(const KParams& p, const KvParams& e, float* lds, float sn, float cs) {
+// The entry from the product src[0 .. kv + rope) (written by this launch or an earlier one; the
+// loads are device-coherent either way): src and gamma are staged in LDS in one pass (one round
+// trip), then RMSNorm and RoPE (sn, cs: this thread's pair, taken earlier).
+__device__ __forceinline__ void kv_entry(const float* src, const KvParams& e, float* lds, float sn, float cs) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int n_all = e.kv + e.rope;
     float* vals = lds;                  // [n_all]
@@ -549,7 +549,7 @@ __device__ __forceinline__ void kv_entry(const KParams& p, const KvParams& e, fl
     float* red = gam + e.kv;            // [kWaves]
     float ss = 0.f;
     for (int i = tid; i < n_all; i += kThreads) {
-        const float v = __hip_atomic_load(p.y + e.c_off + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const float v = __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         vals[i] = v;
         if (i < e.kv) {
             gam[i] = __uint_as_float(uint32_t(e.gamma[i]) << 16);
@@ -608,7 +608,23 @@ __global__ __launch_bounds__(kThreads) void gemv_kv_kernel(const KParams p, cons
         s_last = last;
     }
     __syncthreads();
-    if (s_last) kv_entry(p, e, lds, sn, cs);
+    if (s_last) kv_entry(p.y + e.c_off, e, lds, sn, cs);
+}
+
+// A GEMV launch with one extra workgroup, the last, that builds the cache entry of a product an
+// earlier launch on the stream completed (src).  The decode chain runs the entry of its
+// down-projection this way beside W_UQ, so nothing on the chain waits for it.
+template <int U>
+__global__ __launch_bounds__(kThreads) void gemv_entry_kernel(const KParams p, const KvParams e, const float* src) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    if (blockIdx.x == gridDim.x - 1) {
+        float sn = 0.f, cs = 1.f;
+        if (threadIdx.x < e.rope / 2) rope_angle(e, threadIdx.x, &sn, &cs);
+        kv_entry(src, e, lds, sn, cs);
+        return;
+    }
+    gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -920,10 +936,9 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
     return last_launch_status();
 }
 
-nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
-                          const KvEpilogue& e, void* stream) {
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    const KParams kp = make_params(a, p, tickets, part);
+namespace {
+
+KvParams make_kv_params(const GemvPlan& p, const KvEpilogue& e) {
     KvParams kv{};
     kv.gamma = static_cast<const uint16_t*>(e.gamma);
     kv.row = static_cast<uint16_t*>(e.row);
@@ -938,6 +953,16 @@ nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* ticket
     const int64_t pcols = int64_t(p.cw_full) * 8;
     kv.first_panel = static_cast<int>(e.c_off / pcols);
     kv.n_panels = static_cast<int>((e.c_off + e.kv + e.rope - 1) / pcols) - kv.first_panel + 1;
+    return kv;
+}
+
+}  // namespace
+
+nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
+                          const KvEpilogue& e, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const KParams kp = make_params(a, p, tickets, part);
+    const KvParams kv = make_kv_params(p, e);
     const size_t lds = gemv_kv_lds_bytes(p, e.kv, e.rope);
     const dim3 grid(static_cast<uint32_t>(p.grid)), block(kThreads);
     switch (p.unroll) {
@@ -945,6 +970,22 @@ nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* ticket
         case 8: hipLaunchKernelGGL(gemv_kv_kernel<8>, grid, block, lds, s, kp, kv); break;
         case 4: hipLaunchKernelGGL(gemv_kv_kernel<4>, grid, block, lds, s, kp, kv); break;
         default: hipLaunchKernelGGL(gemv_kv_kernel<2>, grid, block, lds, s, kp, kv); break;
+    }
+    return last_launch_status();
+}
+
+nmm_status launch_gemv_entry(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
+                             const KvEpilogue& e, const float* src, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const KParams kp = make_params(a, p, tickets, part);
+    const KvParams kv = make_kv_params(p, e);
+    const size_t lds = gemv_kv_lds_bytes(p, e.kv, e.rope);
+    const dim3 grid(static_cast<uint32_t>(p.grid + 1)), block(kThreads);
+    switch (p.unroll) {
+        case 16: hipLaunchKernelGGL(gemv_entry_kernel<16>, grid, block, lds, s, kp, kv, src); break;
+        case 8: hipLaunchKernelGGL(gemv_entry_kernel<8>, grid, block, lds, s, kp, kv, src); break;
+        case 4: hipLaunchKernelGGL(gemv_entry_kernel<4>, grid, block, lds, s, kp, kv, src); break;
+        default: hipLaunchKernelGGL(gemv_entry_kernel<2>, grid, block, lds, s, kp, kv, src); break;
     }
     return last_launch_status();
 }

@@ -104,6 +104,10 @@ nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
 // entry of `e` (K > 0).
 nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
                           const KvEpilogue& e, void* stream);
+// The GEMV of a validated M = 1 bf16 plan with one extra workgroup that builds the cache entry
+// of `e` from src[0 .. kv + rope), a product an earlier launch on the stream completed.
+nmm_status launch_gemv_entry(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
+                             const KvEpilogue& e, const float* src, void* stream);
 size_t gemv_kv_lds_bytes(const GemvPlan& p, int kv, int rope);
 
 // The fused decode chain: n (<= 5) M = 1 bf16 GEMVs in one persistent launch.  `sync` points to

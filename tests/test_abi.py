@@ -246,3 +246,54 @@ def test_kv_update_rejects_small_or_missing_workspace():
     assert L.nmm_mla_kv_update(ctypes.byref(k), None, 0, None) == nmm.NMM_ERR_WORKSPACE
     assert L.nmm_mla_kv_update(ctypes.byref(k), ALIGNED, need - 1, None) == nmm.NMM_ERR_WORKSPACE
     assert L.nmm_mla_kv_update(None, ALIGNED, need, None) == nmm.NMM_ERR_NULL
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(kv_gamma=None), nmm.NMM_ERR_NULL),
+    (dict(position=4097), nmm.NMM_ERR_SHAPE),
+    (dict(ld_cache=575), nmm.NMM_ERR_SHAPE),
+    (dict(kv_eps=float("nan")), nmm.NMM_ERR_ARG),
+    (dict(rope_theta=-1.0), nmm.NMM_ERR_ARG),
+    (dict(round=3), nmm.NMM_ERR_ARG),
+    (dict(kv_cache=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+    (dict(kv_gamma=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+])
+def test_chain_rejects_bad_cache_entry(kw, status):
+    dims = dict(hidden=7168, q_lora=1536, kv_lora=512, rope=64, heads=128, nope=128, v_head=128)
+    c, _ = nmm._chain_struct(dims, {})
+    for k in nmm.CHAIN_BUFFERS:
+        setattr(c, k, ALIGNED)
+    vals = dict(kv_gamma=ALIGNED, kv_eps=1e-6, rope_theta=10000.0, position=4096, kv_cache=ALIGNED,
+                ld_cache=576, cache_rows=4097, round=0)
+    vals.update(kw)
+    for k, v in vals.items():
+        setattr(c, k, v)
+    assert L.nmm_mla_decode_chain(ctypes.byref(c), ALIGNED, 1 << 30, None) == status
+
+
+def test_struct_layouts_match_the_header(tmp_path):
+    """The binding's ctypes structures have the C layout of include/nmm.h (compiled with gcc)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    probes = {"nmm_mla_chain": ["x", "events", "n_events", "kv_gamma", "kv_eps", "position", "kv_cache", "round"],
+              "nmm_mla_kv": ["h", "ldw", "gamma", "eps", "rope_theta", "position", "mm", "cache_rows", "round"],
+              "nmm_plan_info": ["path", "grid", "workspace_bytes"]}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "nmm.h"', "int main(void) {"]
+    for st, fields in probes.items():
+        lines.append(f'  printf("{st} sizeof %zu\\n", sizeof({st}));')
+        for f in fields:
+            lines.append(f'  printf("{st} {f} %zu\\n", offsetof({st}, {f}));')
+    lines.append("  return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
+    for st, fields in probes.items():
+        cls = getattr(nmm, st)
+        assert got[(st, "sizeof")] == ctypes.sizeof(cls), st
+        for f in fields:
+            assert got[(st, f)] == getattr(cls, f).offset, (st, f)

@@ -318,3 +318,75 @@ def test_chain_pair_agrees_with_two_launches(monkeypatch):
     assert same > 0.999, same
     check_chain_stepwise(step, one)
     check_chain_stepwise(step, two)
+
+
+def kv_for(step, seed, position, cache_rows, mode=0):
+    d = step.dims
+    rng = np.random.default_rng(seed)
+    gamma = syn.bits_from_f32((1.0 + 0.1 * rng.standard_normal(d["kv_lora"], dtype=np.float32)), syn.BF16)
+    n = d["kv_lora"] + d["rope"]
+    cache = torch.full((cache_rows, n + 8), 0x7FC1, dtype=torch.int16, device="cuda")
+    return dict(gamma=dev16(gamma, syn.BF16), cache=cache.view(torch.bfloat16), eps=syn.KV_EPS,
+                theta=syn.ROPE_THETA, position=position, round=mode), gamma
+
+
+def check_kv_row(step, bufs, kv, gamma):
+    d = step.dims
+    q, kvl, n = d["q_lora"], d["kv_lora"], d["kv_lora"] + d["rope"]
+    mm = bufs["down_f32"].cpu().numpy().astype(np.float64)[q:q + n]
+    row_ref, bits_ref = oracle.kv_entry(mm, gamma, kvl, kv["eps"], kv["theta"], kv["position"], kv["round"])
+    cache = kv["cache"].view(torch.int16).cpu().numpy().view(np.uint16)
+    row = cache[kv["position"]]
+    got = oracle.decode(row[:n], syn.BF16)
+    step_ = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(row_ref), 2.0 ** -126))) - 7)
+    slack = 1e-4 * np.abs(row_ref) + np.concatenate([np.zeros(kvl), 1e-6 * np.repeat(
+        np.abs(mm[kvl::2]) + np.abs(mm[kvl + 1::2]), 2)])
+    assert np.all(np.abs(got - row_ref) <= 0.5 * step_ + slack), "cache entry is not a rounding of the oracle's"
+    assert np.count_nonzero(row[:n] == bits_ref) >= 0.99 * n
+    assert np.all(row[n:] == 0x7FC1)
+    others = np.delete(cache, kv["position"], axis=0)
+    assert np.all(others == 0x7FC1), "another cache row was written"
+
+
+@pytest.mark.parametrize("full", [False, True])
+def test_chain_with_cache_entry(full):
+    step = syn.decode_step() if full else small_step(7)
+    pos = 4096 if full else 37
+    kv, gamma = kv_for(step, 3, pos, pos + 2, mode=nmm.NMM_ROUND_AWAY if not full else nmm.NMM_ROUND_EVEN)
+    bufs = alloc_chain(step)
+    run_chain_kv = lambda b, k: nmm.nmm_mla_decode_chain(step.dims, b, kv=k)
+    run_chain_kv(bufs, kv)
+    ref = alloc_chain(step)
+    run_chain(step, ref)
+    torch.cuda.synchronize()
+    check_chain_stepwise(step, bufs)
+    check_kv_row(step, bufs, kv, gamma)
+    # the entry changes nothing else the chain writes
+    for k in nmm.CHAIN_BUFFERS[6:]:
+        assert torch.equal(bufs[k].view(torch.int32) if bufs[k].dtype == torch.float32 else bufs[k].view(torch.int16),
+                           ref[k].view(torch.int32) if ref[k].dtype == torch.float32 else ref[k].view(torch.int16)), k
+
+
+def test_chain_with_cache_entry_in_graph_replays():
+    # captured once, replayed several times with eager work between replays: the entry's panel
+    # counter must return to zero every time and each replay must write the same row
+    step = small_step(8)
+    kv, gamma = kv_for(step, 4, 5, 9)
+    bufs = alloc_chain(step)
+    s = torch.cuda.Stream()
+    ws = nmm.Workspace()
+    nmm.nmm_mla_decode_chain(step.dims, bufs, kv=kv, workspace=ws)
+    torch.cuda.synchronize()
+    first = kv["cache"].view(torch.int16).clone()
+    with torch.cuda.stream(s):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            nmm.nmm_mla_decode_chain(step.dims, bufs, kv=kv, workspace=ws, stream=s)
+    for _ in range(4):
+        kv["cache"].view(torch.int16).fill_(0x7FC1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(kv["cache"].view(torch.int16), first)
+    check_chain_stepwise(step, bufs)
+    check_kv_row(step, bufs, kv, gamma)
