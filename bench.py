@@ -170,6 +170,45 @@ def matmul2_section(nmm, torch, dev) -> dict:
             "with_cache_entry_us": round(t_kv, 2), "fp32_gbps": round(nbytes / t_plain / 1e3, 1)}
 
 
+def remnant_split(nmm, torch, dev) -> dict:
+    """The paper's remnant split (Condition 4): for M = 16q + r, the first 16q rows on the matrix
+    cores and the r remnant rows on the streaming GEMV at the same time (two streams forked and
+    joined inside one HIP graph), against one matrix-core launch over all M rows.  W_UQ's shape,
+    W rotated over copies totalling > 1 GiB."""
+    import numpy as np
+    import synthetic as syn
+    case = syn.uq_sweep(32)
+    K, N = case.K, case.N
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+    Ws = [up(case.W) for _ in range(14)]
+    x = up(case.x)
+    sa, sb = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    ws_a, ws_b = nmm.Workspace(dev), nmm.Workspace(dev)
+    out = {}
+    for M in (17, 18, 20, 24):
+        q16 = M // 16 * 16
+        y = torch.empty((M, N), dtype=torch.float32, device=dev)
+        t_one = graph_time_us(torch, lambda r: nmm.nmm_gemv(x[:M], Ws[r % len(Ws)], y, path=nmm.NMM_PATH_MFMA,
+                                                            workspace=ws_a))
+
+        def split(r):
+            cur = torch.cuda.current_stream()
+            start = torch.cuda.Event()
+            start.record(cur)
+            sa.wait_event(start)
+            sb.wait_event(start)
+            nmm.nmm_gemv(x[:q16], Ws[r % len(Ws)], y[:q16], path=nmm.NMM_PATH_MFMA, workspace=ws_a, stream=sa)
+            nmm.nmm_gemv(x[q16:M], Ws[r % len(Ws)], y[q16:], path=nmm.NMM_PATH_GEMV, workspace=ws_b, stream=sb)
+            cur.wait_stream(sa)
+            cur.wait_stream(sb)
+        t_split = graph_time_us(torch, split)
+        out[f"M={M}"] = {"mfma_all_rows_us": round(t_one, 2), "split_us": round(t_split, 2),
+                         "split_rows": f"{q16} on MFMA + {M - q16} on GEMV"}
+        log(f"[bench] remnant split M={M}: one MFMA launch {t_one:.2f} us, "
+            f"{q16} rows MFMA + {M - q16} rows GEMV concurrently {t_split:.2f} us")
+    return out
+
+
 def cpu_baseline(step, target_s: float, bytes_per_step: int) -> dict:
     import oracle
     threads = oracle.max_threads()
@@ -396,6 +435,7 @@ def main() -> int:
     matmul2 = matmul2_section(nmm, torch, dev)
 
     crossover = None if args.no_crossover else crossover_sweep(nmm, torch, dev)
+    split = None if args.no_crossover else remnant_split(nmm, torch, dev)
 
     value = (chain_total + attn_total) / (step_ms * 1e-3) / 1e9
     result = {
@@ -454,6 +494,7 @@ def main() -> int:
     }
     if crossover is not None:
         result["detail"]["crossover"] = crossover
+        result["detail"]["remnant_split"] = split
     if not args.no_cpu_baseline:
         log(f"[bench] timing the oracle on the host (~{args.cpu_seconds:.0f}s)")
         result["cpu_baseline"] = cpu_baseline(step, args.cpu_seconds, chain_total + attn_total)

@@ -237,3 +237,23 @@ def test_auto_path_switches_at_crossover():
     for M in (3, 4, 16, 32):
         assert nmm.nmm_gemv_plan(M, 1536, 24576)["path"] == nmm.NMM_PATH_MFMA
     assert nmm.nmm_gemv_plan(16, 128, 512, batch=8)["path"] == nmm.NMM_PATH_GEMV
+
+
+@pytest.mark.parametrize("M", [17, 20])
+def test_remnant_split_on_two_streams(M):
+    # the paper's Condition 4 split: rows [0, 16q) on the matrix cores and the remnant rows on
+    # the streaming GEMV, concurrently on two streams into one y; both parts meet the fp32 bar
+    c = syn.uq_sweep(32)
+    q16 = M // 16 * 16
+    x, W = dev16(c.x[:M], syn.BF16), dev16(c.W, syn.BF16)
+    y = torch.full((M, c.N), float("nan"), dtype=torch.float32, device="cuda")
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    start = torch.cuda.Event()
+    start.record()
+    sa.wait_event(start)
+    sb.wait_event(start)
+    nmm.nmm_gemv(x[:q16], W, y[:q16], path=nmm.NMM_PATH_MFMA, workspace=nmm.Workspace(), stream=sa)
+    nmm.nmm_gemv(x[q16:], W, y[q16:], path=nmm.NMM_PATH_GEMV, workspace=nmm.Workspace(), stream=sb)
+    torch.cuda.synchronize()
+    y_ref, a_ref = oracle.gemv(c.x[:M], c.W, syn.BF16)
+    assert_parity(y, y_ref, a_ref, what=f"remnant split M={M}")
