@@ -170,6 +170,33 @@ def matmul2_section(nmm, torch, dev) -> dict:
             "with_cache_entry_us": round(t_kv, 2), "fp32_gbps": round(nbytes / t_plain / 1e3, 1)}
 
 
+def transposed_weights(nmm, torch, dev) -> dict:
+    """The decode shapes with W stored transposed, Wt[N, K] (a torch Linear weight's layout), on
+    nmm_gemv_nt, beside nmm_gemv on the same product with W [K, N]; M = 1, bf16, W rotated over
+    copies totalling > 1 GiB."""
+    import numpy as np
+    import synthetic as syn
+    out = {}
+    for name, K, N in (("w_o", 16384, 7168), ("down", 7168, 2112), ("w_uq", 1536, 24576), ("matmul2", 7168, 576)):
+        c = syn.gemv_case(900 + K % 97, 1, K, N, syn.BF16, name=name)
+        up = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(dev).view(torch.bfloat16)
+        nw = max(2, int(1.2e9 // (K * N * 2)))
+        W = up(c.W)
+        Ws = [W.clone() for _ in range(nw)]
+        Wts = [W.t().contiguous() for _ in range(nw)]
+        x = up(c.x)
+        y = torch.empty((1, N), dtype=torch.float32, device=dev)
+        ws = nmm.Workspace(dev)
+        t_rm = graph_time_us(torch, lambda r: nmm.nmm_gemv(x, Ws[r % nw], y, workspace=ws))
+        t_nt = graph_time_us(torch, lambda r: nmm.nmm_gemv_nt(x, Wts[r % nw], y, workspace=ws))
+        nbytes = K * 2 + K * N * 2 + N * 4
+        out[name] = {"K": K, "N": N, "row_major_us": round(t_rm, 2), "transposed_us": round(t_nt, 2),
+                     "transposed_gbps": round(nbytes / t_nt / 1e3, 1)}
+        del Ws, Wts
+        log(f"[bench] {name} [{K},{N}] with W as [N,K]: {t_nt:.2f} us (as [K,N]: {t_rm:.2f} us)")
+    return out
+
+
 def remnant_split(nmm, torch, dev) -> dict:
     """The paper's remnant split (Condition 4): for M = 16q + r, the first 16q rows on the matrix
     cores and the r remnant rows on the streaming GEMV at the same time (two streams forked and
@@ -436,6 +463,7 @@ def main() -> int:
 
     crossover = None if args.no_crossover else crossover_sweep(nmm, torch, dev)
     split = None if args.no_crossover else remnant_split(nmm, torch, dev)
+    nt = None if args.no_crossover else transposed_weights(nmm, torch, dev)
 
     value = (chain_total + attn_total) / (step_ms * 1e-3) / 1e9
     result = {
@@ -495,6 +523,7 @@ def main() -> int:
     if crossover is not None:
         result["detail"]["crossover"] = crossover
         result["detail"]["remnant_split"] = split
+        result["detail"]["transposed_weights"] = nt
     if not args.no_cpu_baseline:
         log(f"[bench] timing the oracle on the host (~{args.cpu_seconds:.0f}s)")
         result["cpu_baseline"] = cpu_baseline(step, args.cpu_seconds, chain_total + attn_total)

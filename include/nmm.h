@@ -135,6 +135,28 @@ nmm_status nmm_gemv_bf16(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nmm_gemv_nt -- y[M,N] = x[M,K] . Wt[N,K]^T: the same product with W given transposed, row-major
+ * [N, K] (Wt[n * ldwt + k]), the layout of a torch Linear weight and the one a dense
+ * y = x . Wt^T GEMM reads, so one weight copy serves both (the paper keeps the matrix-unit
+ * path's weight layout in global memory, Section IV-C; its Algorithm 1 multiplies rows by
+ * columns).  Each output is the dot product of two contiguous rows: a wave streams 512 k of up
+ * to 8 Wt rows per step and folds its lanes at the end of the rows.  K is split (partials in
+ * the workspace, combined in slice order in the same launch) only beyond 16384 / mt values,
+ * mt = min(M, 4) rounded up to 1, 2 or 4; M above 4 runs in blocks of 4 rows, each reading Wt
+ * again.
+ *
+ *   x, ldx      as for nmm_gemv (16-byte aligned, ldx >= K, multiple of 8).
+ *   Wt, ldwt    16-byte aligned, ldwt >= K and a multiple of 8; (N-1)*ldwt + roundup(K, 8)
+ *               elements < 2^31 bytes.  Values past K in a row's last 16 bytes are read, masked.
+ *   y, ldy      fp32 output, ldy >= N.
+ *   workspace   >= nmm_gemv_nt_workspace_size(M, K, N, dt) bytes (0 when K is not split).
+ * Errors and empty problems as for nmm_gemv.
+ */
+nmm_status nmm_gemv_nt(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                       const void* x, int64_t ldx, const void* Wt, int64_t ldwt,
+                       float* y, int64_t ldy, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * nmm_mla_kv_update -- DeepSeek-V3 MLA's MatMul 2 for one token and the vector work the paper
  * places behind it (Section IV-A: eq. 1 c^KV = W^DKV h, eq. 2 k^R = RoPE(W^KR h), eq. 3 the two
  * as one product; then RMSNorm, RoPE and caching), in one launch:
@@ -272,6 +294,7 @@ size_t nmm_batched_gemv_workspace_size(int64_t batch, int64_t M, int64_t K, int6
 size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain);
 size_t nmm_latent_attention_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v);
 size_t nmm_mla_kv_update_workspace_size(const nmm_mla_kv* kv);
+size_t nmm_gemv_nt_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt);
 
 /* Zero a workspace on `stream` with a fill kernel (no memset node, so it is safe to capture). */
 nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream);

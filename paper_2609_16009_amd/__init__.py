@@ -73,6 +73,8 @@ EXPORTS = {
     "nmm_gemv_bf16": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
                                      ctypes.c_int, _p, _i64, ctypes.c_int, _p, _sz, _p]),
     "nmm_mla_kv_update": (ctypes.c_int, [ctypes.POINTER(nmm_mla_kv), _p, _sz, _p]),
+    "nmm_gemv_nt": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64, _p, _sz, _p]),
+    "nmm_gemv_nt_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.c_int]),
     "nmm_mla_kv_update_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_kv)]),
     "nmm_mla_decode_chain": (ctypes.c_int, [ctypes.POINTER(nmm_mla_chain), _p, _sz, _p]),
     "nmm_latent_attention": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64,
@@ -193,6 +195,19 @@ def nmm_gemv_bf16(x: torch.Tensor, W: torch.Tensor, y_bf16: torch.Tensor, *, rou
                                _ld(y_bf16), round, y.data_ptr() if y is not None else None,
                                _ld(y) if y is not None else 0, path, wp, wb, _stream(stream)), "nmm_gemv_bf16")
     return y_bf16
+
+
+def nmm_gemv_nt(x: torch.Tensor, Wt: torch.Tensor, y: torch.Tensor, *, K: int | None = None,
+                dt: int | None = None, workspace=None, stream=None) -> torch.Tensor:
+    """y[M,N] = x[M,K] . Wt[N,K]^T for Wt row-major [N, ldwt] (a torch Linear weight's layout)."""
+    code = _dtype_code(x, dt)
+    M, N = x.shape[0], Wt.shape[0]
+    K = Wt.shape[1] if K is None else K
+    need = lib().nmm_gemv_nt_workspace_size(M, K, N, code)
+    wp, wb = _workspace(workspace, need, x.device)
+    _check(lib().nmm_gemv_nt(M, K, N, code, x.data_ptr(), _ld(x), Wt.data_ptr(), _ld(Wt), y.data_ptr(), _ld(y),
+                             wp, wb, _stream(stream)), "nmm_gemv_nt")
+    return y
 
 
 def _kv_struct(h, w, gamma, mm, cache, *, kv_lora: int, rope: int, eps: float, theta: float,

@@ -249,6 +249,33 @@ nmm_status nmm_gemv_bf16(int64_t M, int64_t K, int64_t N, nmm_dtype dt, const vo
     return gemv_common(a, path, workspace, workspace_bytes, stream);
 }
 
+nmm_status nmm_gemv_nt(int64_t M, int64_t K, int64_t N, nmm_dtype dt, const void* x, int64_t ldx,
+                       const void* Wt, int64_t ldwt, float* y, int64_t ldy, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+    GemvArgs a;
+    a.M = M; a.K = K; a.N = N; a.dt = dt;
+    a.x = x; a.ldx = ldx; a.w = Wt; a.ldw = ldwt; a.y = y; a.ldy = ldy;
+    nmm_status st = validate_gemv_nt(a);
+    if (st != NMM_OK) return st;
+    NtPlan p;
+    st = plan_gemv_nt(M, K, N, &p);
+    if (st != NMM_OK) return st;
+    if (M == 0 || N == 0) return NMM_OK;
+    if (K > 0) {
+        st = validate_workspace(workspace, workspace_bytes, p.ws_bytes);
+        if (st != NMM_OK) return st;
+    }
+    unsigned* tickets = static_cast<unsigned*>(workspace);
+    float* part = workspace ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes) : nullptr;
+    return launch_gemv_nt(a, p, p.ks > 1 ? tickets : nullptr, p.ks > 1 ? part : nullptr, stream);
+}
+
+size_t nmm_gemv_nt_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt) {
+    (void)dt;
+    NtPlan p;
+    return plan_gemv_nt(M, K, N, &p) == NMM_OK ? p.ws_bytes : 0;
+}
+
 size_t nmm_gemv_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt, nmm_path path) {
     GemvPlan p;
     return plan_gemv(1, M, K, N, dt, path, &p) == NMM_OK ? p.ws_bytes : 0;

@@ -499,6 +499,250 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// The transposed-weight GEMV: y[m, n] = sum_k x[m, k] * Wt[n, k] for Wt row-major [N, K] (the
+// layout of a torch Linear weight, and the one a dense y = x Wt^T GEMM reads).  Each output is
+// the dot product of two contiguous rows, so one load of a wave covers 512 k of one Wt row
+// (64 lanes x 16 bytes), U loads stay in flight across the wave's rows, and each row is finished
+// by the cross-lane butterfly once its last chunk is in: no cross-wave reduction.  A workgroup
+// owns 4 r consecutive rows (r per wave) of one K-slice; K is split only where x's slice would
+// not fit the LDS staging buffer, and then combined like the GEMV's panels (device-scope
+// partials, one ticket per row block, the last arriver sums the slices in order).
+// ---------------------------------------------------------------------------------------------
+struct NtParams {
+    const uint16_t* x;
+    int64_t ldx;
+    const uint16_t* wt;
+    uint32_t row_bytes;      // ldwt * 2
+    uint32_t w_extent;       // bytes of Wt: (N-1)*ldwt*2 + roundup(K, 8)*2
+    float* y;
+    int64_t ldy;
+    float* part;
+    unsigned* tickets;
+    int M, K, N;
+    int r;                   // rows per wave
+    int slice_k;             // k per K-slice (a multiple of 512)
+    int ks, row_blocks, mblocks;
+};
+
+constexpr int kNtChunk = 512;     // k covered by one wave-load
+constexpr int kNtXPer = kXStageBytes / 16 / kThreads;   // 16-byte x chunks staged per thread
+
+// x[m0 : m0+MT, k0 : k0+span] into LDS as raw 16-bit values, layout [k][m], zero past M and K
+// (span a multiple of 8, span * MT * 2 <= kXStageBytes): the loads, then the LDS stores.
+template <int MT>
+__device__ __forceinline__ void nt_stage_x_issue(i32x4 (&v)[kNtXPer], const NtParams& p, int m0, int k0, int span,
+                                                 int tid) {
+    const int cpr = span / 8;
+    const int mrows = min(MT, p.M - m0);
+    const uint32_t x_extent = uint32_t((int64_t(mrows - 1) * p.ldx + (p.K + 7) / 8 * 8) * 2);
+    const __amdgpu_buffer_rsrc_t xr = make_rsrc(p.x + int64_t(m0) * p.ldx, x_extent);
+#pragma unroll
+    for (int c = 0; c < kNtXPer; ++c) {
+        const int i = tid + c * kThreads;
+        const int m = i / cpr, q = i - m * cpr;
+        const bool ok = i < cpr * MT && m < mrows && k0 + 8 * q < p.K;
+        const uint32_t off = ok ? uint32_t((int64_t(m) * p.ldx + k0 + 8 * q) * 2) : kOutOfRange;
+        v[c] = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+    }
+}
+
+template <int MT>
+__device__ __forceinline__ void nt_stage_x_commit(uint16_t* __restrict__ lds16, const i32x4 (&v)[kNtXPer],
+                                                  const NtParams& p, int k0, int span, int tid) {
+    const int cpr = span / 8;
+#pragma unroll
+    for (int c = 0; c < kNtXPer; ++c) {
+        const int i = tid + c * kThreads;
+        if (i < cpr * MT) {
+            const int m = i / cpr, q = i - m * cpr;
+            const int kb = k0 + 8 * q;
+            i32x4 w = v[c];
+            if (kb + 8 > p.K) {                          // the chunk holding K: zero what lies past it
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const uint32_t u = uint32_t(w[e]);
+                    w[e] = int(((kb + 2 * e < p.K) ? (u & 0xFFFFu) : 0u) | ((kb + 2 * e + 1 < p.K) ? (u & 0xFFFF0000u) : 0u));
+                }
+            }
+            if constexpr (MT == 1) {
+                *reinterpret_cast<i32x4*>(lds16 + 8 * q) = w;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    lds16[(8 * q + e) * MT + m] = static_cast<uint16_t>(uint32_t(w[e >> 1]) >> (16 * (e & 1)));
+            }
+        }
+    }
+}
+
+// One wave's walk over its rows: G groups of R rows; step s is chunk j of every row of group g
+// (s = g * J + j), so x's chunk is read from LDS once for R rows.  D steps are in flight
+// (R * D loads per lane), and the step counter runs on across groups, so the loads of the
+// next group's first chunks issue while the current group finishes.
+template <int DT, int MT, int R, int D>
+__global__ __launch_bounds__(kThreads) void gemv_nt_kernel(const NtParams p) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bid = blockIdx.x;
+    const int sl = bid % p.ks;
+    const int rb = (bid / p.ks) % p.row_blocks;
+    const int mb = bid / (p.ks * p.row_blocks);
+    const int k0 = sl * p.slice_k;
+    const int klen = min(p.slice_k, p.K - k0);
+    const int J = (klen + kNtChunk - 1) / kNtChunk;     // wave-loads per row of the slice
+    const int m0 = mb * MT;
+    const int RW = 4 * p.r;                             // rows per workgroup
+    const int G = p.r / R;                              // row groups per wave
+
+    // ---- x[m0 : m0+MT, k0 : k0 + J*512] as 16-bit values in LDS, layout [k][m], zero past M and K
+    uint16_t* lds16 = reinterpret_cast<uint16_t*>(lds);
+    i32x4 xv[kNtXPer];
+    nt_stage_x_issue<MT>(xv, p, m0, k0, J * kNtChunk, tid);
+
+    const __amdgpu_buffer_rsrc_t wr = make_rsrc(p.wt, p.w_extent);
+    const int row0 = rb * RW + wave * p.r;
+    const int S = G * J;                                // steps of this wave
+    // position of the next step to load (group lg, chunk lj, step ls), advanced without division
+    int lg = 0, lj = 0, ls = 0;
+    auto load_step = [&](i32x4 (&b)[R]) {
+        const int k = k0 + lj * kNtChunk + 8 * lane;
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const int n = row0 + lg * R + i;
+            const uint32_t off = (ls < S && n < p.N && k < p.K) ? uint32_t(n) * p.row_bytes + uint32_t(k) * 2u : kOutOfRange;
+            b[i] = __builtin_amdgcn_raw_buffer_load_b128(wr, off, 0, kLoadNT);
+        }
+        ++ls;
+        if (++lj == J) {
+            lj = 0;
+            ++lg;
+        }
+    };
+    i32x4 buf[D][R];
+#pragma unroll
+    for (int d = 0; d < D; ++d) load_step(buf[d]);
+    nt_stage_x_commit<MT>(lds16, xv, p, k0, J * kNtChunk, tid);
+    __syncthreads();
+
+    const int64_t pbase = ((int64_t(mb) * p.row_blocks + rb) * p.ks + sl) * (int64_t(MT) * RW);
+    const bool ragged_k = (p.K & 7) != 0;
+    float acc[R][MT];
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+        for (int m = 0; m < MT; ++m) acc[i][m] = 0.f;
+    int cg = 0, cj = 0;   // group and chunk of the step being consumed
+    for (int s0 = 0; s0 < S; s0 += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            if (s0 + d < S) {
+                const int kb = cj * kNtChunk + 8 * lane;          // the lane's k within the slice
+                float xr[8][MT];
+                {
+                    const i32x4* xs = reinterpret_cast<const i32x4*>(lds16 + kb * MT);
+#pragma unroll
+                    for (int c = 0; c < MT; ++c) {               // 8 * MT values: MT 16-byte reads
+                        const i32x4 xc = xs[c];
+#pragma unroll
+                        for (int h = 0; h < 8; ++h) {
+                            const int idx = 8 * c + h, e = idx / MT, m = idx - e * MT;
+                            xr[e][m] = widen1<DT>(static_cast<uint16_t>(uint32_t(xc[h >> 1]) >> (16 * (h & 1))));
+                        }
+                    }
+                }
+                const bool mask = ragged_k && k0 + kb + 8 > p.K;   // padding past K must not reach the sums
+#pragma unroll
+                for (int i = 0; i < R; ++i) {
+                    i32x4 v = buf[d][i];
+                    if (mask) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const uint32_t w = uint32_t(v[q]);
+                            const uint32_t lo = (k0 + kb + 2 * q < p.K) ? (w & 0xFFFFu) : 0u;
+                            const uint32_t hi = (k0 + kb + 2 * q + 1 < p.K) ? (w & 0xFFFF0000u) : 0u;
+                            v[q] = int(lo | hi);
+                        }
+                    }
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint32_t w = uint32_t(v[q]);
+                        float lo, hi;
+                        if constexpr (DT == NMM_BF16) {
+                            lo = __uint_as_float(w << 16);
+                            hi = __uint_as_float(w & 0xFFFF0000u);
+                        } else {
+                            const f16x2 h = __builtin_bit_cast(f16x2, w);
+                            lo = static_cast<float>(h[0]);
+                            hi = static_cast<float>(h[1]);
+                        }
+#pragma unroll
+                        for (int m = 0; m < MT; ++m) {
+                            acc[i][m] = __builtin_fmaf(lo, xr[2 * q][m], acc[i][m]);
+                            acc[i][m] = __builtin_fmaf(hi, xr[2 * q + 1][m], acc[i][m]);
+                        }
+                    }
+                }
+                if (cj == J - 1) {                                // the group's rows are complete
+#pragma unroll
+                    for (int i = 0; i < R; ++i) {
+                        const int n = row0 + cg * R + i;
+#pragma unroll
+                        for (int m = 0; m < MT; ++m) {
+                            float v2 = acc[i][m];
+                            v2 = add_ror<1>(v2);
+                            v2 = add_ror<2>(v2);
+                            v2 = add_ror<4>(v2);
+                            v2 = add_ror<8>(v2);
+                            v2 = add_xor16(v2);
+                            v2 = add_xor32(v2);
+                            acc[i][m] = 0.f;
+                            if (lane == 0) {
+                                if (p.ks == 1) {
+                                    if (n < p.N && m0 + m < p.M) p.y[int64_t(m0 + m) * p.ldy + n] = v2;
+                                } else {
+                                    __hip_atomic_store(p.part + pbase + m * RW + wave * p.r + cg * R + i, v2,
+                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                }
+                            }
+                        }
+                    }
+                    cj = 0;
+                    ++cg;
+                } else {
+                    ++cj;
+                }
+            }
+            load_step(buf[d]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    if (p.ks == 1) return;
+    // ---- split K: the row block's ticket; the last slice to arrive sums the slices in order
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) {
+        unsigned* tk = p.tickets + int64_t(mb) * p.row_blocks + rb;
+        const unsigned prev = __hip_atomic_fetch_add(tk, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int last = prev == unsigned(p.ks - 1);
+        if (last) __hip_atomic_store(tk, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = last;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    const int64_t gbase = (int64_t(mb) * p.row_blocks + rb) * p.ks * (int64_t(MT) * RW);
+    for (int o = tid; o < MT * RW; o += kThreads) {
+        const int m = o / RW, rr = o - m * RW;
+        float sum = 0.f;
+        for (int q = 0; q < p.ks; ++q)
+            sum += __hip_atomic_load(p.part + gbase + int64_t(q) * (MT * RW) + o, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
+        const int n = rb * RW + rr;
+        if (n < p.N && m0 + m < p.M) p.y[int64_t(m0 + m) * p.ldy + n] = sum;
+    }
+}
+
+// ---------------------------------------------------------------------------------------------
 // MatMul 2 and the vector work behind it (Section IV-A, eq. 1-3): y = [c^KV | k^R] = h . W, then
 // the cache entry [RMSNorm(c^KV) | RoPE(k^R, t)] in bf16.  The GEMV runs as above, except that
 // y is stored device-coherently; every workgroup that writes the final outputs of a panel
@@ -957,6 +1201,72 @@ KvParams make_kv_params(const GemvPlan& p, const KvEpilogue& e) {
 }
 
 }  // namespace
+
+nmm_status launch_gemv_nt(const GemvArgs& a, const NtPlan& p, unsigned* tickets, float* part, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (a.M == 0 || a.N == 0) return NMM_OK;
+    if (a.K == 0) {
+        const int64_t total = a.M * a.N;
+        const int64_t blocks = std::min<int64_t>(4096, (total + 255) / 256);
+        hipLaunchKernelGGL(zero_output_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(256), 0, s, a.y, a.ldy,
+                           int64_t(0), static_cast<uint16_t*>(nullptr), int64_t(1), int64_t(1), int64_t(0), int64_t(0),
+                           a.M, a.N, int64_t(1));
+        return last_launch_status();
+    }
+    NtParams np{};
+    np.x = static_cast<const uint16_t*>(a.x);
+    np.ldx = a.ldx;
+    np.wt = static_cast<const uint16_t*>(a.w);
+    np.row_bytes = static_cast<uint32_t>(a.ldw * 2);
+    np.w_extent = static_cast<uint32_t>(((a.N - 1) * a.ldw + (a.K + 7) / 8 * 8) * 2);
+    np.y = a.y;
+    np.ldy = a.ldy;
+    np.part = part;
+    np.tickets = tickets;
+    np.M = static_cast<int>(a.M);
+    np.K = static_cast<int>(a.K);
+    np.N = static_cast<int>(a.N);
+    np.r = p.r;
+    np.slice_k = p.slice_k;
+    np.ks = p.ks;
+    np.row_blocks = p.row_blocks;
+    np.mblocks = p.mblocks;
+    const size_t lds = size_t(p.slice_k) * p.mt * 2;
+    const dim3 grid(static_cast<uint32_t>(p.grid)), block(kThreads);
+#define NMM_NT_LAUNCH(DTV, MTV)                                                                                  \
+    do {                                                                                                         \
+        switch (p.rgroup) {                                                                                      \
+            case 8: hipLaunchKernelGGL((gemv_nt_kernel<DTV, MTV, 8, 1>), grid, block, lds, s, np); break;        \
+            case 4: hipLaunchKernelGGL((gemv_nt_kernel<DTV, MTV, 4, 2>), grid, block, lds, s, np); break;        \
+            case 2: hipLaunchKernelGGL((gemv_nt_kernel<DTV, MTV, 2, 4>), grid, block, lds, s, np); break;        \
+            default: hipLaunchKernelGGL((gemv_nt_kernel<DTV, MTV, 1, 8>), grid, block, lds, s, np); break;       \
+        }                                                                                                        \
+    } while (0)
+#define NMM_NT_LAUNCH16(DTV)                                                                                     \
+    do {                                                                                                         \
+        switch (p.rgroup) {                                                                                      \
+            case 8: hipLaunchKernelGGL((gemv_nt_kernel<DTV, 1, 8, 2>), grid, block, lds, s, np); break;          \
+            case 4: hipLaunchKernelGGL((gemv_nt_kernel<DTV, 1, 4, 4>), grid, block, lds, s, np); break;          \
+            case 2: hipLaunchKernelGGL((gemv_nt_kernel<DTV, 1, 2, 8>), grid, block, lds, s, np); break;          \
+            default: hipLaunchKernelGGL((gemv_nt_kernel<DTV, 1, 1, 16>), grid, block, lds, s, np); break;        \
+        }                                                                                                        \
+    } while (0)
+    if (p.depth == 16) {
+        if (a.dt == NMM_BF16) NMM_NT_LAUNCH16(NMM_BF16);
+        else NMM_NT_LAUNCH16(NMM_F16);
+    } else if (a.dt == NMM_BF16) {
+        if (p.mt == 1) NMM_NT_LAUNCH(NMM_BF16, 1);
+        else if (p.mt == 2) NMM_NT_LAUNCH(NMM_BF16, 2);
+        else NMM_NT_LAUNCH(NMM_BF16, 4);
+    } else {
+        if (p.mt == 1) NMM_NT_LAUNCH(NMM_F16, 1);
+        else if (p.mt == 2) NMM_NT_LAUNCH(NMM_F16, 2);
+        else NMM_NT_LAUNCH(NMM_F16, 4);
+    }
+#undef NMM_NT_LAUNCH
+#undef NMM_NT_LAUNCH16
+    return last_launch_status();
+}
 
 nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
                           const KvEpilogue& e, void* stream) {

@@ -87,6 +87,21 @@ struct KvEpilogue {
 constexpr int kKvMaxWidth = 4096;   // kv + rope values the epilogue stages in LDS
 constexpr int kKvMaxRope = 512;     // RoPE width: one pair per thread of a 256-thread workgroup
 
+// The transposed-weight GEMV (Wt row-major [N, K]): 4 r rows per workgroup, r per wave; K split
+// into slices of slice_k (a multiple of 512) only where x's slice exceeds the LDS staging buffer.
+struct NtPlan {
+    int mt = 1, mblocks = 1;
+    int r = 1, row_blocks = 1;
+    int rgroup = 1;        // rows a wave walks together (1, 2, 4 or 8; r is a multiple of it)
+    int depth = 8;         // loads in flight per lane: rgroup x steps (8, or 16 for 1-row tiles)
+    int slice_k = 512, ks = 1;
+    int64_t grid = 0;
+    int64_t n_tickets = 0;
+    size_t ws_bytes = 0;
+};
+nmm_status validate_gemv_nt(const GemvArgs& a);
+nmm_status plan_gemv_nt(int64_t M, int64_t K, int64_t N, NtPlan* p);
+
 // Pure host functions (no HIP calls): argument checks and the partition.
 nmm_status validate_gemv(const GemvArgs& a, int path);
 // unroll > 0 requests that many row-steps in flight (2, 4, 8, or 16 for tiles of <= 2 rows);
@@ -100,6 +115,7 @@ nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
 // plan does not split K).
 nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 nmm_status launch_zero_fill(void* ptr, size_t bytes, void* stream);
+nmm_status launch_gemv_nt(const GemvArgs& a, const NtPlan& p, unsigned* tickets, float* part, void* stream);
 // The GEMV of a validated M = 1 bf16 plan (path GEMV) followed in the same launch by the cache
 // entry of `e` (K > 0).
 nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,

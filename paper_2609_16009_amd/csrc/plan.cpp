@@ -245,4 +245,68 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     return NMM_OK;
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// The transposed-weight GEMV.  x's K-slice is staged in LDS as 16-bit values (at most
+// kXStageBytes), so a slice holds at most 16384 / mt values of k; rows are dealt so that at
+// least one workgroup per CU streams (4 r rows each, r at most 8).
+// ---------------------------------------------------------------------------------------------
+nmm_status validate_gemv_nt(const GemvArgs& a) {
+    if (a.dt != NMM_F16 && a.dt != NMM_BF16) return NMM_ERR_DTYPE;
+    if (a.M < 0 || a.K < 0 || a.N < 0 || a.M >= kLimit || a.K >= kLimit || a.N >= kLimit) return NMM_ERR_SHAPE;
+    if (a.ldx < 0 || a.ldw < 0 || a.ldy < 0 || a.ldx >= kLimit || a.ldw >= kLimit || a.ldy >= kLimit)
+        return NMM_ERR_SHAPE;
+    if (a.M == 0 || a.N == 0) return NMM_OK;
+    if (!a.y) return NMM_ERR_NULL;
+    if (a.ldy < a.N) return NMM_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(a.y) & 3u) return NMM_ERR_ALIGN;
+    if (a.K == 0) return NMM_OK;
+    if (!a.x || !a.w) return NMM_ERR_NULL;
+    if (a.ldx < a.K || a.ldw < a.K) return NMM_ERR_SHAPE;
+    if (!aligned16(a.x) || !aligned16(a.w) || a.ldx % 8 || a.ldw % 8) return NMM_ERR_ALIGN;
+    const int64_t extent = ((a.N - 1) * a.ldw + rup(a.K, 8)) * 2;     // bytes of Wt
+    if (extent >= kLimit) return NMM_ERR_SHAPE;
+    const int64_t x_extent = ((std::min<int64_t>(a.M, 4) - 1) * a.ldx + rup(a.K, 8)) * 2;
+    if (x_extent >= kLimit) return NMM_ERR_SHAPE;
+    return NMM_OK;
+}
+
+nmm_status plan_gemv_nt(int64_t M, int64_t K, int64_t N, NtPlan* p) {
+    NtPlan q;
+    q.mt = M <= 1 ? 1 : M <= 2 ? 2 : 4;
+    q.mblocks = static_cast<int>(std::max<int64_t>(1, cdiv(M, q.mt)));
+    if (M == 0 || N == 0 || K == 0) {
+        *p = q;
+        return NMM_OK;
+    }
+    const int64_t slice_max = kXStageBytes / 2 / q.mt;          // 16384, 8192 or 4096 (16-bit x in LDS)
+    int64_t ks = cdiv(K, slice_max);
+    const int64_t slice = rup(cdiv(K, ks), 512);
+    ks = cdiv(K, slice);
+    q.slice_k = static_cast<int>(slice);
+    q.ks = static_cast<int>(ks);
+    const int64_t target_rb = std::max<int64_t>(1, 256 / (ks * q.mblocks));
+    // at most 8 rows per wave: short rows (small K) then spread over more workgroups, which
+    // measured faster for W_UQ's [24576, 1536] (768 workgroups) than 24 rows per wave
+    int r = static_cast<int>(std::min<int64_t>(8, std::max<int64_t>(1, N / (4 * target_rb))));
+    r = static_cast<int>(std::min<int64_t>(32, std::max<int64_t>(1, env_int("NMM_NT_ROWS", r))));
+    q.rgroup = r >= 8 ? 8 : r >= 4 ? 4 : r >= 2 ? 2 : 1;
+    const int rg = env_int("NMM_NT_GROUP", q.rgroup);
+    if (rg == 1 || rg == 2 || rg == 4 || rg == 8) q.rgroup = rg;
+    q.depth = (q.mt == 1 && env_int("NMM_NT_DEPTH", 8) == 16) ? 16 : 8;
+    q.r = (r + q.rgroup - 1) / q.rgroup * q.rgroup;
+    const int64_t rb = cdiv(N, 4 * q.r);
+    if (rb >= kLimit) return NMM_ERR_SHAPE;
+    q.row_blocks = static_cast<int>(rb);
+    q.grid = int64_t(q.mblocks) * rb * ks;
+    if (q.grid >= kLimit) return NMM_ERR_SHAPE;
+    if (ks > 1) {
+        q.n_tickets = int64_t(q.mblocks) * rb;
+        if (q.n_tickets > kMaxTickets) return NMM_ERR_SHAPE;
+        q.ws_bytes = size_t(kTicketBytes) + size_t(q.grid) * q.mt * 4 * q.r * 4;
+    }
+    *p = q;
+    return NMM_OK;
+}
+
 }  // namespace nmm

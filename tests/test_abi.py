@@ -297,3 +297,38 @@ def test_struct_layouts_match_the_header(tmp_path):
         assert got[(st, "sizeof")] == ctypes.sizeof(cls), st
         for f in fields:
             assert got[(st, f)] == getattr(cls, f).offset, (st, f)
+
+
+def gemv_nt(**kw):
+    a = dict(M=1, K=64, N=64, dt=nmm.NMM_BF16, x=ALIGNED, ldx=64, W=ALIGNED, ldw=64, y=ALIGNED, ldy=64,
+             ws=ALIGNED, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return L.nmm_gemv_nt(a["M"], a["K"], a["N"], a["dt"], a["x"], a["ldx"], a["W"], a["ldw"], a["y"], a["ldy"],
+                         a["ws"], a["wsb"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), nmm.NMM_ERR_NULL),
+    (dict(W=None), nmm.NMM_ERR_NULL),
+    (dict(y=None), nmm.NMM_ERR_NULL),
+    (dict(dt=0), nmm.NMM_ERR_DTYPE),
+    (dict(M=-1), nmm.NMM_ERR_SHAPE),
+    (dict(ldx=56), nmm.NMM_ERR_SHAPE),
+    (dict(ldw=56), nmm.NMM_ERR_SHAPE),              # ldwt < K
+    (dict(ldy=60), nmm.NMM_ERR_SHAPE),
+    (dict(K=60, ldw=60, ldx=64), nmm.NMM_ERR_ALIGN),  # ldwt not a multiple of 8
+    (dict(W=ALIGNED + 8), nmm.NMM_ERR_ALIGN),
+    (dict(y=ALIGNED + 2), nmm.NMM_ERR_ALIGN),
+    (dict(N=40000, K=40000, ldw=40000, ldx=40000, ldy=40000), nmm.NMM_ERR_SHAPE),   # Wt > 2 GiB
+    (dict(K=20000, ldw=20000, ldx=20000, ws=None), nmm.NMM_ERR_WORKSPACE),          # split K needs one
+])
+def test_gemv_nt_rejects_invalid_arguments(kw, status):
+    assert gemv_nt(**kw) == status
+
+
+def test_gemv_nt_workspace_only_when_k_splits():
+    assert L.nmm_gemv_nt_workspace_size(1, 16384, 7168, nmm.NMM_BF16) == 0
+    assert L.nmm_gemv_nt_workspace_size(1, 16385, 7168, nmm.NMM_BF16) > 64 * 1024
+    assert L.nmm_gemv_nt_workspace_size(4, 4096, 100, nmm.NMM_BF16) == 0
+    assert L.nmm_gemv_nt_workspace_size(4, 4097, 100, nmm.NMM_BF16) > 0       # 4096 k per slice at mt = 4
+    assert gemv_nt(M=0, x=None, W=None, y=None) == nmm.NMM_OK

@@ -259,3 +259,63 @@ def test_kv_update_launch_stays_in_bounds(hidden, kv, rope, ldw):
     assert n + kv + WAVES <= lds_floats and lds_floats * 4 <= 64 * 1024   # y values, gamma, per-wave sums
     assert rope // 2 <= THREADS                         # one RoPE pair per thread
 
+
+
+NT_SHAPES = [  # M, K, N, ldx, ldwt
+    (1, 16384, 7168, 16384, 16384), (1, 7168, 2112, 7168, 7168), (1, 1536, 24576, 1536, 1536),
+    (1, 1021, 1031, 1024, 1024), (1, 13, 8, 16, 16), (2, 20000, 40, 20000, 20000), (3, 4099, 520, 4104, 4104),
+    (4, 9000, 4200, 9000, 9000), (5, 777, 300, 784, 784), (16, 1536, 3000, 1536, 1536), (1, 1, 1, 8, 8),
+    (1, 100000, 64, 100000, 100000),
+]
+
+
+@pytest.mark.parametrize("M,K,N,ldx,ldwt", NT_SHAPES)
+def test_gemv_nt_launch_stays_in_bounds(M, K, N, ldx, ldwt):
+    """The transposed-weight GEMV (gemv_nt_kernel): every Wt load inside Wt's extent, x's staged
+    slice (16-bit) inside the 32 KB staging limit and the launch's LDS, every LDS read of x inside it,
+    partial sums and tickets inside the workspace, y writes inside y."""
+    import ctypes
+    L = nmm.lib()
+    mt = 1 if M <= 1 else 2 if M <= 2 else 4
+    mblocks = -(-M // mt)
+    slice_max = 16384 // mt
+    ks = -(-K // slice_max)
+    slice_k = -(-(-(-K // ks)) // 512) * 512
+    ks = -(-K // slice_k)
+    target_rb = max(1, 256 // (ks * mblocks))
+    r = min(8, max(1, N // (4 * target_rb)))
+    rg = 8 if r >= 8 else 4 if r >= 4 else 2 if r >= 2 else 1
+    r = -(-r // rg) * rg
+    R = 4 * r
+    row_blocks = -(-N // R)
+    grid = mblocks * row_blocks * ks
+    ws = L.nmm_gemv_nt_workspace_size(M, K, N, nmm.NMM_BF16)
+    if ks > 1:
+        assert ws == 64 * 1024 + grid * mt * R * 4 and mblocks * row_blocks <= 16384
+    else:
+        assert ws == 0
+    extent = ((N - 1) * ldwt + (K + 7) // 8 * 8) * 2
+    lds_halves = slice_k * mt
+    lane = np.arange(64)
+    part_floats = grid * mt * R
+    for sl in sorted({0, ks - 1}):
+        k0 = sl * slice_k
+        klen = min(slice_k, K - k0)
+        J = -(-klen // 512)
+        assert J * 512 * mt <= 16384 and J * 512 * mt <= lds_halves         # staged x fits
+        for rb in sorted({0, row_blocks - 1}):
+            for wave in range(4):
+                row0 = rb * R + wave * r
+                for i in range(r):
+                    n = row0 + i
+                    for j in range(J):
+                        k = k0 + j * 512 + 8 * lane
+                        issued = (n < N) & (k < K)
+                        off = n * ldwt * 2 + k * 2
+                        assert np.all(off[issued] + 16 <= extent)
+                        kb = j * 512 + 8 * lane
+                        assert np.all((kb + 7) * mt + mt - 1 < lds_halves)   # LDS reads of x
+                    if ks > 1:
+                        for mb in range(mblocks):
+                            pbase = ((mb * row_blocks + rb) * ks + sl) * mt * R
+                            assert pbase + (mt - 1) * R + wave * r + i < part_floats
