@@ -170,6 +170,104 @@ def matmul2_section(nmm, torch, dev) -> dict:
             "with_cache_entry_us": round(t_kv, 2), "fp32_gbps": round(nbytes / t_plain / 1e3, 1)}
 
 
+def mla_step_section(nmm, torch, dev, step, copies, up, args) -> dict:
+    """One MLA single-token decode step in its real dependency order (the paper's overlap): the
+    query path (x . W_DQ -> W_UQ -> [q_nope . W_UK | RoPE(q_pe)]) on stream A beside MatMul 2 and
+    its cache entry on stream B, then attention over the t + 1 cache rows, W_UV and W_O on A.
+    W_DQ and (W_DKV | W_KR) are the column blocks of the down-projection.  Timed as HIP graph
+    replays: one stream, two streams, and each branch alone."""
+    import synthetic as syn
+    d = step.dims
+    H, ql, kvl, rp, nope = d["heads"], d["q_lora"], d["kv_lora"], d["rope"], d["nope"]
+    qk = nope + rp
+    seq = step.kv.shape[0]
+    kvc = syn.kv_update_case()
+    gamma = up(kvc.gamma)
+    caches = []
+    for c in range(args.copies):
+        cache = torch.zeros((seq + 1, kvl + rp), dtype=torch.bfloat16, device=dev)
+        cache[:seq] = copies[c][2]
+        caches.append(cache)
+    f32 = lambda *shape: torch.zeros(shape, dtype=torch.float32, device=dev)
+    b16 = lambda *shape: torch.zeros(shape, dtype=torch.bfloat16, device=dev)
+    b = dict(cq=f32(1, ql), cq_b=b16(1, ql), q=f32(1, H * qk), q_b=b16(1, H * qk), qlat=f32(H, kvl),
+             query=b16(H, kvl + rp), kv=f32(kvl + rp), att=f32(H, kvl), att_b=b16(H, kvl), o=f32(H, d["v_head"]),
+             o_b=b16(H, d["v_head"]), y=f32(1, d["hidden"]))
+    sa, sb = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
+    ws_a, ws_b = nmm.Workspace(dev), nmm.Workspace(dev)
+
+    def q_path(c, st):
+        w = copies[c][0]
+        nmm.nmm_gemv_bf16(w["x"].view(1, -1), w["w_down"].view(d["hidden"], -1)[:, :ql], b["cq_b"], y=b["cq"],
+                          workspace=ws_a, stream=st)
+        nmm.nmm_gemv_bf16(b["cq_b"], w["w_uq"].view(ql, -1), b["q_b"], y=b["q"], workspace=ws_a, stream=st)
+        nmm.nmm_mla_query(b["q"], b["q_b"], w["w_uk"].view(H, nope, kvl), b["qlat"], b["query"], nope=nope, rope=rp,
+                          position=seq, theta=syn.ROPE_THETA, workspace=ws_a, stream=st)
+
+    def kv_path(c, st):
+        w = copies[c][0]
+        nmm.nmm_mla_kv_update(w["x"].view(1, -1), w["w_down"].view(d["hidden"], -1)[:, ql:], gamma, b["kv"],
+                              caches[c], kv_lora=kvl, rope=rp, eps=syn.KV_EPS, theta=syn.ROPE_THETA, position=seq,
+                              workspace=ws_b, stream=st)
+
+    def tail(c, st):
+        w = copies[c][0]
+        nmm.nmm_latent_attention_bf16(b["query"], caches[c], b["att"], b["att_b"], step.scale, d_v=kvl,
+                                      workspace=ws_a, stream=st)
+        nmm.nmm_batched_gemv_bf16(b["att_b"].view(H, 1, kvl), w["w_uv"].view(H, kvl, -1), b["o_b"].view(H, 1, -1),
+                                  y=b["o"].view(H, 1, -1), workspace=ws_a, stream=st)
+        nmm.nmm_gemv(b["o_b"].view(1, -1), w["w_o"].view(H * d["v_head"], -1), b["y"], workspace=ws_a, stream=st)
+
+    def one_stream(c):
+        st = torch.cuda.current_stream()
+        kv_path(c, st)
+        q_path(c, st)
+        tail(c, st)
+
+    def two_streams(c):
+        st = torch.cuda.current_stream()
+        fork = torch.cuda.Event()
+        fork.record(st)
+        sb.wait_event(fork)
+        kv_path(c, sb)
+        q_path(c, st)
+        join = torch.cuda.Event()
+        join.record(sb)
+        st.wait_event(join)
+        tail(c, st)
+
+    # MI355X's form: W_DQ and (W_DKV | W_KR) as one GEMV over the down-projection, the cache entry
+    # on a spare workgroup of W_UQ, then the query: one stream, three launches
+    down = torch.zeros((1, ql + kvl + rp), dtype=torch.float32, device=dev)
+    qpaths = [nmm.PreparedQueryPath(d, dict(x=copies[c][0]["x"], w_down=copies[c][0]["w_down"],
+                                            w_uq=copies[c][0]["w_uq"], w_uk=copies[c][0]["w_uk"], kv_gamma=gamma,
+                                            kv_cache=caches[c], down_f32=down, cq_bf16=b["cq_b"], q_f32=b["q"],
+                                            q_bf16=b["q_b"], qlat_f32=b["qlat"], query=b["query"]),
+                                    eps=syn.KV_EPS, theta=syn.ROPE_THETA, position=seq, workspace=ws_a)
+              for c in range(args.copies)]
+
+    def fused(c):
+        st = torch.cuda.current_stream()
+        qpaths[c].launch(stream=st)
+        tail(c, st)
+
+    nc = args.copies
+    out = {}
+    for name, fn in (("one_stream", one_stream), ("two_streams", two_streams), ("fused_query_path", fused),
+                     ("fused_query_path_only", lambda c: qpaths[c].launch(stream=torch.cuda.current_stream())),
+                     ("query_path", lambda c: q_path(c, torch.cuda.current_stream())),
+                     ("kv_path", lambda c: kv_path(c, torch.cuda.current_stream())),
+                     ("attention_and_output", lambda c: tail(c, torch.cuda.current_stream()))):
+        out[name + "_us"] = round(graph_time_us(torch, lambda r: fn(r % nc), reps=6, iters=max(3, args.steps // 20),
+                                                mean=True), 2)
+    out["overlap_gain"] = round(1.0 - out["two_streams_us"] / out["one_stream_us"], 4)
+    log(f"[bench] MLA step in dependency order: one stream {out['one_stream_us']} us, two streams "
+        f"{out['two_streams_us']} us, fused query path {out['fused_query_path_us']} us (query path "
+        f"{out['query_path_us']}, MatMul 2 + entry {out['kv_path_us']}, fused both {out['fused_query_path_only_us']}, "
+        f"attention + W_UV + W_O {out['attention_and_output_us']})")
+    return out
+
+
 def transposed_weights(nmm, torch, dev) -> dict:
     """The decode shapes with W stored transposed, Wt[N, K] (a torch Linear weight's layout), on
     nmm_gemv_nt, beside nmm_gemv on the same product with W [K, N]; M = 1, bf16, W rotated over
@@ -460,6 +558,7 @@ def main() -> int:
     chain_gbps = chain_total / (t_a * 1e-3) / 1e9
 
     matmul2 = matmul2_section(nmm, torch, dev)
+    mla_step = mla_step_section(nmm, torch, dev, step, copies, up, args)
 
     crossover = None if args.no_crossover else crossover_sweep(nmm, torch, dev)
     split = None if args.no_crossover else remnant_split(nmm, torch, dev)
@@ -513,6 +612,7 @@ def main() -> int:
             "per_matmul_us": {n: round(t, 2) for n, t in per_matmul.items()},
             "chain_with_cache_entry_us": round(t_a_kv * 1e3, 2),
             "matmul2": matmul2,
+            "mla_step_dependency_order": mla_step,
             "per_matmul_gbps": {n: round(cb[n] / t / 1e3, 1) for n, t in per_matmul.items()},
             "hbm_read_probe_gbps": probe,
             "hbm_copy_gbps": round(copy_gbps, 1),

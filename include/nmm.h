@@ -135,6 +135,70 @@ nmm_status nmm_gemv_bf16(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nmm_batched_gemv_bf16 -- nmm_batched_gemv with the sums also rounded once to bf16:
+ * y_bf16[b*stride_yb + m*ldyb + n] (ldyb >= N, 2-byte aligned), ties per `round`; y (fp32, with
+ * ldy and stride_y) may be NULL.  The per-head W_UV of the absorbed MLA step, whose bf16 output
+ * feeds W_O.  Workspace as nmm_batched_gemv_workspace_size.
+ */
+nmm_status nmm_batched_gemv_bf16(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                                 const void* x, int64_t ldx, int64_t stride_x,
+                                 const void* W, int64_t ldw, int64_t stride_w,
+                                 void* y_bf16, int64_t ldyb, int64_t stride_yb, nmm_round round,
+                                 float* y, int64_t ldy, int64_t stride_y, nmm_path path,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * nmm_mla_query -- the absorbed MLA query of one token (the q path's end, Section IV-A's Cube
+ * work that does not depend on MatMul 2), in one launch.  For each head h:
+ *   q_out[h*ldq + c]           = bf16(sum_d q_nope[h,d] * W_UK[h][d, c])      c < kv_lora
+ *   q_out[h*ldq + kv_lora + i] = bf16(RoPE(q[h, nope : nope+rope], position)[i])   i < rope
+ * where q (fp32) and q_bf16 are W_UQ's output [heads, nope + rope] and its bf16 rounding, and
+ * q_nope = q_bf16[h, :nope].  qlat_f32[h*kv_lora + c] receives the fp32 products.  RoPE as in
+ * nmm_mla_kv_update (adjacent pairs, angle position * rope_theta^(-2i/rope)).  q_out is the
+ * query nmm_latent_attention takes (d_qk = kv_lora + rope).
+ *   heads >= 0; nope > 0 with nope and nope + rope multiples of 8; rope even, <= 512;
+ *   ldq >= kv_lora + rope; q 4-byte, q_bf16 and w_uk 16-byte, q_out 2-byte aligned.
+ * Workspace: nmm_mla_query_workspace_size(heads, nope, kv_lora).
+ */
+nmm_status nmm_mla_query(int64_t heads, int64_t nope, int64_t rope, int64_t kv_lora, const float* q,
+                         const void* q_bf16, const void* w_uk, int64_t position, float rope_theta,
+                         float* qlat_f32, void* q_out, int64_t ldq, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/*
+ * nmm_mla_query_path -- everything of one MLA decode step that precedes attention, in three
+ * launches on one stream, MI355X's form of the paper's overlap (Section IV-A): MatMul 2 shares
+ * its input with the query's down-projection, so both run as one GEMV, and the vector work
+ * behind MatMul 2 runs on a spare workgroup of the next launch instead of on separate units.
+ *   down    = x . w_down              [hidden, q_lora + kv_lora + rope]; c_q = bf16(down[:q_lora])
+ *   q       = c_q . w_uq              q_f32 and its bf16 rounding q_bf16 [heads*(nope+rope)]
+ *   kv_cache[position] = bf16([RMSNorm(down[q_lora : +kv_lora]) | RoPE(down[q_lora+kv_lora :])])
+ *                                     (one extra workgroup of the W_UQ launch)
+ *   query   = nmm_mla_query(q, q_bf16, w_uk)   [heads, ldq] bf16, qlat_f32 [heads*kv_lora]
+ * Fields as in nmm_mla_decode_chain, nmm_mla_kv_update and nmm_mla_query (same limits; every
+ * buffer required).  Workspace: nmm_mla_query_path_workspace_size.
+ */
+typedef struct {
+    int64_t hidden, q_lora, kv_lora, rope, heads, nope;
+    const void *x, *w_down, *w_uq, *w_uk, *kv_gamma;
+    float kv_eps, rope_theta;
+    int64_t position;
+    void* kv_cache;
+    int64_t ld_cache, cache_rows;
+    nmm_round round;
+    float* down_f32;   /* [q_lora + kv_lora + rope] */
+    void* cq_bf16;     /* [q_lora] */
+    float* q_f32;      /* [heads*(nope+rope)] */
+    void* q_bf16;      /* [heads*(nope+rope)] */
+    float* qlat_f32;   /* [heads*kv_lora] */
+    void* query;       /* [heads, ldq] bf16 */
+    int64_t ldq;
+} nmm_mla_query_path;
+
+nmm_status nmm_mla_query_path_run(const nmm_mla_query_path* qp, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+
+/*
  * nmm_gemv_nt -- y[M,N] = x[M,K] . Wt[N,K]^T: the same product with W given transposed, row-major
  * [N, K] (Wt[n * ldwt + k]), the layout of a torch Linear weight and the one a dense
  * y = x . Wt^T GEMM reads, so one weight copy serves both (the paper keeps the matrix-unit
@@ -287,6 +351,13 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
                                 float scale, float* out, int64_t ldo,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* nmm_latent_attention, also writing out_bf16[h*ldob + n] = bf16(out[h*ldo + n]) (ties to even;
+ * ldob >= d_v, 2-byte aligned): the operand of the per-head W_UV that follows attention. */
+nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
+                                     const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
+                                     float scale, float* out, int64_t ldo, void* out_bf16, int64_t ldob,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
 /* Workspace sizes in bytes (0 when none is needed; never fails: invalid sizes give 0). */
 size_t nmm_gemv_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt, nmm_path path);
 size_t nmm_batched_gemv_workspace_size(int64_t batch, int64_t M, int64_t K, int64_t N,
@@ -295,6 +366,8 @@ size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain);
 size_t nmm_latent_attention_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v);
 size_t nmm_mla_kv_update_workspace_size(const nmm_mla_kv* kv);
 size_t nmm_gemv_nt_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt);
+size_t nmm_mla_query_workspace_size(int64_t heads, int64_t nope, int64_t kv_lora);
+size_t nmm_mla_query_path_workspace_size(const nmm_mla_query_path* qp);
 
 /* Zero a workspace on `stream` with a fill kernel (no memset node, so it is safe to capture). */
 nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream);

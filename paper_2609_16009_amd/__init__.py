@@ -65,6 +65,14 @@ class nmm_mla_kv(ctypes.Structure):
                 ("mm", _p), ("cache", _p), ("ld_cache", _i64), ("cache_rows", _i64), ("round", ctypes.c_int)]
 
 
+class nmm_mla_query_path(ctypes.Structure):
+    _fields_ = [(n, _i64) for n in ("hidden", "q_lora", "kv_lora", "rope", "heads", "nope")] + \
+               [(n, _p) for n in ("x", "w_down", "w_uq", "w_uk", "kv_gamma")] + \
+               [("kv_eps", ctypes.c_float), ("rope_theta", ctypes.c_float), ("position", _i64), ("kv_cache", _p),
+                ("ld_cache", _i64), ("cache_rows", _i64), ("round", ctypes.c_int)] + \
+               [(n, _p) for n in ("down_f32", "cq_bf16", "q_f32", "q_bf16", "qlat_f32", "query")] + [("ldq", _i64)]
+
+
 EXPORTS = {
     "nmm_gemv": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
                                 ctypes.c_int, _p, _sz, _p]),
@@ -73,6 +81,15 @@ EXPORTS = {
     "nmm_gemv_bf16": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
                                      ctypes.c_int, _p, _i64, ctypes.c_int, _p, _sz, _p]),
     "nmm_mla_kv_update": (ctypes.c_int, [ctypes.POINTER(nmm_mla_kv), _p, _sz, _p]),
+    "nmm_batched_gemv_bf16": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_int, _p, _i64, _i64, _p, _i64, _i64,
+                                             _p, _i64, _i64, ctypes.c_int, _p, _i64, _i64, ctypes.c_int, _p, _sz, _p]),
+    "nmm_mla_query": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _p, _p, _i64, ctypes.c_float, _p, _p, _i64, _p,
+                                     _sz, _p]),
+    "nmm_mla_query_workspace_size": (_sz, [_i64, _i64, _i64]),
+    "nmm_mla_query_path_run": (ctypes.c_int, [ctypes.POINTER(nmm_mla_query_path), _p, _sz, _p]),
+    "nmm_mla_query_path_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_query_path)]),
+    "nmm_latent_attention_bf16": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64, ctypes.c_float, _p, _i64,
+                                                 _p, _i64, _p, _sz, _p]),
     "nmm_gemv_nt": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64, _p, _sz, _p]),
     "nmm_gemv_nt_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.c_int]),
     "nmm_mla_kv_update_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_kv)]),
@@ -195,6 +212,62 @@ def nmm_gemv_bf16(x: torch.Tensor, W: torch.Tensor, y_bf16: torch.Tensor, *, rou
                                _ld(y_bf16), round, y.data_ptr() if y is not None else None,
                                _ld(y) if y is not None else 0, path, wp, wb, _stream(stream)), "nmm_gemv_bf16")
     return y_bf16
+
+
+def nmm_batched_gemv_bf16(x: torch.Tensor, W: torch.Tensor, y_bf16: torch.Tensor, *, y: torch.Tensor | None = None,
+                          N: int | None = None, round: int = NMM_ROUND_EVEN, path: int = NMM_PATH_AUTO,
+                          dt: int | None = None, workspace=None, stream=None) -> torch.Tensor:
+    """y_bf16[b] = bf16(x[b] . W[b]) for 3-D x, W, y_bf16 (strided views allowed); ``y`` fp32 optional."""
+    code = _dtype_code(x, dt)
+    B, M, K = x.shape[0], x.shape[1], W.shape[1]
+    N = W.shape[2] if N is None else N
+    need = lib().nmm_batched_gemv_workspace_size(B, M, K, N, code, path)
+    wp, wb = _workspace(workspace, need, x.device)
+    _check(lib().nmm_batched_gemv_bf16(B, M, K, N, code, x.data_ptr(), _ld(x), x.stride(0), W.data_ptr(), _ld(W),
+                                       W.stride(0), y_bf16.data_ptr(), _ld(y_bf16), y_bf16.stride(0), round,
+                                       y.data_ptr() if y is not None else None, _ld(y) if y is not None else 0,
+                                       y.stride(0) if y is not None else 0, path, wp, wb, _stream(stream)),
+           "nmm_batched_gemv_bf16")
+    return y_bf16
+
+
+def nmm_mla_query(q: torch.Tensor, q_bf16: torch.Tensor, w_uk: torch.Tensor, qlat: torch.Tensor, q_out: torch.Tensor,
+                  *, nope: int, rope: int, position: int, theta: float, workspace=None, stream=None) -> torch.Tensor:
+    """q_out[h] = bf16([q_nope[h] . W_UK[h] | RoPE(q[h, nope:], position)]) for q [heads, nope + rope] fp32,
+    q_bf16 its bf16 rounding, w_uk [heads, nope, kv_lora]; qlat [heads, kv_lora] fp32 receives the products."""
+    heads, kv_lora = w_uk.shape[0], w_uk.shape[2]
+    need = lib().nmm_mla_query_workspace_size(heads, nope, kv_lora)
+    wp, wb = _workspace(workspace, need, q.device)
+    _check(lib().nmm_mla_query(heads, nope, rope, kv_lora, q.data_ptr(), q_bf16.data_ptr(), w_uk.data_ptr(),
+                               int(position), float(theta), qlat.data_ptr(), q_out.data_ptr(), _ld(q_out), wp, wb,
+                               _stream(stream)), "nmm_mla_query")
+    return q_out
+
+
+class PreparedQueryPath:
+    """nmm_mla_query_path_run with its argument struct built once.  ``dims``: hidden, q_lora,
+    kv_lora, rope, heads, nope; ``bufs``: x, w_down, w_uq, w_uk, kv_gamma, kv_cache, down_f32,
+    cq_bf16, q_f32, q_bf16, qlat_f32, query (tensors); ``eps``, ``theta``, ``position``."""
+
+    def __init__(self, dims: dict, bufs: dict, *, eps: float, theta: float, position: int,
+                 round: int = NMM_ROUND_EVEN, workspace=None):
+        self._bufs = bufs
+        c = nmm_mla_query_path()
+        for k in ("hidden", "q_lora", "kv_lora", "rope", "heads", "nope"):
+            setattr(c, k, int(dims[k]))
+        for k in ("x", "w_down", "w_uq", "w_uk", "kv_gamma", "kv_cache", "down_f32", "cq_bf16", "q_f32", "q_bf16",
+                  "qlat_f32", "query"):
+            setattr(c, k, bufs[k].data_ptr())
+        c.kv_eps, c.rope_theta, c.position, c.round = float(eps), float(theta), int(position), int(round)
+        c.ld_cache, c.cache_rows = _ld(bufs["kv_cache"]), bufs["kv_cache"].shape[0]
+        c.ldq = _ld(bufs["query"])
+        self._c = c
+        need = lib().nmm_mla_query_path_workspace_size(ctypes.byref(c))
+        self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
+
+    def launch(self, stream=None) -> None:
+        _check(lib().nmm_mla_query_path_run(ctypes.byref(self._c), self._wp, self._wb, _stream(stream)),
+               "nmm_mla_query_path_run")
 
 
 def nmm_gemv_nt(x: torch.Tensor, Wt: torch.Tensor, y: torch.Tensor, *, K: int | None = None,
@@ -357,6 +430,20 @@ def nmm_latent_attention(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, s
     _check(lib().nmm_latent_attention(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(),
                                       _ld(kv), float(scale), out.data_ptr(), _ld(out), wp, wb,
                                       _stream(stream)), "nmm_latent_attention")
+    return out
+
+
+def nmm_latent_attention_bf16(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, out_bf16: torch.Tensor,
+                              scale: float, *, d_qk: int | None = None, d_v: int = 512, workspace=None,
+                              stream=None) -> torch.Tensor:
+    """nmm_latent_attention, also writing out_bf16 = bf16(out)."""
+    heads, seq = q.shape[0], kv.shape[0]
+    d_qk = q.shape[1] if d_qk is None else d_qk
+    need = lib().nmm_latent_attention_workspace_size(heads, seq, d_qk, d_v)
+    wp, wb = _workspace(workspace, need, q.device)
+    _check(lib().nmm_latent_attention_bf16(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(), _ld(kv),
+                                           float(scale), out.data_ptr(), _ld(out), out_bf16.data_ptr(), _ld(out_bf16),
+                                           wp, wb, _stream(stream)), "nmm_latent_attention_bf16")
     return out
 
 

@@ -276,6 +276,153 @@ size_t nmm_gemv_nt_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt)
     return plan_gemv_nt(M, K, N, &p) == NMM_OK ? p.ws_bytes : 0;
 }
 
+nmm_status nmm_batched_gemv_bf16(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                                 const void* x, int64_t ldx, int64_t stride_x,
+                                 const void* W, int64_t ldw, int64_t stride_w,
+                                 void* y_bf16, int64_t ldyb, int64_t stride_yb, nmm_round round,
+                                 float* y, int64_t ldy, int64_t stride_y, nmm_path path,
+                                 void* workspace, size_t workspace_bytes, void* stream) {
+    if (round != NMM_ROUND_EVEN && round != NMM_ROUND_AWAY) return NMM_ERR_ARG;
+    GemvArgs a;
+    a.batch = batch; a.M = M; a.K = K; a.N = N; a.dt = dt;
+    a.x = x; a.ldx = ldx; a.sx = stride_x;
+    a.w = W; a.ldw = ldw; a.sw = stride_w;
+    a.y = y; a.ldy = y ? ldy : 0; a.sy = y ? stride_y : 0;
+    if (batch > 0 && M > 0 && N > 0 && !y_bf16) return NMM_ERR_NULL;
+    if (ldyb < N || stride_yb < 0) return NMM_ERR_SHAPE;
+    a.ybf = y_bf16; a.ybf_group = std::max<int64_t>(N, 1); a.ybf_keep = a.ybf_group; a.ybf_ldm = ldyb;
+    a.ybf_sb = stride_yb;
+    a.ybf_away = round == NMM_ROUND_AWAY ? 1 : 0;
+    return gemv_common(a, path, workspace, workspace_bytes, stream);
+}
+
+nmm_status nmm_mla_query(int64_t heads, int64_t nope, int64_t rope, int64_t kv_lora, const float* q,
+                         const void* q_bf16, const void* w_uk, int64_t position, float rope_theta,
+                         float* qlat_f32, void* q_out, int64_t ldq, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+    constexpr int64_t kLim = int64_t(1) << 31;
+    if (heads < 0 || nope <= 0 || rope < 0 || (rope & 1) || rope > kKvMaxRope || kv_lora <= 0 || heads >= kLim ||
+        kv_lora >= kLim || nope + rope >= kLim / std::max<int64_t>(heads, 1))
+        return NMM_ERR_SHAPE;
+    if (heads == 0) return NMM_OK;
+    if (!q || !q_bf16 || !w_uk || !qlat_f32 || !q_out) return NMM_ERR_NULL;
+    if (ldq < kv_lora + rope || ldq >= kLim || position < 0 || position >= kLim) return NMM_ERR_SHAPE;
+    if (!std::isfinite(rope_theta) || rope_theta <= 0.f) return NMM_ERR_ARG;
+    if ((reinterpret_cast<uintptr_t>(q) & 3u) || (reinterpret_cast<uintptr_t>(q_out) & 1u)) return NMM_ERR_ALIGN;
+    // lat[h] = q_nope[h] . w_uk[h], q_nope = the first nope values of each head's bf16 query
+    GemvArgs a;
+    a.batch = heads; a.M = 1; a.K = nope; a.N = kv_lora; a.dt = NMM_BF16;
+    a.x = q_bf16; a.ldx = nope; a.sx = nope + rope;
+    a.w = w_uk; a.ldw = kv_lora; a.sw = nope * kv_lora;
+    a.y = qlat_f32; a.ldy = kv_lora; a.sy = kv_lora;
+    a.ybf = q_out; a.ybf_group = kv_lora; a.ybf_keep = kv_lora; a.ybf_ldm = ldq; a.ybf_sb = ldq;
+    nmm_status st = validate_gemv(a, NMM_PATH_GEMV);
+    if (st != NMM_OK) return st;
+    GemvPlan p;
+    st = plan_gemv(heads, 1, nope, kv_lora, NMM_BF16, NMM_PATH_GEMV, &p);
+    if (st != NMM_OK) return st;
+    st = validate_workspace(workspace, workspace_bytes, p.ws_bytes);
+    if (st != NMM_OK) return st;
+    unsigned* tickets = p.split() ? static_cast<unsigned*>(workspace) : nullptr;
+    float* part = p.split() ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes) : nullptr;
+    return launch_gemv_qrope(a, p, tickets, part, q, q_out, ldq, static_cast<int>(heads), static_cast<int>(nope),
+                             static_cast<int>(kv_lora), static_cast<int>(rope), position, rope_theta, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// The three launches of nmm_mla_query_path with their plans.
+struct QueryPath {
+    GemvArgs down, uq, uk;
+    GemvPlan p_down, p_uq, p_uk;
+    size_t ws_bytes = 0;
+};
+
+nmm_status build_query_path(const nmm_mla_query_path& c, QueryPath* out) {
+    constexpr int64_t kLim = int64_t(1) << 31;
+    const int64_t d[] = {c.hidden, c.q_lora, c.kv_lora, c.heads, c.nope};
+    for (int64_t v : d)
+        if (v <= 0 || v >= kLim) return NMM_ERR_SHAPE;
+    if (c.rope < 0 || (c.rope & 1) || c.rope > kKvMaxRope || c.nope + c.rope >= kLim / c.heads) return NMM_ERR_SHAPE;
+    const int64_t n_down = c.q_lora + c.kv_lora + c.rope, qk = c.nope + c.rope;
+    QueryPath q;
+    q.down.K = c.hidden; q.down.N = n_down; q.down.x = c.x; q.down.ldx = c.hidden;
+    q.down.w = c.w_down; q.down.ldw = n_down; q.down.y = c.down_f32; q.down.ldy = n_down;
+    q.down.ybf = c.cq_bf16; q.down.ybf_group = n_down; q.down.ybf_keep = c.q_lora; q.down.ybf_ldm = c.q_lora;
+    q.uq.K = c.q_lora; q.uq.N = c.heads * qk; q.uq.x = c.cq_bf16; q.uq.ldx = c.q_lora;
+    q.uq.w = c.w_uq; q.uq.ldw = c.heads * qk; q.uq.y = c.q_f32; q.uq.ldy = c.heads * qk;
+    q.uq.ybf = c.q_bf16; q.uq.ybf_group = c.heads * qk; q.uq.ybf_keep = c.heads * qk; q.uq.ybf_ldm = c.heads * qk;
+    q.uk.batch = c.heads; q.uk.K = c.nope; q.uk.N = c.kv_lora; q.uk.x = c.q_bf16; q.uk.ldx = c.nope; q.uk.sx = qk;
+    q.uk.w = c.w_uk; q.uk.ldw = c.kv_lora; q.uk.sw = c.nope * c.kv_lora;
+    q.uk.y = c.qlat_f32; q.uk.ldy = c.kv_lora; q.uk.sy = c.kv_lora;
+    q.uk.ybf = c.query; q.uk.ybf_group = c.kv_lora; q.uk.ybf_keep = c.kv_lora; q.uk.ybf_ldm = c.ldq; q.uk.ybf_sb = c.ldq;
+    GemvArgs* a[] = {&q.down, &q.uq, &q.uk};
+    GemvPlan* p[] = {&q.p_down, &q.p_uq, &q.p_uk};
+    for (int i = 0; i < 3; ++i) {
+        a[i]->M = 1;
+        a[i]->dt = NMM_BF16;
+        nmm_status st = plan_gemv(a[i]->batch, 1, a[i]->K, a[i]->N, NMM_BF16, NMM_PATH_GEMV, p[i]);
+        if (st != NMM_OK) return st;
+        q.ws_bytes = std::max(q.ws_bytes, p[i]->ws_bytes);
+    }
+    *out = q;
+    return NMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t nmm_mla_query_path_workspace_size(const nmm_mla_query_path* qp) {
+    if (!qp) return 0;
+    QueryPath q;
+    return build_query_path(*qp, &q) == NMM_OK ? q.ws_bytes : 0;
+}
+
+nmm_status nmm_mla_query_path_run(const nmm_mla_query_path* qp, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+    if (!qp) return NMM_ERR_NULL;
+    const nmm_mla_query_path& c = *qp;
+    if (!c.x || !c.w_down || !c.w_uq || !c.w_uk || !c.kv_gamma || !c.kv_cache || !c.down_f32 || !c.cq_bf16 ||
+        !c.q_f32 || !c.q_bf16 || !c.qlat_f32 || !c.query)
+        return NMM_ERR_NULL;
+    QueryPath q;
+    nmm_status st = build_query_path(c, &q);
+    if (st != NMM_OK) return st;
+    for (const GemvArgs* a : {&q.down, &q.uq, &q.uk}) {
+        st = validate_gemv(*a, NMM_PATH_GEMV);
+        if (st != NMM_OK) return st;
+    }
+    st = validate_kv_entry(c.kv_lora, c.rope, c.kv_eps, c.rope_theta, c.position, c.ld_cache, c.cache_rows, c.round);
+    if (st != NMM_OK) return st;
+    if (c.ldq < c.kv_lora + c.rope || c.ldq >= (int64_t(1) << 31)) return NMM_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(c.kv_gamma) & 1u || reinterpret_cast<uintptr_t>(c.kv_cache) & 1u ||
+        reinterpret_cast<uintptr_t>(c.query) & 1u)
+        return NMM_ERR_ALIGN;
+    st = validate_workspace(workspace, workspace_bytes, q.ws_bytes);
+    if (st != NMM_OK) return st;
+    unsigned* tickets = static_cast<unsigned*>(workspace);
+    float* part = workspace ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes) : nullptr;
+    auto tk = [&](const GemvPlan& p) { return p.split() ? tickets : nullptr; };
+    auto pt = [&](const GemvPlan& p) { return p.split() ? part : nullptr; };
+    st = launch_gemv(q.down, q.p_down, tk(q.p_down), pt(q.p_down), stream);
+    if (st != NMM_OK) return st;
+    const KvEpilogue e = kv_epilogue(c.kv_gamma, c.kv_eps, c.rope_theta, c.position, c.kv_cache, c.ld_cache, c.q_lora,
+                                     c.kv_lora, c.rope, c.round, nullptr);
+    st = launch_gemv_entry(q.uq, q.p_uq, tk(q.p_uq), pt(q.p_uq), e, c.down_f32 + c.q_lora, stream);
+    if (st != NMM_OK) return st;
+    return launch_gemv_qrope(q.uk, q.p_uk, tk(q.p_uk), pt(q.p_uk), c.q_f32, c.query, c.ldq, static_cast<int>(c.heads),
+                             static_cast<int>(c.nope), static_cast<int>(c.kv_lora), static_cast<int>(c.rope),
+                             c.position, c.rope_theta, stream);
+}
+
+size_t nmm_mla_query_workspace_size(int64_t heads, int64_t nope, int64_t kv_lora) {
+    GemvPlan p;
+    return plan_gemv(heads, 1, nope, kv_lora, NMM_BF16, NMM_PATH_GEMV, &p) == NMM_OK ? p.ws_bytes : 0;
+}
+
 size_t nmm_gemv_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt, nmm_path path) {
     GemvPlan p;
     return plan_gemv(1, M, K, N, dt, path, &p) == NMM_OK ? p.ws_bytes : 0;

@@ -29,6 +29,7 @@
 #include <cstdint>
 #include <cstdlib>
 
+#include "bf16_cast.h"
 #include "nmm_internal.h"
 
 namespace nmm {
@@ -52,6 +53,8 @@ struct AttnParams {
     int64_t ldkv;
     float* out;
     int64_t ldo;
+    uint16_t* outb;     // optional bf16 copy of out (nearest, ties to even), outb[h * ldob + n]
+    int64_t ldob;
     float* part_o;      // [n_hb][nsp][64][d_v]
     float* part_ml;     // [n_hb][nsp][64][2]
     int heads, seq, dqk, dv;
@@ -277,8 +280,17 @@ void attention_kernel(const AttnParams p) {
             const float inv = 1.f / l_run;
 #pragma unroll
             for (int t = 0; t < NT; ++t)
-                if (EXACT || t < ntiles)
-                    *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + 16 * t + 4 * g) = o[t] * inv;
+                if (EXACT || t < ntiles) {
+                    const f32x4 r = o[t] * inv;
+                    *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + 16 * t + 4 * g) = r;
+                    if (p.outb) {
+                        uint16_t* ob = p.outb + int64_t(h) * p.ldob + 16 * t + 4 * g;
+                        ob[0] = to_bf16_bits(r[0]);
+                        ob[1] = to_bf16_bits(r[1]);
+                        ob[2] = to_bf16_bits(r[2]);
+                        ob[3] = to_bf16_bits(r[3]);
+                    }
+                }
         }
         return;
     }
@@ -353,6 +365,7 @@ __global__ __launch_bounds__(kAThreads) void attention_merge_kernel(const AttnPa
             if (q0 + u < p.nsp) acc += wgt[(q0 + u) * kMergeHeads + i] * v[u];
     }
     p.out[int64_t(h) * p.ldo + n] = acc;
+    if (p.outb) p.outb[int64_t(h) * p.ldob + n] = to_bf16_bits(acc);
 }
 
 struct AttnPlan {
@@ -416,10 +429,13 @@ size_t nmm_latent_attention_workspace_size(int64_t heads, int64_t seq, int64_t d
     return plan_attention(heads, seq, d_qk, d_v, &a) == NMM_OK ? a.ws_bytes : 0;
 }
 
-nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
-                                const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
-                                float scale, float* out, int64_t ldo, void* workspace,
-                                size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+nmm_status attention_common(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const void* q, int64_t ldq,
+                            const void* kv, int64_t ld_kv, float scale, float* out, int64_t ldo, void* outb,
+                            int64_t ldob, void* workspace, size_t workspace_bytes, void* stream) {
     AttnPlan a;
     nmm_status st = plan_attention(heads, seq, d_qk, d_v, &a);
     if (st != NMM_OK) return st;
@@ -443,6 +459,8 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
     p.ldkv = ld_kv;
     p.out = out;
     p.ldo = ldo;
+    p.outb = static_cast<uint16_t*>(outb);
+    p.ldob = ldob;
     if (a.ws_bytes) {
         p.part_o = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes);
         p.part_ml = p.part_o + size_t(a.n_hb) * a.nsp * kHB * d_v;
@@ -477,6 +495,29 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
         if (hipGetLastError() != hipSuccess) return NMM_ERR_HIP;
     }
     return NMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
+                                const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
+                                float scale, float* out, int64_t ldo, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, nullptr, 0, workspace,
+                            workspace_bytes, stream);
+}
+
+nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
+                                     const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
+                                     float scale, float* out, int64_t ldo, void* out_bf16, int64_t ldob,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+    if (heads > 0 && !out_bf16) return NMM_ERR_NULL;
+    if (ldob < d_v || ldob >= (int64_t(1) << 31)) return NMM_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(out_bf16) & 1u) return NMM_ERR_ALIGN;
+    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, out_bf16, ldob, workspace,
+                            workspace_bytes, stream);
 }
 
 }  // extern "C"

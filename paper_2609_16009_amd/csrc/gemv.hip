@@ -855,6 +855,39 @@ __global__ __launch_bounds__(kThreads) void gemv_kv_kernel(const KParams p, cons
     if (s_last) kv_entry(p.y + e.c_off, e, lds, sn, cs);
 }
 
+// A batched GEMV launch (the per-head q_nope . W_UK of the absorbed query) with one extra
+// workgroup, the last, that rotates each head's rope part of the query, q[h, nope : nope+rope]
+// (fp32, from an earlier launch), and writes it as bf16 at q_out[h, kv : kv + rope].
+struct QropeParams {
+    const float* q;          // [heads, nope + rope] fp32
+    uint16_t* q_out;         // [heads, ldq] bf16
+    int64_t ldq;
+    int heads, nope, kv;
+};
+
+template <int U>
+__global__ __launch_bounds__(kThreads) void gemv_qrope_kernel(const KParams p, const KvParams e, const QropeParams r) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    if (blockIdx.x == gridDim.x - 1) {
+        const int pairs = e.rope / 2;
+        if (pairs == 0) return;
+        const int j = threadIdx.x % pairs, h0 = threadIdx.x / pairs, hstep = kThreads / pairs;
+        if (h0 >= hstep) return;                     // threads past the last whole group of pairs
+        float sn, cs;
+        rope_angle(e, j, &sn, &cs);
+        const int qk = r.nope + e.rope;
+        for (int h = h0; h < r.heads; h += hstep) {
+            const float k0 = r.q[int64_t(h) * qk + r.nope + 2 * j], k1 = r.q[int64_t(h) * qk + r.nope + 2 * j + 1];
+            uint16_t* dst = r.q_out + int64_t(h) * r.ldq + r.kv + 2 * j;
+            dst[0] = to_bf16_bits(k0 * cs - k1 * sn);
+            dst[1] = to_bf16_bits(k0 * sn + k1 * cs);
+        }
+        return;
+    }
+    gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
+}
+
 // A GEMV launch with one extra workgroup, the last, that builds the cache entry of a product an
 // earlier launch on the stream completed (src).  The decode chain runs the entry of its
 // down-projection this way beside W_UQ, so nothing on the chain waits for it.
@@ -1296,6 +1329,34 @@ nmm_status launch_gemv_entry(const GemvArgs& a, const GemvPlan& p, unsigned* tic
         case 8: hipLaunchKernelGGL(gemv_entry_kernel<8>, grid, block, lds, s, kp, kv, src); break;
         case 4: hipLaunchKernelGGL(gemv_entry_kernel<4>, grid, block, lds, s, kp, kv, src); break;
         default: hipLaunchKernelGGL(gemv_entry_kernel<2>, grid, block, lds, s, kp, kv, src); break;
+    }
+    return last_launch_status();
+}
+
+nmm_status launch_gemv_qrope(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, const float* q,
+                             void* q_out, int64_t ldq, int heads, int nope, int kv, int rope, int64_t position,
+                             float theta, void* stream) {
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const KParams kp = make_params(a, p, tickets, part);
+    KvEpilogue e;
+    e.theta = theta;
+    e.position = position;
+    e.rope = rope;
+    const KvParams kv_p = make_kv_params(p, e);
+    QropeParams r{};
+    r.q = q;
+    r.q_out = static_cast<uint16_t*>(q_out);
+    r.ldq = ldq;
+    r.heads = heads;
+    r.nope = nope;
+    r.kv = kv;
+    const size_t lds = gemv_lds_bytes(p);
+    const dim3 grid(static_cast<uint32_t>(p.grid + 1)), block(kThreads);
+    switch (p.unroll) {
+        case 16: hipLaunchKernelGGL(gemv_qrope_kernel<16>, grid, block, lds, s, kp, kv_p, r); break;
+        case 8: hipLaunchKernelGGL(gemv_qrope_kernel<8>, grid, block, lds, s, kp, kv_p, r); break;
+        case 4: hipLaunchKernelGGL(gemv_qrope_kernel<4>, grid, block, lds, s, kp, kv_p, r); break;
+        default: hipLaunchKernelGGL(gemv_qrope_kernel<2>, grid, block, lds, s, kp, kv_p, r); break;
     }
     return last_launch_status();
 }

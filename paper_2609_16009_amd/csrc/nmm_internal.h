@@ -124,6 +124,11 @@ nmm_status launch_gemv_kv(const GemvArgs& a, const GemvPlan& p, unsigned* ticket
 // of `e` from src[0 .. kv + rope), a product an earlier launch on the stream completed.
 nmm_status launch_gemv_entry(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part,
                              const KvEpilogue& e, const float* src, void* stream);
+// A validated M = 1 bf16 batched GEMV plan with one extra workgroup that writes
+// bf16(RoPE(q[h, nope : nope + rope], position)) to q_out[h * ldq + kv ..] for every head.
+nmm_status launch_gemv_qrope(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, const float* q,
+                             void* q_out, int64_t ldq, int heads, int nope, int kv, int rope, int64_t position,
+                             float theta, void* stream);
 size_t gemv_kv_lds_bytes(const GemvPlan& p, int kv, int rope);
 
 // The fused decode chain: n (<= 5) M = 1 bf16 GEMVs in one persistent launch.  `sync` points to

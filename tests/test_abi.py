@@ -279,7 +279,8 @@ def test_struct_layouts_match_the_header(tmp_path):
         pytest.skip("gcc not available")
     probes = {"nmm_mla_chain": ["x", "events", "n_events", "kv_gamma", "kv_eps", "position", "kv_cache", "round"],
               "nmm_mla_kv": ["h", "ldw", "gamma", "eps", "rope_theta", "position", "mm", "cache_rows", "round"],
-              "nmm_plan_info": ["path", "grid", "workspace_bytes"]}
+              "nmm_plan_info": ["path", "grid", "workspace_bytes"],
+              "nmm_mla_query_path": ["x", "kv_gamma", "kv_eps", "position", "round", "down_f32", "query", "ldq"]}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "nmm.h"', "int main(void) {"]
     for st, fields in probes.items():
         lines.append(f'  printf("{st} sizeof %zu\\n", sizeof({st}));')
