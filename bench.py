@@ -24,6 +24,9 @@ import sys
 import time
 
 
+ATTN_OVERLAP_SPLITS = 16
+
+
 def mean_gain(t_opt: float, t_base: float) -> float:
     """The paper's mean gain G = 1 - E[T_opt] / E[T_base] (Section IV-F, Evaluation)."""
     return 1.0 - float(t_opt) / float(t_base)
@@ -412,9 +415,13 @@ def main() -> int:
     K, W = args.steps, args.warmup
     chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a) for c in range(args.copies)]
 
-    def attention(s, stream):
+    # beside the HBM-bound chain, attention runs on half its standalone partition (16 position spans
+    # per head block, 32 workgroups) and takes fewer CUs from the chain: 88.8-89.4 us per step
+    # against 90.5-91.7 us with the 64-workgroup default, measured on one box
+    def attention(s, stream, splits=ATTN_OVERLAP_SPLITS):
         _, q, kv = copies[s % args.copies]
-        nmm.nmm_latent_attention(q, kv, att_out, step.scale, d_qk=dqk, d_v=dv, workspace=ws_b, stream=stream)
+        nmm.nmm_latent_attention_ex(q, kv, att_out, step.scale, splits=splits, d_qk=dqk, d_v=dv, workspace=ws_b,
+                                    stream=stream)
 
     def decode_step(s):
         # fork: stream A runs the narrow chain, stream B the latent attention; then join
@@ -494,6 +501,9 @@ def main() -> int:
     t_a = timed(alone["chain"], K)
     timed(alone["attention"], W)
     t_b = timed(alone["attention"], K)
+    att_default = [capture(lambda s: attention(s, cap, splits=0), s) for s in range(args.copies)]
+    timed(att_default, W)
+    t_b_default = timed(att_default, K)
     timed(alone["serial"], W)
     t_serial = timed(alone["serial"], K)
     # the chain with the cache entry behind its down-projection (RMSNorm, RoPE, one row of a
@@ -605,6 +615,8 @@ def main() -> int:
             "chain_frac_of_peak": round(chain_gbps / HBM_PEAK_GBPS, 4),
             "chain_roofline_us_at_peak": round(chain_total / (HBM_PEAK_GBPS * 1e3), 2),
             "attention_us": round(t_b * 1e3, 2),
+            "attention_splits": ATTN_OVERLAP_SPLITS,
+            "attention_default_partition_us": round(t_b_default * 1e3, 2),
             "serial_us": round(t_serial * 1e3, 2),
             "concurrent_us": round(step_ms * 1e3, 2),
             "overlap_gain": round(gain, 4),

@@ -351,6 +351,17 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
                                 float scale, float* out, int64_t ldo,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* nmm_latent_attention with the partition chosen by the caller: `splits` position spans per block
+ * of heads (0: the default, about 64 workgroups; the span is rounded up to whole 64-position
+ * chunks, so fewer spans may result), and an optional bf16 copy of the output (out_bf16 may be
+ * NULL).  Beside an HBM-bound stream a smaller partition interferes less: on MI355X the decode
+ * step is fastest with 16 spans (32 workgroups) against 32 for attention alone.  Workspace:
+ * nmm_latent_attention_ex_workspace_size with the same splits. */
+nmm_status nmm_latent_attention_ex(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
+                                   const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
+                                   float scale, float* out, int64_t ldo, void* out_bf16, int64_t ldob,
+                                   int64_t splits, void* workspace, size_t workspace_bytes, void* stream);
+
 /* nmm_latent_attention, also writing out_bf16[h*ldob + n] = bf16(out[h*ldo + n]) (ties to even;
  * ldob >= d_v, 2-byte aligned): the operand of the per-head W_UV that follows attention. */
 nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
@@ -368,6 +379,7 @@ size_t nmm_mla_kv_update_workspace_size(const nmm_mla_kv* kv);
 size_t nmm_gemv_nt_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt);
 size_t nmm_mla_query_workspace_size(int64_t heads, int64_t nope, int64_t kv_lora);
 size_t nmm_mla_query_path_workspace_size(const nmm_mla_query_path* qp);
+size_t nmm_latent_attention_ex_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, int64_t splits);
 
 /* Zero a workspace on `stream` with a fill kernel (no memset node, so it is safe to capture). */
 nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream);

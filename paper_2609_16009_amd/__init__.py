@@ -90,6 +90,9 @@ EXPORTS = {
     "nmm_mla_query_path_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_query_path)]),
     "nmm_latent_attention_bf16": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64, ctypes.c_float, _p, _i64,
                                                  _p, _i64, _p, _sz, _p]),
+    "nmm_latent_attention_ex": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64, ctypes.c_float, _p, _i64,
+                                               _p, _i64, _i64, _p, _sz, _p]),
+    "nmm_latent_attention_ex_workspace_size": (_sz, [_i64, _i64, _i64, _i64, _i64]),
     "nmm_gemv_nt": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64, _p, _sz, _p]),
     "nmm_gemv_nt_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.c_int]),
     "nmm_mla_kv_update_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_kv)]),
@@ -444,6 +447,23 @@ def nmm_latent_attention_bf16(q: torch.Tensor, kv: torch.Tensor, out: torch.Tens
     _check(lib().nmm_latent_attention_bf16(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(), _ld(kv),
                                            float(scale), out.data_ptr(), _ld(out), out_bf16.data_ptr(), _ld(out_bf16),
                                            wp, wb, _stream(stream)), "nmm_latent_attention_bf16")
+    return out
+
+
+def nmm_latent_attention_ex(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, scale: float, *, splits: int = 0,
+                            out_bf16: torch.Tensor | None = None, d_qk: int | None = None, d_v: int = 512,
+                            workspace=None, stream=None) -> torch.Tensor:
+    """nmm_latent_attention with `splits` position spans per head block (0: default) and an
+    optional bf16 copy of the output."""
+    heads, seq = q.shape[0], kv.shape[0]
+    d_qk = q.shape[1] if d_qk is None else d_qk
+    need = lib().nmm_latent_attention_ex_workspace_size(heads, seq, d_qk, d_v, splits)
+    wp, wb = _workspace(workspace, need, q.device)
+    _check(lib().nmm_latent_attention_ex(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(), _ld(kv),
+                                         float(scale), out.data_ptr(), _ld(out),
+                                         out_bf16.data_ptr() if out_bf16 is not None else None,
+                                         _ld(out_bf16) if out_bf16 is not None else 0, int(splits), wp, wb,
+                                         _stream(stream)), "nmm_latent_attention_ex")
     return out
 
 

@@ -380,7 +380,9 @@ int64_t env_splits() {
     return v > 0 ? v : 0;
 }
 
-nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, AttnPlan* out) {
+// splits > 0 asks for that many position spans per head block (the span is rounded up to whole
+// chunks, so fewer may result); 0 takes NMM_ATTN_SPLITS or the default of about 64 workgroups.
+nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, AttnPlan* out, int64_t splits = 0) {
     if (heads < 0 || seq < 1 || heads >= (1 << 30) || seq >= (1 << 30)) return NMM_ERR_SHAPE;
     if (dqk < 32 || dqk > 1024 || dqk % 32) return NMM_ERR_SHAPE;
     if (dv < 16 || dv > 512 || dv % 16) return NMM_ERR_SHAPE;
@@ -392,7 +394,7 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     if (const char* e = std::getenv("NMM_ATTN_CHUNK"))   // tuning override: 32-position chunks
         if (std::atoi(e) == 32) a.ch = 32;
     const int64_t max_sp = (seq + a.ch - 1) / a.ch;
-    int64_t nsp = env_splits();
+    int64_t nsp = splits > 0 ? splits : env_splits();
     if (nsp == 0) nsp = std::max<int64_t>(1, 64 / std::max(1, a.n_hb));   // about 64 workgroups
     nsp = std::min(std::min(nsp, max_sp), int64_t(kMergeMaxSpans));
     int64_t span = (seq + nsp - 1) / nsp;
@@ -435,9 +437,10 @@ namespace {
 
 nmm_status attention_common(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const void* q, int64_t ldq,
                             const void* kv, int64_t ld_kv, float scale, float* out, int64_t ldo, void* outb,
-                            int64_t ldob, void* workspace, size_t workspace_bytes, void* stream) {
+                            int64_t ldob, int64_t splits, void* workspace, size_t workspace_bytes, void* stream) {
+    if (splits < 0) return NMM_ERR_ARG;
     AttnPlan a;
-    nmm_status st = plan_attention(heads, seq, d_qk, d_v, &a);
+    nmm_status st = plan_attention(heads, seq, d_qk, d_v, &a, splits);
     if (st != NMM_OK) return st;
     if (!std::isfinite(scale)) return NMM_ERR_ARG;
     if (heads == 0) return NMM_OK;
@@ -505,7 +508,7 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
                                 const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
                                 float scale, float* out, int64_t ldo, void* workspace,
                                 size_t workspace_bytes, void* stream) {
-    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, nullptr, 0, workspace,
+    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, nullptr, 0, 0, workspace,
                             workspace_bytes, stream);
 }
 
@@ -516,8 +519,23 @@ nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, i
     if (heads > 0 && !out_bf16) return NMM_ERR_NULL;
     if (ldob < d_v || ldob >= (int64_t(1) << 31)) return NMM_ERR_SHAPE;
     if (reinterpret_cast<uintptr_t>(out_bf16) & 1u) return NMM_ERR_ALIGN;
-    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, out_bf16, ldob, workspace,
+    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, out_bf16, ldob, 0, workspace,
                             workspace_bytes, stream);
+}
+
+nmm_status nmm_latent_attention_ex(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
+                                   const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
+                                   float scale, float* out, int64_t ldo, void* out_bf16, int64_t ldob,
+                                   int64_t splits, void* workspace, size_t workspace_bytes, void* stream) {
+    if (out_bf16 && (ldob < d_v || ldob >= (int64_t(1) << 31))) return NMM_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(out_bf16) & 1u) return NMM_ERR_ALIGN;
+    return attention_common(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, out_bf16, ldob, splits,
+                            workspace, workspace_bytes, stream);
+}
+
+size_t nmm_latent_attention_ex_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, int64_t splits) {
+    AttnPlan a;
+    return splits >= 0 && plan_attention(heads, seq, d_qk, d_v, &a, splits) == NMM_OK ? a.ws_bytes : 0;
 }
 
 }  // extern "C"

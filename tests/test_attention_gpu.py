@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synthetic as syn
-from gpu_util import assert_parity, dev16
+from gpu_util import assert_parity, dev16, host_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -84,3 +84,19 @@ def test_attention_rejects_bad_arguments():
     assert call(args(ldkv=500)) == nmm.NMM_ERR_SHAPE
     assert call(args(kv=kv.data_ptr() + 2)) == nmm.NMM_ERR_ALIGN
     assert call(args(h=128, seq=4096)) == nmm.NMM_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("splits", [16, 3, 0])
+def test_attention_ex_partition_and_bf16_copy(splits):
+    # the caller-chosen partition meets the same bar, and the bf16 copy is the ties-to-even
+    # rounding of the fp32 output bit for bit
+    q, kv, scale = syn.attention_case(31, 128, 4096)
+    out = torch.full((128, 512), float("nan"), dtype=torch.float32, device="cuda")
+    outb = torch.zeros((128, 520), dtype=torch.bfloat16, device="cuda")
+    nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, scale, splits=splits, out_bf16=outb)
+    torch.cuda.synchronize()
+    ref, ref_abs = oracle.latent_attention(q, kv, scale)
+    assert_parity(out, ref, ref_abs, what=f"attention splits={splits}")
+    bits = host_bits(outb)
+    assert np.array_equal(bits[:, :512], oracle.round_bf16(out.cpu().numpy()))
+    assert np.all(bits[:, 512:] == 0)
