@@ -333,3 +333,101 @@ def test_gemv_nt_workspace_only_when_k_splits():
     assert L.nmm_gemv_nt_workspace_size(4, 4096, 100, nmm.NMM_BF16) == 0
     assert L.nmm_gemv_nt_workspace_size(4, 4097, 100, nmm.NMM_BF16) > 0       # 4096 k per slice at mt = 4
     assert gemv_nt(M=0, x=None, W=None, y=None) == nmm.NMM_OK
+
+
+def mla_query(**kw):
+    a = dict(heads=128, nope=128, rope=64, kv=512, q=ALIGNED, qb=ALIGNED, w=ALIGNED, pos=4096, theta=10000.0,
+             qlat=ALIGNED, out=ALIGNED, ldq=576, ws=ALIGNED, wsb=1 << 30)
+    a.update(kw)
+    return L.nmm_mla_query(a["heads"], a["nope"], a["rope"], a["kv"], a["q"], a["qb"], a["w"], a["pos"], a["theta"],
+                           a["qlat"], a["out"], a["ldq"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), nmm.NMM_ERR_NULL),
+    (dict(qb=None), nmm.NMM_ERR_NULL),
+    (dict(w=None), nmm.NMM_ERR_NULL),
+    (dict(qlat=None), nmm.NMM_ERR_NULL),
+    (dict(out=None), nmm.NMM_ERR_NULL),
+    (dict(rope=63), nmm.NMM_ERR_SHAPE),
+    (dict(rope=514), nmm.NMM_ERR_SHAPE),
+    (dict(nope=0), nmm.NMM_ERR_SHAPE),
+    (dict(ldq=575), nmm.NMM_ERR_SHAPE),
+    (dict(pos=-1), nmm.NMM_ERR_SHAPE),
+    (dict(theta=0.0), nmm.NMM_ERR_ARG),
+    (dict(theta=float("nan")), nmm.NMM_ERR_ARG),
+    (dict(q=ALIGNED + 2), nmm.NMM_ERR_ALIGN),
+    (dict(out=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+    (dict(nope=120, rope=6), nmm.NMM_ERR_ALIGN),      # head stride nope + rope = 126: not a multiple of 8
+    (dict(qb=ALIGNED + 8), nmm.NMM_ERR_ALIGN),
+])
+def test_mla_query_rejects_invalid_arguments(kw, status):
+    assert mla_query(**kw) == status
+
+
+def test_mla_query_empty_and_workspace():
+    assert mla_query(heads=0, q=None, qb=None, w=None, qlat=None, out=None) == nmm.NMM_OK
+    need = L.nmm_mla_query_workspace_size(128, 128, 512)
+    assert need == nmm.nmm_batched_gemv_workspace_size(128, 1, 128, 512)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(yb=None), nmm.NMM_ERR_NULL),
+    (dict(round=7), nmm.NMM_ERR_ARG),
+    (dict(ldyb=60), nmm.NMM_ERR_SHAPE),
+    (dict(syb=-1), nmm.NMM_ERR_SHAPE),
+    (dict(yb=ALIGNED + 1), nmm.NMM_ERR_ALIGN),
+    (dict(sx=68), nmm.NMM_ERR_ALIGN),
+])
+def test_batched_gemv_bf16_rejects_invalid_arguments(kw, status):
+    a = dict(B=4, M=1, K=64, N=64, x=ALIGNED, ldx=64, sx=64, W=ALIGNED, ldw=64, sw=64 * 64, yb=ALIGNED, ldyb=64,
+             syb=64, round=0, y=None, ldy=0, sy=0)
+    a.update(kw)
+    assert L.nmm_batched_gemv_bf16(a["B"], a["M"], a["K"], a["N"], nmm.NMM_BF16, a["x"], a["ldx"], a["sx"], a["W"],
+                                   a["ldw"], a["sw"], a["yb"], a["ldyb"], a["syb"], a["round"], a["y"], a["ldy"],
+                                   a["sy"], nmm.NMM_PATH_AUTO, ALIGNED, 1 << 30, None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(splits=-1), nmm.NMM_ERR_ARG),
+    (dict(ob=ALIGNED + 1, ldob=512), nmm.NMM_ERR_ALIGN),
+    (dict(ob=ALIGNED, ldob=500), nmm.NMM_ERR_SHAPE),
+    (dict(out=None), nmm.NMM_ERR_NULL),
+    (dict(scale=float("inf")), nmm.NMM_ERR_ARG),
+])
+def test_attention_ex_rejects_invalid_arguments(kw, status):
+    a = dict(q=ALIGNED, kv=ALIGNED, out=ALIGNED, ob=None, ldob=0, splits=16, scale=0.07)
+    a.update(kw)
+    assert L.nmm_latent_attention_ex(128, 4096, 576, 512, a["q"], 576, a["kv"], 576, a["scale"], a["out"], 512, a["ob"],
+                                     a["ldob"], a["splits"], ALIGNED, 1 << 30, None) == status
+
+
+def test_attention_ex_workspace_follows_the_partition():
+    w16 = L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 16)
+    w32 = L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 32)
+    assert 0 < w16 < w32 and w32 == nmm.nmm_latent_attention_workspace_size(128, 4096, 576, 512)
+    assert L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 1) == 0     # one span: no merge
+    assert L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, -1) == 0
+
+
+def test_query_path_rejects_invalid_arguments():
+    c = nmm.nmm_mla_query_path()
+    for k, v in dict(hidden=7168, q_lora=1536, kv_lora=512, rope=64, heads=128, nope=128).items():
+        setattr(c, k, v)
+    assert L.nmm_mla_query_path_run(None, ALIGNED, 1 << 30, None) == nmm.NMM_ERR_NULL
+    assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, 1 << 30, None) == nmm.NMM_ERR_NULL
+    for k in ("x", "w_down", "w_uq", "w_uk", "kv_gamma", "kv_cache", "down_f32", "cq_bf16", "q_f32", "q_bf16",
+              "qlat_f32", "query"):
+        setattr(c, k, ALIGNED)
+    c.kv_eps, c.rope_theta, c.position, c.ld_cache, c.cache_rows, c.ldq = 1e-6, 10000.0, 4096, 576, 4097, 576
+    need = L.nmm_mla_query_path_workspace_size(ctypes.byref(c))
+    assert need > 0
+    assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need - 1, None) == nmm.NMM_ERR_WORKSPACE
+    c.position = 4097
+    assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need, None) == nmm.NMM_ERR_SHAPE
+    c.position, c.ldq = 4096, 570
+    assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need, None) == nmm.NMM_ERR_SHAPE
+    c.ldq, c.rope = 576, 65
+    assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need, None) == nmm.NMM_ERR_SHAPE
+    c.rope, c.query = 64, ALIGNED + 1
+    assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need, None) == nmm.NMM_ERR_ALIGN

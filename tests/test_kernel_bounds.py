@@ -319,3 +319,27 @@ def test_gemv_nt_launch_stays_in_bounds(M, K, N, ldx, ldwt):
                         for mb in range(mblocks):
                             pbase = ((mb * row_blocks + rb) * ks + sl) * mt * R
                             assert pbase + (mt - 1) * R + wave * r + i < part_floats
+
+
+@pytest.mark.parametrize("heads,nope,rope,kv,ldq", [(128, 128, 64, 512, 576), (6, 40, 24, 136, 160), (4, 16, 8, 24, 40),
+                                                    (3, 8, 512, 8, 520), (1, 8, 2, 8, 10), (7, 16, 0, 8, 8)])
+def test_qrope_workgroup_covers_each_pair_once(heads, nope, rope, kv, ldq):
+    """The extra workgroup of the query launch (gemv_qrope_kernel): thread t takes pair
+    t % (rope/2) of heads t / (rope/2), t / (rope/2) + 256 / (rope/2), ...; every (head, pair) is
+    written exactly once, reads stay inside q [heads, nope + rope] and writes inside
+    q_out[h * ldq + kv .. kv + rope)."""
+    pairs = rope // 2
+    if pairs == 0:
+        return
+    qk = nope + rope
+    seen = np.zeros((heads, pairs), int)
+    hstep = THREADS // pairs
+    for t in range(THREADS):
+        j, h0 = t % pairs, t // pairs
+        if h0 >= hstep:
+            continue
+        for h in range(h0, heads, hstep):
+            seen[h, j] += 1
+            assert h * qk + nope + 2 * j + 1 < heads * qk
+            assert kv + 2 * j + 1 < ldq and h * ldq + kv + 2 * j + 1 < heads * ldq
+    assert np.all(seen == 1)
