@@ -369,6 +369,42 @@ nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, i
                                      float scale, float* out, int64_t ldo, void* out_bf16, int64_t ldob,
                                      void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * nmm_mla_decode_step -- one decode step: the chain of nmm_mla_decode_chain and an independent
+ * latent attention (the arguments of nmm_latent_attention_ex) on one stream, with the attention
+ * run beside the chain's last MatMul instead of after it.  The paper's decode overlaps the narrow
+ * MatMuls with matrix-unit work that does not depend on them (Condition 1 "Data Independence",
+ * Section III-A; Section IV-A).  Here the overlap is fixed by one launch: W_O's GEMV workgroups and
+ * the attention's workgroups (splits position spans per block of 64 heads) share a grid, the
+ * GEMV's streaming the weight while attention's use the compute units the GEMV leaves free; the
+ * attention's merge follows.  This needs d_qk = 576, d_v = 512 and the chain's W_O in its
+ * single-row bf16 form; other shapes run the attention after W_O (same results).
+ *
+ * Results: every chain output as nmm_mla_decode_chain writes it, and out / out_bf16 as
+ * nmm_latent_attention_ex writes them for the same splits (the same kernels' arithmetic).  The
+ * attention must be independent of the chain: its q, kv, out and out_bf16 may not overlap any
+ * buffer the chain writes (the cache row included), and out / out_bf16 no buffer the chain reads
+ * (NMM_ERR_ARG).  Same limits as the two calls; `events` as in nmm_mla_decode_chain (event 4 is
+ * recorded before the shared launch, event 5 after the merge).  The chain runs as separate
+ * launches (not the persistent form).  Workspace: nmm_mla_decode_step_workspace_size.
+ */
+typedef struct {
+    int64_t heads, seq, d_qk, d_v;   /* DeepSeek-V3: 128 heads, 576, 512 */
+    const void* q;                   /* bf16 [heads, ldq] */
+    int64_t ldq;
+    const void* kv;                  /* bf16 [seq, ld_kv] latent cache */
+    int64_t ld_kv;
+    float scale;
+    float* out;                      /* fp32 [heads, ldo] */
+    int64_t ldo;
+    void* out_bf16;                  /* optional bf16 copy [heads, ldob], or NULL */
+    int64_t ldob;
+    int64_t splits;                  /* position spans per head block (0: the default) */
+} nmm_latent_attn;
+
+nmm_status nmm_mla_decode_step(const nmm_mla_chain* chain, const nmm_latent_attn* attn, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
 /* Workspace sizes in bytes (0 when none is needed; never fails: invalid sizes give 0). */
 size_t nmm_gemv_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt, nmm_path path);
 size_t nmm_batched_gemv_workspace_size(int64_t batch, int64_t M, int64_t K, int64_t N,
@@ -380,6 +416,7 @@ size_t nmm_gemv_nt_workspace_size(int64_t M, int64_t K, int64_t N, nmm_dtype dt)
 size_t nmm_mla_query_workspace_size(int64_t heads, int64_t nope, int64_t kv_lora);
 size_t nmm_mla_query_path_workspace_size(const nmm_mla_query_path* qp);
 size_t nmm_latent_attention_ex_workspace_size(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, int64_t splits);
+size_t nmm_mla_decode_step_workspace_size(const nmm_mla_chain* chain, const nmm_latent_attn* attn);
 
 /* Zero a workspace on `stream` with a fill kernel (no memset node, so it is safe to capture). */
 nmm_status nmm_workspace_init(void* workspace, size_t workspace_bytes, void* stream);

@@ -65,6 +65,13 @@ class nmm_mla_kv(ctypes.Structure):
                 ("mm", _p), ("cache", _p), ("ld_cache", _i64), ("cache_rows", _i64), ("round", ctypes.c_int)]
 
 
+class nmm_latent_attn(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("heads", "seq", "d_qk", "d_v")] + [
+        ("q", ctypes.c_void_p), ("ldq", ctypes.c_int64), ("kv", ctypes.c_void_p), ("ld_kv", ctypes.c_int64),
+        ("scale", ctypes.c_float), ("out", ctypes.c_void_p), ("ldo", ctypes.c_int64), ("out_bf16", ctypes.c_void_p),
+        ("ldob", ctypes.c_int64), ("splits", ctypes.c_int64)]
+
+
 class nmm_mla_query_path(ctypes.Structure):
     _fields_ = [(n, _i64) for n in ("hidden", "q_lora", "kv_lora", "rope", "heads", "nope")] + \
                [(n, _p) for n in ("x", "w_down", "w_uq", "w_uk", "kv_gamma")] + \
@@ -97,6 +104,9 @@ EXPORTS = {
     "nmm_gemv_nt_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.c_int]),
     "nmm_mla_kv_update_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_kv)]),
     "nmm_mla_decode_chain": (ctypes.c_int, [ctypes.POINTER(nmm_mla_chain), _p, _sz, _p]),
+    "nmm_mla_decode_step": (ctypes.c_int, [ctypes.POINTER(nmm_mla_chain), ctypes.POINTER(nmm_latent_attn), _p, _sz,
+                                           _p]),
+    "nmm_mla_decode_step_workspace_size": (_sz, [ctypes.POINTER(nmm_mla_chain), ctypes.POINTER(nmm_latent_attn)]),
     "nmm_latent_attention": (ctypes.c_int, [_i64, _i64, _i64, _i64, _p, _i64, _p, _i64,
                                             ctypes.c_float, _p, _i64, _p, _sz, _p]),
     "nmm_gemv_workspace_size": (_sz, [_i64, _i64, _i64, ctypes.c_int, ctypes.c_int]),
@@ -400,6 +410,60 @@ class PreparedChain:
         c = self._slots[slot][0]
         _check(lib().nmm_mla_decode_chain(ctypes.byref(c), self._wp, self._wb, _stream(stream)),
                "nmm_mla_decode_chain")
+
+
+def _attn_struct(attn: dict) -> nmm_latent_attn:
+    """nmm_latent_attn from {q, kv, out, scale[, out_bf16, splits, d_qk, d_v]} (q [heads, >= d_qk] and
+    kv [seq, >= max(d_qk, d_v)] bf16, out [heads, >= d_v] fp32)."""
+    q, kv, out = attn["q"], attn["kv"], attn["out"]
+    ob = attn.get("out_bf16")
+    a = nmm_latent_attn()
+    a.heads, a.seq = q.shape[0], kv.shape[0]
+    a.d_qk = attn.get("d_qk", q.shape[1])
+    a.d_v = attn.get("d_v", 512)
+    a.q, a.ldq, a.kv, a.ld_kv = q.data_ptr(), _ld(q), kv.data_ptr(), _ld(kv)
+    a.scale = float(attn["scale"])
+    a.out, a.ldo = out.data_ptr(), _ld(out)
+    a.out_bf16, a.ldob = (ob.data_ptr(), _ld(ob)) if ob is not None else (None, 0)
+    a.splits = int(attn.get("splits", 0))
+    return a
+
+
+class PreparedStep:
+    """A decode step (nmm_mla_decode_step: the chain and an independent latent attention, the
+    attention sharing W_O's launch) with its argument structs built once, so that a launch is a
+    single C call.  ``attn`` is {q, kv, out, scale[, out_bf16, splits, d_qk, d_v]}."""
+
+    def __init__(self, dims: dict, bufs: dict, attn: dict, workspace=None, events=None, kv: dict | None = None):
+        self._bufs, self._attn_bufs, self._kv = bufs, attn, kv   # keep the tensors alive
+        self._a = _attn_struct(attn)
+        self._slots = []
+        for evs in (events or [None]):
+            c, keep = _chain_struct(dims, bufs, evs, kv)
+            self._slots.append((c, keep))
+        need = lib().nmm_mla_decode_step_workspace_size(ctypes.byref(self._slots[0][0]), ctypes.byref(self._a))
+        if need == 0:
+            raise ValueError("nmm_mla_decode_step: invalid chain or attention sizes")
+        self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
+
+    def launch(self, slot: int = 0, stream=None) -> None:
+        c = self._slots[slot][0]
+        _check(lib().nmm_mla_decode_step(ctypes.byref(c), ctypes.byref(self._a), self._wp, self._wb, _stream(stream)),
+               "nmm_mla_decode_step")
+
+
+def nmm_mla_decode_step(dims: dict, bufs: dict, attn: dict, *, workspace=None, stream=None, events=None,
+                        kv: dict | None = None) -> None:
+    """One decode step (see nmm.h): the chain of nmm_mla_decode_chain and the attention ``attn``
+    ({q, kv, out, scale[, out_bf16, splits, d_qk, d_v]}), the attention sharing W_O's launch."""
+    PreparedStep(dims, bufs, attn, workspace=workspace, events=None if events is None else [events],
+                 kv=kv).launch(stream=stream)
+
+
+def nmm_mla_decode_step_workspace_size(dims: dict, attn: dict) -> int:
+    c, _ = _chain_struct(dims, {})
+    a = _attn_struct(attn)
+    return int(lib().nmm_mla_decode_step_workspace_size(ctypes.byref(c), ctypes.byref(a)))
 
 
 def nmm_mla_decode_chain_workspace_size(dims: dict) -> int:

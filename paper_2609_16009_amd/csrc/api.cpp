@@ -373,6 +373,68 @@ nmm_status build_query_path(const nmm_mla_query_path& c, QueryPath* out) {
 
 }  // namespace
 
+namespace {
+
+AttnArgs attn_args(const nmm_latent_attn& l) {
+    AttnArgs a;
+    a.heads = l.heads; a.seq = l.seq; a.d_qk = l.d_qk; a.d_v = l.d_v;
+    a.q = l.q; a.ldq = l.ldq; a.kv = l.kv; a.ld_kv = l.ld_kv; a.scale = l.scale;
+    a.out = l.out; a.ldo = l.ldo; a.outb = l.out_bf16; a.ldob = l.ldob; a.splits = l.splits;
+    return a;
+}
+
+struct Span {
+    uintptr_t lo = 0, hi = 0;   // [lo, hi) in bytes; empty when lo == hi
+};
+Span span_of(const void* p, int64_t bytes) {
+    Span s;
+    if (p && bytes > 0) {
+        s.lo = reinterpret_cast<uintptr_t>(p);
+        s.hi = s.lo + static_cast<uintptr_t>(bytes);
+    }
+    return s;
+}
+bool overlaps(const Span& a, const Span& b) { return a.lo < a.hi && b.lo < b.hi && a.lo < b.hi && b.lo < a.hi; }
+
+// The attention of a decode step runs concurrently with the chain, so neither may touch what the
+// other writes.  Called with validated shapes (the chain built, the attention planned).
+nmm_status validate_attention_independent(const nmm_mla_chain& c, const AttnArgs& a) {
+    if (a.heads == 0) return NMM_OK;
+    const int64_t lim = int64_t(1) << 31;
+    if (a.ldq < a.d_qk || a.ldq >= lim || a.ld_kv < std::max(a.d_qk, a.d_v) || a.ld_kv >= lim || a.ldo < a.d_v ||
+        a.ldo >= lim || (a.outb && (a.ldob < a.d_v || a.ldob >= lim)))
+        return NMM_ERR_SHAPE;
+    const int64_t n_down = c.q_lora + c.kv_lora + c.rope, qk = c.nope + c.rope;
+    const Span writes[] = {
+        span_of(c.down_f32, n_down * 4), span_of(c.q_f32, c.heads * qk * 4), span_of(c.lat_f32, c.heads * c.kv_lora * 4),
+        span_of(c.o_f32, c.heads * c.v_head * 4), span_of(c.y, c.hidden * 4), span_of(c.cq_bf16, c.q_lora * 2),
+        span_of(c.qnope_bf16, c.heads * c.nope * 2), span_of(c.lat_bf16, c.heads * c.kv_lora * 2),
+        span_of(c.o_bf16, c.heads * c.v_head * 2),
+        span_of(c.kv_cache ? static_cast<const uint8_t*>(c.kv_cache) + c.position * c.ld_cache * 2 : nullptr,
+                (c.kv_lora + c.rope) * 2)};
+    const Span reads[] = {
+        span_of(c.x, c.hidden * 2), span_of(c.w_down, c.hidden * n_down * 2), span_of(c.w_uq, c.q_lora * c.heads * qk * 2),
+        span_of(c.w_uk, c.heads * c.nope * c.kv_lora * 2), span_of(c.w_uv, c.heads * c.kv_lora * c.v_head * 2),
+        span_of(c.w_o, c.heads * c.v_head * c.hidden * 2),
+        span_of(c.kv_cache ? c.kv_gamma : nullptr, c.kv_lora * 2)};
+    const Span att_in[] = {span_of(a.q, ((a.heads - 1) * a.ldq + a.d_qk) * 2),
+                           span_of(a.kv, ((a.seq - 1) * a.ld_kv + std::max(a.d_qk, a.d_v)) * 2)};
+    const Span att_out[] = {span_of(a.out, ((a.heads - 1) * a.ldo + a.d_v) * 4),
+                            span_of(a.outb, ((a.heads - 1) * a.ldob + a.d_v) * 2)};
+    for (const Span& w : writes) {
+        for (const Span& r : att_in)
+            if (overlaps(w, r)) return NMM_ERR_ARG;
+        for (const Span& o : att_out)
+            if (overlaps(w, o)) return NMM_ERR_ARG;
+    }
+    for (const Span& r : reads)
+        for (const Span& o : att_out)
+            if (overlaps(r, o)) return NMM_ERR_ARG;
+    return NMM_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 size_t nmm_mla_query_path_workspace_size(const nmm_mla_query_path* qp) {
@@ -467,22 +529,34 @@ size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain) {
     return std::max(a.ws_total, b.ws_total);
 }
 
-nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
-                                size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The chain's launches; with `att`, W_O and the attention share one launch (launch_gemv_attention)
+// and the attention's workspace follows the chain's at a 256-byte boundary.
+nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* workspace, size_t workspace_bytes,
+                     void* stream) {
     if (!chain) return NMM_ERR_NULL;
     const nmm_mla_chain& c = *chain;
     if (!c.x || !c.w_down || !c.w_uq || !c.w_uk || !c.w_uv || !c.w_o || !c.down_f32 || !c.q_f32 ||
         !c.lat_f32 || !c.o_f32 || !c.y || !c.cq_bf16 || !c.qnope_bf16 || !c.lat_bf16 || !c.o_bf16)
         return NMM_ERR_NULL;
     Chain ch;
-    const bool want_fused = chain_fused_requested();
+    const bool want_fused = !att && chain_fused_requested();
     nmm_status st = build_chain(c, &ch, want_fused ? chain_unroll() : 0);
     if (st != NMM_OK) return st;
     for (int i = 0; i < 5; ++i) {
         st = validate_gemv(ch.step[i], NMM_PATH_GEMV);
         if (st != NMM_OK) return st;
     }
-    st = validate_workspace(workspace, workspace_bytes, ch.ws_total);
+    size_t att_ws = 0;
+    if (att) {
+        st = attention_workspace_bytes(*att, &att_ws);
+        if (st != NMM_OK) return st;
+    }
+    const size_t att_off = rup256(ch.ws_total);
+    st = validate_workspace(workspace, workspace_bytes, att ? att_off + att_ws : ch.ws_total);
     if (st != NMM_OK) return st;
     if (c.kv_cache) {
         if (!c.kv_gamma) return NMM_ERR_NULL;
@@ -491,6 +565,12 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
         if (st != NMM_OK) return st;
         if (reinterpret_cast<uintptr_t>(c.kv_gamma) & 1u || reinterpret_cast<uintptr_t>(c.kv_cache) & 1u)
             return NMM_ERR_ALIGN;
+    }
+    if (att) {
+        st = validate_attention_args(*att, att_ws ? static_cast<uint8_t*>(workspace) + att_off : nullptr, att_ws);
+        if (st != NMM_OK) return st;
+        st = validate_attention_independent(c, *att);
+        if (st != NMM_OK) return st;
     }
     if (c.events) {
         if (c.n_events < 6) return NMM_ERR_ARG;
@@ -543,6 +623,9 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
             const KvEpilogue e = kv_epilogue(c.kv_gamma, c.kv_eps, c.rope_theta, c.position, c.kv_cache, c.ld_cache,
                                              c.q_lora, c.kv_lora, c.rope, c.round, nullptr);
             st = launch_gemv_entry(ch.step[1], ch.plan[1], tickets, part, e, c.down_f32 + c.q_lora, stream);
+        } else if (i == 4 && att) {
+            st = launch_gemv_attention(ch.step[4], ch.plan[4], tickets, part, *att,
+                                       att_ws ? static_cast<uint8_t*>(workspace) + att_off : nullptr, att_ws, stream);
         } else {
             st = launch_gemv(ch.step[i], ch.plan[i], tickets, part, stream);
         }
@@ -551,6 +634,30 @@ nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace,
     if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[5]), s) != hipSuccess)
         return NMM_ERR_HIP;
     return NMM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+nmm_status nmm_mla_decode_chain(const nmm_mla_chain* chain, void* workspace, size_t workspace_bytes, void* stream) {
+    return run_chain(chain, nullptr, workspace, workspace_bytes, stream);
+}
+
+size_t nmm_mla_decode_step_workspace_size(const nmm_mla_chain* chain, const nmm_latent_attn* attn) {
+    if (!chain || !attn) return 0;
+    Chain ch;
+    if (build_chain(*chain, &ch) != NMM_OK) return 0;
+    size_t att_ws = 0;
+    if (attention_workspace_bytes(attn_args(*attn), &att_ws) != NMM_OK) return 0;
+    return rup256(ch.ws_total) + att_ws;
+}
+
+nmm_status nmm_mla_decode_step(const nmm_mla_chain* chain, const nmm_latent_attn* attn, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    if (!chain || !attn) return NMM_ERR_NULL;
+    const AttnArgs a = attn_args(*attn);
+    return run_chain(chain, &a, workspace, workspace_bytes, stream);
 }
 
 size_t nmm_mla_kv_update_workspace_size(const nmm_mla_kv* kv) {

@@ -27,6 +27,7 @@
 #include <cstdint>
 #include <cstdlib>
 
+#include "attention_core.h"
 #include "bf16_cast.h"
 #include "nmm_internal.h"
 
@@ -496,6 +497,27 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
     extern __shared__ float lds[];
     __shared__ int s_last;
     gemv_item<DT, MT, U, SM>(p, blockIdx.x, lds, &s_last);
+}
+
+// A bf16 single-row GEMV and an independent latent attention in one launch: workgroups
+// [0, gemv_grid) are the GEMV's (exactly as in its own launch, its x slice staged in the first of
+// attention's two chunk buffers), the rest are attention's, each a workgroup of the attention
+// launch.  The paper overlaps narrow MatMuls with independent matrix-core work (Condition 1 of
+// Section III-A); here the overlap is fixed by the launch itself -- the GEMV's workgroups stream
+// the weight while attention's run on the compute units the GEMV leaves free -- instead of
+// depending on how two streams are scheduled.
+constexpr int kAttnCh = 64, kAttnPitch = 584;
+static_assert(kThreads == attn::kAThreads, "the two kinds of workgroup have the same size");
+template <int U>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemv_attention_kernel(const KParams p, const attn::AttnParams a, uint32_t gemv_grid) {
+    __shared__ int s_last;
+    if (blockIdx.x < gemv_grid) {
+        float* lds = reinterpret_cast<float*>(attn::chunk_buffer_a<kAttnCh, kAttnPitch>());
+        gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
+    } else {
+        attn::attention_block<kAttnCh, 18, 32, kAttnPitch, true>(a, static_cast<int>(blockIdx.x - gemv_grid));
+    }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1211,6 +1233,32 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
     if (a.dt == NMM_BF16) launch_m<NMM_BF16>(kp, p.grid, lds, p.mt, p.unroll, s);
     else launch_m<NMM_F16>(kp, p.grid, lds, p.mt, p.unroll, s);
     return last_launch_status();
+}
+
+nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                                 const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream) {
+    attn::AttnLaunch al;
+    nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
+    if (st != NMM_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool fuse = al.grid > 0 && al.variant == attn::kAttnExact64 && al.p.pitch <= kAttnPitch &&
+                      g.dt == NMM_BF16 && g.batch == 1 && g.M == 1 && g.K > 0 && g.N > 0 && g.y && gp.mt == 1 &&
+                      (gp.unroll == 8 || gp.unroll == 16) &&
+                      gemv_lds_bytes(gp) <= size_t(kAttnCh) * kAttnPitch * 2 && gp.grid + al.grid < (int64_t(1) << 31);
+    if (!fuse) {
+        st = launch_gemv(g, gp, tickets, part, stream);
+        if (st != NMM_OK) return st;
+        return launch_prepared_attention(al, s);
+    }
+    const KParams kp = make_params(g, gp, tickets, part);
+    const dim3 grid(static_cast<uint32_t>(gp.grid + al.grid));
+    if (gp.unroll == 16)
+        hipLaunchKernelGGL(gemv_attention_kernel<16>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(gp.grid));
+    else
+        hipLaunchKernelGGL(gemv_attention_kernel<8>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(gp.grid));
+    st = last_launch_status();
+    if (st != NMM_OK) return st;
+    return launch_attention_merge(al, s);
 }
 
 namespace {

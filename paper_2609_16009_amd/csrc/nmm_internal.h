@@ -151,4 +151,26 @@ nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, con
 nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
                         unsigned* const* tickets, float* const* part, int grid, void* stream);
 
+// One latent-attention call (the arguments of nmm_latent_attention_ex).
+struct AttnArgs {
+    int64_t heads = 0, seq = 0, d_qk = 0, d_v = 0;
+    const void* q = nullptr; int64_t ldq = 0;
+    const void* kv = nullptr; int64_t ld_kv = 0;
+    float scale = 1.f;
+    float* out = nullptr; int64_t ldo = 0;
+    void* outb = nullptr; int64_t ldob = 0;
+    int64_t splits = 0;
+};
+// Workspace bytes of a valid call (0 when it needs none); NMM_ERR_* when the call is invalid.
+nmm_status attention_workspace_bytes(const AttnArgs& a, size_t* bytes);
+nmm_status launch_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes, void* stream);
+// Every check of launch_attention_args, without launching.
+nmm_status validate_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes);
+// The GEMV `g` (plain launch) and the attention `a` in one launch where both fit it (bf16, M = 1,
+// the 576 / 512 attention shape, the GEMV's LDS within one attention chunk buffer): attention's
+// workgroups follow the GEMV's, then attention's merge.  Other shapes take the two launches in
+// order.  The two must not touch each other's buffers.
+nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                                 const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
+
 }  // namespace nmm

@@ -280,7 +280,8 @@ def test_struct_layouts_match_the_header(tmp_path):
     probes = {"nmm_mla_chain": ["x", "events", "n_events", "kv_gamma", "kv_eps", "position", "kv_cache", "round"],
               "nmm_mla_kv": ["h", "ldw", "gamma", "eps", "rope_theta", "position", "mm", "cache_rows", "round"],
               "nmm_plan_info": ["path", "grid", "workspace_bytes"],
-              "nmm_mla_query_path": ["x", "kv_gamma", "kv_eps", "position", "round", "down_f32", "query", "ldq"]}
+              "nmm_mla_query_path": ["x", "kv_gamma", "kv_eps", "position", "round", "down_f32", "query", "ldq"],
+              "nmm_latent_attn": ["heads", "q", "ldq", "kv", "scale", "out", "ldo", "out_bf16", "ldob", "splits"]}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "nmm.h"', "int main(void) {"]
     for st, fields in probes.items():
         lines.append(f'  printf("{st} sizeof %zu\\n", sizeof({st}));')
@@ -431,3 +432,65 @@ def test_query_path_rejects_invalid_arguments():
     assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need, None) == nmm.NMM_ERR_SHAPE
     c.rope, c.query = 64, ALIGNED + 1
     assert L.nmm_mla_query_path_run(ctypes.byref(c), ALIGNED, need, None) == nmm.NMM_ERR_ALIGN
+
+
+def fake_step(chain_kv=False):
+    """A decode step's argument structs over fake, disjoint 1 GiB "device" regions (validation only)."""
+    c = nmm.nmm_mla_chain()
+    for k, v in dict(hidden=7168, q_lora=1536, kv_lora=512, rope=64, heads=128, nope=128, v_head=128).items():
+        setattr(c, k, v)
+    region = iter(range(1 << 34, 1 << 40, 1 << 30))
+    for k in nmm.CHAIN_BUFFERS:
+        setattr(c, k, next(region))
+    if chain_kv:
+        c.kv_gamma, c.kv_cache = next(region), next(region)
+        c.kv_eps, c.rope_theta, c.position, c.ld_cache, c.cache_rows = 1e-6, 10000.0, 4096, 576, 4097
+    a = nmm.nmm_latent_attn()
+    a.heads, a.seq, a.d_qk, a.d_v, a.ldq, a.ld_kv, a.ldo, a.scale, a.splits = 128, 4096, 576, 512, 576, 576, 512, 0.07, 16
+    a.q, a.kv, a.out = next(region), next(region), next(region)
+    return c, a
+
+
+def test_decode_step_workspace_and_validation():
+    c, a = fake_step()
+    chain_ws = L.nmm_mla_decode_chain_workspace_size(ctypes.byref(c))
+    need = L.nmm_mla_decode_step_workspace_size(ctypes.byref(c), ctypes.byref(a))
+    att_ws = L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 16)
+    assert need == (chain_ws + 255) // 256 * 256 + att_ws and att_ws > 0
+    step = lambda wsb=need: L.nmm_mla_decode_step(ctypes.byref(c), ctypes.byref(a), ALIGNED, wsb, None)
+    assert L.nmm_mla_decode_step(None, ctypes.byref(a), ALIGNED, need, None) == nmm.NMM_ERR_NULL
+    assert L.nmm_mla_decode_step(ctypes.byref(c), None, ALIGNED, need, None) == nmm.NMM_ERR_NULL
+    assert L.nmm_mla_decode_step_workspace_size(ctypes.byref(c), None) == 0
+    assert step(need - 1) == nmm.NMM_ERR_WORKSPACE
+    # the attention reads what the chain writes (its q on the chain's q_f32)
+    q = a.q
+    a.q = c.q_f32
+    assert step() == nmm.NMM_ERR_ARG
+    # ... or writes what the chain reads (its output on W_O; its bf16 copy on x)
+    a.q, out = q, a.out
+    a.out = c.w_o + 4096
+    assert step() == nmm.NMM_ERR_ARG
+    a.out, a.out_bf16, a.ldob = out, c.x, 512
+    assert step() == nmm.NMM_ERR_ARG
+    a.out_bf16, a.ldob = None, 0
+    # the attention's own limits, all before any launch
+    a.out = out + 4
+    assert step() == nmm.NMM_ERR_ALIGN
+    a.out, a.ldq = out, 1 << 40
+    assert step() == nmm.NMM_ERR_SHAPE
+    a.ldq, a.d_qk = 576, 577
+    assert L.nmm_mla_decode_step_workspace_size(ctypes.byref(c), ctypes.byref(a)) == 0
+    assert step() == nmm.NMM_ERR_SHAPE
+    a.d_qk, a.splits = 576, -1
+    assert step() == nmm.NMM_ERR_ARG
+
+
+def test_decode_step_refuses_attention_over_the_new_cache_row():
+    c, a = fake_step(chain_kv=True)
+    need = L.nmm_mla_decode_step_workspace_size(ctypes.byref(c), ctypes.byref(a))
+    step = lambda: L.nmm_mla_decode_step(ctypes.byref(c), ctypes.byref(a), ALIGNED, need, None)
+    a.kv = c.kv_cache                       # rows 0 .. 4095; the chain writes row 4096
+    a.seq = 4097
+    assert step() == nmm.NMM_ERR_ARG
+    a.seq = 4096                            # stops short of the new row: independent, but this would
+    assert L.nmm_mla_decode_step_workspace_size(ctypes.byref(c), ctypes.byref(a)) > 0   # launch; not run here

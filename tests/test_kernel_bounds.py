@@ -343,3 +343,29 @@ def test_qrope_workgroup_covers_each_pair_once(heads, nope, rope, kv, ldq):
             assert h * qk + nope + 2 * j + 1 < heads * qk
             assert kv + 2 * j + 1 < ldq and h * ldq + kv + 2 * j + 1 < heads * ldq
     assert np.all(seen == 1)
+
+
+@pytest.mark.parametrize("K,N", [(16384, 7168), (144, 1032), (2048, 512)])
+def test_gemv_attention_launch_shares_lds_and_grid(K, N):
+    """gemv_attention_kernel: workgroups [0, gemv_grid) run the GEMV exactly as its own launch
+    (same ids, so the same items), the rest are attention workgroups 0 .. attention grid - 1; the
+    GEMV's x slice (rows_max * 4 bytes, or the 4 x 256 x 8 floats of its reduction) must fit the
+    first attention chunk buffer of 64 x 584 bf16."""
+    p = nmm.nmm_gemv_plan(1, K, N, nmm.NMM_BF16, nmm.NMM_PATH_GEMV)
+    assert p["m_tile"] == 1 and p["unroll"] in (8, 16)
+    rows_max = max(p["rows_full"], p["rows_tail"])
+    gemv_lds = max(rows_max * 1 * 4, 1 * 256 * 8 * 4)
+    assert gemv_lds <= 64 * 584 * 2
+    for heads, seq, splits in ((128, 4096, 16), (128, 4096, 0), (70, 300, 3), (1, 64, 1)):
+        ws = nmm.nmm_latent_attention_workspace_size(heads, seq, 576, 512)
+        n_hb = (heads + 63) // 64
+        span = -(-seq // max(1, min(splits or max(1, 64 // n_hb), -(-seq // 64))))
+        span = -(-span // 64) * 64
+        nsp = -(-seq // span)
+        agrid = n_hb * nsp
+        total = p["grid"] + agrid
+        ids = np.arange(total)
+        gemv_ids, attn_ids = ids[ids < p["grid"]], ids[ids >= p["grid"]] - p["grid"]
+        assert np.array_equal(gemv_ids, np.arange(p["grid"]))
+        assert np.array_equal(attn_ids, np.arange(agrid)) and total < 2 ** 31
+        assert ws >= 0
