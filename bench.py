@@ -3,10 +3,13 @@
 
 A step is one pass of the whole hot path over one token: the narrow-MatMul chain
 (x[1,7168] -> down-projection [7168,2112] -> W_UQ [1536,24576] -> per-head W_UK [128 x 128x512]
--> per-head W_UV [128 x 512x128] -> W_O [16384,7168], bf16 hand-offs fused into each gather) on
-stream A, concurrently with latent attention (128 heads over a 4096-position latent cache,
-d_qk 576, d_v 512) on stream B -- the paper's overlap of narrow MatMul with independent
-matrix-unit work, on two HIP streams.
+-> per-head W_UV [128 x 512x128] -> W_O [16384,7168], bf16 hand-offs fused into each gather) and,
+concurrently, latent attention (128 heads over a 4096-position latent cache, d_qk 576, d_v 512)
+-- the paper's overlap of narrow MatMul with independent matrix-unit work.  The step is one call
+of nmm_mla_decode_step on one stream: attention's workgroups share W_O's launch, so the overlap
+is fixed by the launch.  Steps are issued back to back (one C call each); the graph-replay form
+and the earlier two-stream form (chain and attention on two streams, fork / join per step) are
+timed beside it.
 
 Inputs are seeded synthetic tensors at the model's shapes (trained weights are not available).
 `--copies` weight sets (3 x 380 MB by default, > 1 GiB) are rotated step by step so that W comes
@@ -410,21 +413,31 @@ def main() -> int:
 
     sa, sb = torch.cuda.Stream(device=dev), torch.cuda.Stream(device=dev)
     cap = torch.cuda.Stream(device=dev)        # capture / replay stream
-    ws_a, ws_b = nmm.Workspace(dev), nmm.Workspace(dev)
+    ws_a, ws_b, ws_s = nmm.Workspace(dev), nmm.Workspace(dev), nmm.Workspace(dev)
     ev = lambda: torch.cuda.Event(enable_timing=True)
     K, W = args.steps, args.warmup
     chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a) for c in range(args.copies)]
 
-    # beside the HBM-bound chain, attention runs on half its standalone partition (16 position spans
-    # per head block, 32 workgroups) and takes fewer CUs from the chain: 88.8-89.4 us per step
-    # against 90.5-91.7 us with the 64-workgroup default, measured on one box
+    # attention beside the chain runs on 16 position spans per head block (32 workgroups): in the
+    # decode step's shared launch W_O's 224 workgroups and these fill the 256 compute units once
+    # (78.4 us per step; 78.1 with 11 spans, 81.9 with 32, 85.0 with 8, on one box)
     def attention(s, stream, splits=ATTN_OVERLAP_SPLITS):
         _, q, kv = copies[s % args.copies]
         nmm.nmm_latent_attention_ex(q, kv, att_out, step.scale, splits=splits, d_qk=dqk, d_v=dv, workspace=ws_b,
                                     stream=stream)
 
+    # the decode step: one call, attention's workgroups in W_O's launch
+    steps_one = [nmm.PreparedStep(d, {**copies[c][0], **inter},
+                                  dict(q=copies[c][1], kv=copies[c][2], out=att_out, scale=step.scale,
+                                       splits=ATTN_OVERLAP_SPLITS, d_qk=dqk, d_v=dv), workspace=ws_s)
+                 for c in range(args.copies)]
+
+    def one_launch(s):
+        steps_one[s % args.copies].launch(stream=cap)
+
     def decode_step(s):
-        # fork: stream A runs the narrow chain, stream B the latent attention; then join
+        # the two-stream form: stream A runs the narrow chain, stream B the latent attention; fork,
+        # then join
         start = torch.cuda.Event()
         start.record(cap)
         sa.wait_event(start)
@@ -456,10 +469,11 @@ def main() -> int:
     torch.cuda.synchronize()
     y_eager, att_eager = inter["y"].clone(), att_out.clone()
     t = time.perf_counter()
-    step_graphs = [capture(decode_step, s) for s in range(args.copies)]
+    two_stream_graphs = [capture(decode_step, s) for s in range(args.copies)]
+    one_launch_graphs = [capture(one_launch, s) for s in range(args.copies)]
     alone = {name: [capture(fn, s) for s in range(args.copies)]
              for name, fn in (("chain", chain_only), ("attention", attn_only), ("serial", serial))}
-    log(f"[bench] captured {4 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
+    log(f"[bench] captured {5 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
 
     def timed(graphs, n):
         """Mean time per replay of n replays (graphs rotated), events on the replay stream."""
@@ -472,29 +486,41 @@ def main() -> int:
         torch.cuda.synchronize()
         return a.elapsed_time(b) / n
 
-    # ---- warmup, then exactly K timed decode steps (one graph replay each)
-    timed(step_graphs, W)
-    step_ms = timed(step_graphs, K)
+    def issued(fn, n):
+        """Mean time per step of n steps issued back to back on the replay stream (events on it),
+        and the host's issue time per step."""
+        a, b = ev(), ev()
+        torch.cuda.synchronize()
+        with torch.cuda.stream(cap):
+            a.record(cap)
+            h0 = time.perf_counter()
+            for s in range(n):
+                fn(s)
+            h1 = time.perf_counter()
+            b.record(cap)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n, (h1 - h0) / n * 1e3
+
+    # ---- warmup, then exactly K timed decode steps (one nmm_mla_decode_step call each)
+    issued(one_launch, W)
+    step_ms, host_ms = issued(one_launch, K)
+    assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
+        "the one-launch decode step must reproduce the two-stream step bit for bit"
+    # ---- the same step as graph replays, and the two-stream form (graph replays, and issued on
+    # the two streams with a fork / join per step)
+    timed(one_launch_graphs, W)
+    graph_ms = timed(one_launch_graphs, K)
+    timed(two_stream_graphs, W)
+    two_graph_ms = timed(two_stream_graphs, K)
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
         "graph replays must reproduce the eager decode step bit for bit"
-
-    # ---- the same K decode steps launched eagerly on the two streams (each stream has its own
-    # hardware queue, so the branches really run side by side; a graph replay issues all of its
-    # nodes through one queue, where a dependent node waits for every node queued before it)
-    def eager_steps(n):
-        a, b = ev(), ev()
-        a.record(cap)
-        for s in range(n):
-            decode_step(s)
-        b.record(cap)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / n
-
-    eager_steps(W)
-    eager_ms = eager_steps(K)
+    issued(decode_step, W)
+    two_eager_ms, _ = issued(decode_step, K)
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
-        "eager two-stream steps must reproduce the first eager step bit for bit"
-    log(f"[bench] decode step: graph replay {step_ms * 1e3:.1f} us, eager on two streams {eager_ms * 1e3:.1f} us")
+        "two-stream steps must reproduce the first step bit for bit"
+    log(f"[bench] decode step (one launch for W_O + attention): {step_ms * 1e3:.1f} us issued back to back "
+        f"(host {host_ms * 1e3:.1f} us per call), {graph_ms * 1e3:.1f} us as graph replays; two streams: "
+        f"{two_graph_ms * 1e3:.1f} us graph replays, {two_eager_ms * 1e3:.1f} us issued")
 
     # ---- the overlap experiment: each stream alone, then both serially on one stream
     timed(alone["chain"], W)
@@ -506,6 +532,11 @@ def main() -> int:
     t_b_default = timed(att_default, K)
     timed(alone["serial"], W)
     t_serial = timed(alone["serial"], K)
+    # chain alone and chain then attention, issued like the decode step (the overlap's baseline)
+    issued(chain_only, W)
+    t_a_issued, _ = issued(chain_only, K)
+    issued(serial, W)
+    t_serial_issued, _ = issued(serial, K)
     # the chain with the cache entry behind its down-projection (RMSNorm, RoPE, one row of a
     # latent cache), timed right after the chain alone
     kvc = syn.kv_update_case()
@@ -519,11 +550,11 @@ def main() -> int:
     timed(kv_graphs, W)
     t_a_kv = timed(kv_graphs, K)
     log(f"[bench] chain with the cache entry {t_a_kv * 1e3:.1f} us (without: {t_a * 1e3:.1f} us)")
-    gain = mean_gain(step_ms, t_serial)
+    gain = mean_gain(step_ms, t_serial_issued)
     bound = 1.0 - max(t_a, t_b) / (t_a + t_b)
-    log(f"[bench] chain alone {t_a * 1e3:.1f} us, attention alone {t_b * 1e3:.1f} us, serial "
-        f"{t_serial * 1e3:.1f} us, concurrent {step_ms * 1e3:.1f} us: gain {100 * gain:.1f}% "
-        f"(bound {100 * bound:.1f}%)")
+    log(f"[bench] chain alone {t_a * 1e3:.1f} us (issued {t_a_issued * 1e3:.1f} us), attention alone "
+        f"{t_b * 1e3:.1f} us, serial {t_serial * 1e3:.1f} us (issued {t_serial_issued * 1e3:.1f} us), decode step "
+        f"{step_ms * 1e3:.1f} us: gain {100 * gain:.1f}% (bound {100 * bound:.1f}%)")
     assert torch.isfinite(inter["y"]).all() and torch.isfinite(att_out).all()
 
     # ---- each MatMul of the chain alone (same shapes and plans, its own graph)
@@ -591,10 +622,11 @@ def main() -> int:
         "config": {
             "workload": "DeepSeek-V3 MLA single-token decode step: narrow chain x[1,7168] . "
                         "down[7168,2112] . W_UQ[1536,24576] . 128 x W_UK[128,512] . 128 x W_UV[512,128] . "
-                        "W_O[16384,7168] on stream A, concurrent latent attention 128 heads x 4096 "
-                        "positions (d_qk 576, d_v 512) on stream B",
+                        "W_O[16384,7168], with latent attention 128 heads x 4096 positions (d_qk 576, "
+                        "d_v 512) beside W_O in one launch (nmm_mla_decode_step, one stream, steps issued "
+                        "back to back)",
             "tokens": 1, "heads": d["heads"], "kv_len": seq, "weight_copies_rotated": args.copies,
-            "bytes_per_step": chain_total + attn_total, "parallelism": "single GPU, two HIP streams",
+            "bytes_per_step": chain_total + attn_total, "parallelism": "single GPU, one HIP stream",
         },
         "roofline": {
             "bound": "hbm",
@@ -618,7 +650,13 @@ def main() -> int:
             "attention_splits": ATTN_OVERLAP_SPLITS,
             "attention_default_partition_us": round(t_b_default * 1e3, 2),
             "serial_us": round(t_serial * 1e3, 2),
+            "chain_issued_us": round(t_a_issued * 1e3, 2),
+            "serial_issued_us": round(t_serial_issued * 1e3, 2),
             "concurrent_us": round(step_ms * 1e3, 2),
+            "decode_step_host_us_per_call": round(host_ms * 1e3, 2),
+            "decode_step_graph_us": round(graph_ms * 1e3, 2),
+            "two_streams_graph_us": round(two_graph_ms * 1e3, 2),
+            "two_streams_issued_us": round(two_eager_ms * 1e3, 2),
             "overlap_gain": round(gain, 4),
             "overlap_gain_bound": round(bound, 4),
             "per_matmul_us": {n: round(t, 2) for n, t in per_matmul.items()},
