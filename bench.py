@@ -420,7 +420,7 @@ def main() -> int:
 
     # attention beside the chain runs on 16 position spans per head block (32 workgroups): in the
     # decode step's shared launch W_O's 224 workgroups and these fill the 256 compute units once
-    # (78.4 us per step; 78.1 with 11 spans, 81.9 with 32, 85.0 with 8, on one box)
+    # (78.4 us per step; 78.1 with 11 spans, 81.9 with 32, 85.0 with 8, measured on one MI355X)
     def attention(s, stream, splits=ATTN_OVERLAP_SPLITS):
         _, q, kv = copies[s % args.copies]
         nmm.nmm_latent_attention_ex(q, kv, att_out, step.scale, splits=splits, d_qk=dqk, d_v=dv, workspace=ws_b,
