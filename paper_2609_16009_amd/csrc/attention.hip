@@ -48,8 +48,9 @@ void attention_kernel(const AttnParams p) {
 //   out = sum_s w_s O_s,  w_s = 2^(m_s - M) / sum_q 2^(m_q - M) l_q,  M = max_s m_s.
 // One output per thread: a workgroup owns 4 heads x 64 columns, so 64 threads read one
 // 256-byte segment of a (head, span) row.  The partial outputs' loads go out first; the spans'
-// (max, sum) pairs follow, one pair per thread, into LDS, where one thread per head forms the
-// weights -- so the whole merge waits for about one memory round trip.
+// (max, sum) pairs follow, one pair per thread, into LDS.  Up to 16 spans, wave 0 forms the
+// weights with one lane per (span, head) and an xor butterfly across the spans; beyond that one
+// thread per head walks them.  The whole merge waits for about one memory round trip.
 constexpr int kMergeCols = 64;
 constexpr int kMergeHeads = kAThreads / kMergeCols;   // 4
 constexpr int kMergeBatch = 32;
@@ -77,7 +78,24 @@ __global__ __launch_bounds__(kAThreads) void attention_merge_kernel(const AttnPa
         mls[2 * t + 1] = ml[1];
     }
     __syncthreads();
-    if (tid < kMergeHeads) {
+    if (p.nsp * kMergeHeads <= 64) {
+        // up to 16 spans: lane q * 4 + hh of wave 0 holds span q of head hh; each head's max and
+        // normaliser cross the lanes of that head with a fixed xor butterfly (lanes past the
+        // spans contribute a weight of 0)
+        if (tid < 64) {
+            const bool ok = tid < p.nsp * kMergeHeads;
+            const float m = ok ? mls[2 * tid] : -INFINITY;
+            const float l = ok ? mls[2 * tid + 1] : 0.f;
+            float M = m;
+#pragma unroll
+            for (int off = kMergeHeads; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+            const float w = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - M);
+            float den = w * l;
+#pragma unroll
+            for (int off = kMergeHeads; off < 64; off <<= 1) den += __shfl_xor(den, off);
+            if (ok) wgt[tid] = w * (1.f / den);
+        }
+    } else if (tid < kMergeHeads) {
         float M = -INFINITY;
         for (int q = 0; q < p.nsp; ++q) M = fmaxf(M, mls[2 * (q * kMergeHeads + tid)]);
         float den = 0.f;
