@@ -27,7 +27,7 @@ import sys
 import time
 
 
-ATTN_OVERLAP_SPLITS = 16
+ATTN_OVERLAP_SPLITS = 12
 
 
 def mean_gain(t_opt: float, t_base: float) -> float:
@@ -418,9 +418,10 @@ def main() -> int:
     K, W = args.steps, args.warmup
     chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a) for c in range(args.copies)]
 
-    # attention beside the chain runs on 16 position spans per head block (32 workgroups): in the
-    # decode step's shared launch W_O's 224 workgroups and these fill the 256 compute units once
-    # (78.4 us per step; 78.1 with 11 spans, 81.9 with 32, 85.0 with 8, measured on one MI355X)
+    # attention beside the chain: 12 position spans requested per head block (11 result, of 6
+    # chunks each: 22 workgroups beside W_O's 224 in the decode step's shared launch).  Fewer spans
+    # write fewer partial outputs into the HBM-bound launch: 77.4-77.7 us per step against
+    # 78.0-78.3 with 16 spans (32 workgroups), 81.9 with 32 and 85.0 with 8, measured on one MI355X
     def attention(s, stream, splits=ATTN_OVERLAP_SPLITS):
         _, q, kv = copies[s % args.copies]
         nmm.nmm_latent_attention_ex(q, kv, att_out, step.scale, splits=splits, d_qk=dqk, d_v=dv, workspace=ws_b,

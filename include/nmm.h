@@ -355,7 +355,8 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
  * of heads (0: the default, about 64 workgroups; the span is rounded up to whole 64-position
  * chunks, so fewer spans may result), and an optional bf16 copy of the output (out_bf16 may be
  * NULL).  Beside an HBM-bound stream a smaller partition interferes less: on MI355X the decode
- * step is fastest with 16 spans (32 workgroups) against 32 for attention alone.  Workspace:
+ * step (nmm_mla_decode_step) is fastest with 11 to 16 spans (22 to 32 workgroups) against 32 for
+ * attention alone.  Workspace:
  * nmm_latent_attention_ex_workspace_size with the same splits. */
 nmm_status nmm_latent_attention_ex(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
                                    const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
