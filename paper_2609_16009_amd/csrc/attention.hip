@@ -20,8 +20,9 @@
 //    LDS reads, V^T fragments (8 positions of one column) with ds_read_b64_tr_b16, gfx950's
 //    transposing LDS read.
 //  * Spans write (max, sum, unnormalised output) partials; a merge kernel on the same stream
-//    combines them in span order.  The spans of one head block sit on one XCD (workgroup ids 8
-//    apart) so the cache rows they share are read from HBM once per XCD.
+//    combines them in span order.  From 8 spans on, the head blocks of one span sit on one XCD
+//    (workgroup ids 8 apart, the grid padded to whole groups of 8 spans) so the cache rows they
+//    share are read from HBM once per XCD.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -126,6 +127,7 @@ __global__ __launch_bounds__(kAThreads) void attention_merge_kernel(const AttnPa
 
 struct AttnPlan {
     int n_hb = 0, nsp = 1, span = 0, xcd_map = 0, ch = 64, cols = 0, pitch = 0;
+    int grid_sp = 1;    // spans in the grid: nsp, padded to a multiple of 8 when xcd_map
     size_t ws_bytes = 0;
 };
 
@@ -158,7 +160,11 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     nsp = (seq + span - 1) / span;
     a.nsp = static_cast<int>(nsp);
     a.span = static_cast<int>(span);
-    a.xcd_map = (a.nsp % 8 == 0) ? 1 : 0;
+    // spans grouped per XCD (the same span of every head block on one XCD, so its cache rows are
+    // read once per XCD) from 8 spans on; past 8 the grid is padded to a multiple of 8 spans and
+    // the padding workgroups exit at once
+    a.xcd_map = (a.nsp % 8 == 0 || a.nsp > 8) ? 1 : 0;
+    a.grid_sp = a.xcd_map ? (a.nsp + 7) / 8 * 8 : a.nsp;
     if (a.pitch > (a.ch == 64 ? 584 : 1032)) return NMM_ERR_SHAPE;
     // partial results live past the workspace's counter block (which GEMV calls sharing the
     // workspace rely on being zero)
@@ -242,7 +248,7 @@ nmm_status prepare(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const 
     p.scale_log2 = scale * 1.4426950408889634f;
     p.kv_extent = static_cast<uint32_t>(extent);
     p.q_extent = static_cast<uint32_t>(q_extent);
-    out->grid = int64_t(a.n_hb) * a.nsp;
+    out->grid = int64_t(a.n_hb) * a.grid_sp;
     out->merge_grid = a.nsp > 1 ? ((heads + kMergeHeads - 1) / kMergeHeads) * ((d_v + kMergeCols - 1) / kMergeCols) : 0;
     out->variant = (d_qk == 576 && d_v == 512) ? (a.ch == 64 ? kAttnExact64 : kAttnExact32)
                                                 : (a.ch == 64 ? kAttnGeneral64 : kAttnGeneral32);

@@ -40,7 +40,7 @@ struct AttnParams {
     int cols;           // staged columns per cache row: max(d_qk, d_v)
     int pitch;          // LDS row pitch of a staged chunk (elements)
     int nsp, span, n_hb;
-    int xcd_map;        // 1: spans grouped per XCD (nsp % 8 == 0)
+    int xcd_map;        // 1: spans grouped per XCD (grid of n_hb x nsp padded to a multiple of 8)
     float scale_log2;   // scale * log2(e): scores are kept in log2 units
     uint32_t kv_extent; // bytes of the cache that may be read
     uint32_t q_extent;  // bytes of q that may be read
@@ -139,6 +139,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     if (p.xcd_map) {
         sp = (bid & 7) + 8 * (bid / (8 * p.n_hb));
         hb = (bid >> 3) % p.n_hb;
+        if (sp >= p.nsp) return;    // padding of the grid to whole groups of 8 spans
     } else {
         hb = bid % p.n_hb;
         sp = bid / p.n_hb;

@@ -362,10 +362,36 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
         span = -(-seq // max(1, min(splits or max(1, 64 // n_hb), -(-seq // 64))))
         span = -(-span // 64) * 64
         nsp = -(-seq // span)
-        agrid = n_hb * nsp
+        agrid = n_hb * ((nsp + 7) // 8 * 8 if (nsp % 8 == 0 or nsp > 8) else nsp)
         total = p["grid"] + agrid
         ids = np.arange(total)
         gemv_ids, attn_ids = ids[ids < p["grid"]], ids[ids >= p["grid"]] - p["grid"]
         assert np.array_equal(gemv_ids, np.arange(p["grid"]))
         assert np.array_equal(attn_ids, np.arange(agrid)) and total < 2 ** 31
         assert ws >= 0
+
+
+@pytest.mark.parametrize("n_hb,nsp", [(2, 16), (2, 11), (2, 32), (1, 9), (3, 22), (2, 3), (1, 1), (2, 64)])
+def test_attention_workgroups_cover_every_head_block_and_span_once(n_hb, nsp):
+    """attention_block's workgroup -> (head block, span) map: from 8 spans on (xcd_map) the grid
+    holds nsp padded to a multiple of 8 per head block, workgroup b takes span (b % 8) + 8 (b / 8
+    n_hb) of head block (b / 8) % n_hb, and the padding spans exit; otherwise the plain order.
+    Every (head block, span) runs once, and with xcd_map the workgroups of one span sit 8 ids
+    apart, on one XCD (ids are dealt to the 8 XCDs round robin; the decode step's launch puts
+    attention after 224 GEMV workgroups, a multiple of 8)."""
+    xcd_map = nsp % 8 == 0 or nsp > 8
+    grid_sp = (nsp + 7) // 8 * 8 if xcd_map else nsp
+    seen = {}
+    for b in range(n_hb * grid_sp):
+        if xcd_map:
+            sp, hb = (b & 7) + 8 * (b // (8 * n_hb)), (b >> 3) % n_hb
+            if sp >= nsp:
+                continue
+        else:
+            hb, sp = b % n_hb, b // n_hb
+        assert (hb, sp) not in seen
+        seen[(hb, sp)] = b
+    assert set(seen) == {(h, s_) for h in range(n_hb) for s_ in range(nsp)}
+    if xcd_map:
+        for s_ in range(nsp):
+            assert len({seen[(h, s_)] % 8 for h in range(n_hb)}) == 1
