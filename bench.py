@@ -519,6 +519,21 @@ def main() -> int:
     two_eager_ms, _ = issued(decode_step, K)
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
         "two-stream steps must reproduce the first step bit for bit"
+    # the step's segments from the chain's event hook (events before each launch and after the
+    # merge; a separate pass, since the events add work between the launches)
+    ev_slots = [[ev() for _ in range(6)] for _ in range(K)]
+    steps_ev = [nmm.PreparedStep(d, {**copies[c][0], **inter},
+                                 dict(q=copies[c][1], kv=copies[c][2], out=att_out, scale=step.scale,
+                                      splits=ATTN_OVERLAP_SPLITS, d_qk=dqk, d_v=dv), workspace=ws_s, events=ev_slots)
+                for c in range(args.copies)]
+    with torch.cuda.stream(cap):
+        for i in range(K):
+            steps_ev[i % args.copies].launch(slot=i, stream=cap)
+    torch.cuda.synchronize()
+    seg = (("down", 0, 1), ("w_uq", 1, 2), ("w_uk_w_uv_pair", 2, 4), ("w_o_with_attention_and_merge", 4, 5))
+    segments = {n: round(sum(ev_slots[i][a].elapsed_time(ev_slots[i][b]) for i in range(K)) / K * 1e3, 2)
+                for n, a, b in seg}
+    assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager)
     log(f"[bench] decode step (one launch for W_O + attention): {step_ms * 1e3:.1f} us issued back to back "
         f"(host {host_ms * 1e3:.1f} us per call), {graph_ms * 1e3:.1f} us as graph replays; two streams: "
         f"{two_graph_ms * 1e3:.1f} us graph replays, {two_eager_ms * 1e3:.1f} us issued")
@@ -656,6 +671,7 @@ def main() -> int:
             "concurrent_us": round(step_ms * 1e3, 2),
             "decode_step_host_us_per_call": round(host_ms * 1e3, 2),
             "decode_step_graph_us": round(graph_ms * 1e3, 2),
+            "decode_step_segments_with_events_us": segments,
             "two_streams_graph_us": round(two_graph_ms * 1e3, 2),
             "two_streams_issued_us": round(two_eager_ms * 1e3, 2),
             "overlap_gain": round(gain, 4),
