@@ -1,7 +1,8 @@
 // Single-token latent attention on the matrix cores (gfx950), the decode step's independent
 // dense work.  The paper's point is that narrow MatMuls moved off the matrix unit let
 // independent matrix-unit work start earlier (Condition 1 "Data Independence", Section III-A;
-// Section IV-A); this kernel is that independent work here, run on its own stream.
+// Section IV-A); this kernel is that independent work here, run on its own or with its workgroups
+// beside the last narrow MatMul's in one launch (the decode step).
 //
 //   s_j = scale * q_h . kv_j[:d_qk],  p = softmax(s),  out_h = sum_j p_j kv_j[:d_v]
 //
