@@ -494,3 +494,19 @@ def test_decode_step_refuses_attention_over_the_new_cache_row():
     assert step() == nmm.NMM_ERR_ARG
     a.seq = 4096                            # stops short of the new row: independent, but this would
     assert L.nmm_mla_decode_step_workspace_size(ctypes.byref(c), ctypes.byref(a)) > 0   # launch; not run here
+
+
+def test_prepared_step_refuses_invalid_sizes_before_any_launch():
+    """The binding's PreparedStep queries the workspace size first: an invalid attention shape
+    (d_qk not a multiple of 32) gives 0 and a ValueError, with nothing allocated or launched."""
+    import torch
+    dims = dict(hidden=7168, q_lora=1536, kv_lora=512, rope=64, heads=128, nope=128, v_head=128)
+    t = torch.zeros(8, dtype=torch.bfloat16)
+    bufs = {k: t for k in nmm.CHAIN_BUFFERS}
+    attn = dict(q=torch.zeros((4, 577), dtype=torch.bfloat16), kv=torch.zeros((16, 577), dtype=torch.bfloat16),
+                out=torch.zeros((4, 512)), scale=0.1, d_qk=577)
+    with pytest.raises(ValueError):
+        nmm.PreparedStep(dims, bufs, attn)
+    a = nmm._attn_struct(dict(attn, d_qk=576, splits=12))
+    assert (a.heads, a.seq, a.d_qk, a.d_v, a.ldq, a.ld_kv, a.ldo, a.splits) == (4, 16, 576, 512, 577, 577, 512, 12)
+    assert not a.out_bf16 and a.ldob == 0
