@@ -34,9 +34,15 @@ def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
+# Sources whose matrix-core accumulators must stay in ordinary VGPRs (the attention's softmax and
+# output stages touch them with vector instructions; in AGPRs each touch costs copies).
+VGPR_FORM = {"attention.hip", "gemv.hip"}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    extra = ["-mllvm", "-amdgpu-mfma-vgpr-form=true"] if os.path.basename(src) in VGPR_FORM else []
+    cmd = [HIPCC, *CFLAGS, *extra, "-c", src, "-o", obj]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)

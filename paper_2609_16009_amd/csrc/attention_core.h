@@ -1,6 +1,7 @@
-// The latent-attention workgroup (flash-decoding over a span of cache positions for 64 heads),
-// shared by the attention launch and by the W_O launch that runs attention workgroups beside
-// its GEMV workgroups.  The design is described where the attention launch is defined.
+// The latent-attention workgroup (flash-decoding over a span of cache positions for a block of
+// heads), shared by the attention launch and by the W_O launch that runs attention workgroups
+// beside its GEMV workgroups.  The design is described where the attention launch is defined
+// (attention.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -18,12 +19,27 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kHB = 64;           // heads per workgroup (16 per wave)
-constexpr int kAThreads = 256;
+constexpr int kAThreads = 256;            // 4 waves (the W_O launch's attention workgroups)
+constexpr int kAThreads8 = 512;           // 8 waves (the attention launch)
+constexpr int kCh = 64;                   // cache positions per chunk (16 per wave in Q.K^T)
+constexpr int kMaxCols = 576;             // staged columns per cache row: max(d_qk, d_v)
+constexpr int kPadSlots = 2;              // 16-byte padding slots after each staged row
+constexpr int kPitchMax = kMaxCols + 8 * kPadSlots;   // 592 elements: LDS row pitch at 576 columns
+constexpr int kMaxKs = kMaxCols / 32;     // Q.K^T k-steps (32 dims each)
+constexpr int kMaxNtw = 8;                // P.V column tiles (16 columns) per wave: d_v <= 512
+constexpr int kMaxHt = 2;                 // head tiles (16 heads) per workgroup, at most
+constexpr int kHt = 2;                    // head tiles per workgroup of the attention launches
+constexpr int kPPitch = kCh + 8;          // row pitch (elements) of P in LDS
+constexpr int kKw = 6;                    // K fragments in flight in Q.K^T
 constexpr int kRsrcWord3 = 0x00020000;
 constexpr uint32_t kOutOfRange = 0x80000000u;
+// A chunk rescales the running output only when its maximum exceeds the running reference by
+// more than this (log2 units), so probabilities stay below 2^kLazyTh and the rescale is rare.
+constexpr float kLazyTh = 8.f;
 
 struct AttnParams {
     const uint16_t* q;
@@ -34,13 +50,14 @@ struct AttnParams {
     int64_t ldo;
     uint16_t* outb;     // optional bf16 copy of out (nearest, ties to even), outb[h * ldob + n]
     int64_t ldob;
-    float* part_o;      // [n_hb][nsp][64][d_v]
-    float* part_ml;     // [n_hb][nsp][64][2]
+    float* part_o;      // [n_hb][nsp][hb][d_v]: unnormalised span outputs (hb = heads per block)
+    float* part_ml;     // [n_hb][nsp][hb][2]: the span's reference maximum and probability sum
     int heads, seq, dqk, dv;
     int cols;           // staged columns per cache row: max(d_qk, d_v)
     int pitch;          // LDS row pitch of a staged chunk (elements)
     int nsp, span, n_hb;
-    int xcd_map;        // 1: spans grouped per XCD (grid of n_hb x nsp padded to a multiple of 8)
+    int hbh;            // heads per block (16 per head tile)
+    int xcd_map;        // 1: the head blocks of a span grouped on one XCD (grid padded to 8 spans)
     float scale_log2;   // scale * log2(e): scores are kept in log2 units
     uint32_t kv_extent; // bytes of the cache that may be read
     uint32_t q_extent;  // bytes of q that may be read
@@ -51,8 +68,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(i32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 // Row exchanges between the four 16-lane rows of a wave: permlane32_swap(a, b) gives
 // ([a0 a1 b0 b1], [a2 a3 b2 b3]) and permlane16_swap(a, b) gives ([a0 b0 a2 b2], [a1 b1 a3 b3]),
@@ -80,183 +95,327 @@ __device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
            (unsigned(__builtin_bit_cast(uint16_t, static_cast<__bf16>(hi))) << 16);
 }
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// Stage a chunk's cache rows into LDS with buffer loads that write LDS directly (no registers):
-// one instruction moves 64 x 16 bytes into consecutive LDS slots, lane l into slot l.  The
-// chunk is viewed as CH rows of cpr + 1 slots (one slot of padding per row); slot s of the
-// chunk holds piece (s / (cpr + 1), s % (cpr + 1)) of the rows c0 .. c0 + CH - 1, and padding
-// slots and positions past the span read zeros.  Wave w issues instructions w, w + 4, ...
-template <int CH, int SPR>
-__device__ __forceinline__ void stage_chunk(uint16_t* buf, __amdgpu_buffer_rsrc_t kvr, const AttnParams& p, int c0,
-                                            int s_end, int wave, int lane) {
-    const int spr = SPR ? SPR : p.cols / 8 + 1;   // slots per row (a constant for the fixed shape)
-    const int slots = CH * spr;
-    for (int ins = wave; ins * 64 < slots; ins += 4) {
-        const int sl = ins * 64 + lane;
-        const int row = sl / spr, c = sl - row * spr;
-        const bool ok = c < spr - 1 && c0 + row < s_end;
-        const uint32_t off = ok ? uint32_t((int64_t(c0 + row) * p.ldkv + 8 * c) * 2) : kOutOfRange;
-        if (sl < slots)
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(kvr, (lds_void*)(buf + ins * 64 * 8), 16, off, 0, 0, 0);
+// Staging a chunk's cache rows into LDS: buffer loads that write LDS directly (no registers), one
+// instruction moving 64 x 16 bytes into consecutive LDS slots, lane l into slot l.  A chunk is
+// kCh rows of spr slots (cols / 8 data slots, then kPadSlots of padding), so instruction i covers
+// slots 64 i .. 64 i + 63 and a chunk takes spr instructions; wave w of W issues i = w, w + W, ...
+// stage_offsets computes once where each of this lane's slots lies in the cache relative to the
+// chunk's first row (padding slots get an offset past any extent, so they read zeros); the chunk's
+// row offset is added at issue.  Rows past the cache end fall outside the buffer's range and read
+// zeros; a span's chunks never cross into the next span (spans are whole chunks).
+template <int W>
+struct Stage {
+    static constexpr int kIns = (kPitchMax / 8 + W - 1) / W;   // instructions per wave
+    uint32_t off[kIns];
+    __device__ __forceinline__ void init(int spr, int64_t ldkv, int wave, int lane) {
+#pragma unroll
+        for (int k = 0; k < kIns; ++k) {
+            const int ins = wave + W * k;
+            const int sl = ins * 64 + lane;
+            const int row = sl / spr, c = sl - row * spr;
+            off[k] = (ins < spr && c < spr - kPadSlots) ? uint32_t((int64_t(row) * ldkv + 8 * c) * 2) : kOutOfRange;
+        }
     }
+    __device__ __forceinline__ void piece(uint16_t* buf, __amdgpu_buffer_rsrc_t kvr, int k, int spr, uint32_t row_off,
+                                          int wave) const {
+        const int ins = wave + W * k;
+        if (k < kIns && ins < spr)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(kvr, (lds_void*)(buf + ins * 64 * 8), 16, off[k] + row_off, 0, 0, 0);
+    }
+};
+
+// A workgroup barrier for the LDS exchanges inside a chunk: this wave's LDS operations complete
+// (lgkmcnt), then the barrier.  A fenced barrier (__syncthreads, or a fence on LDS alone) would
+// also wait for the next chunk's staging loads, which write LDS through the vector memory counter,
+// and so serialise the prefetch with the chunk; those loads target the other chunk buffer, which
+// nothing reads before the end-of-chunk barrier waits for them.  The asm's memory clobber keeps
+// the compiler from moving memory operations across it.
+__device__ __forceinline__ void lds_sync() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// One workgroup of the attention launch: workgroup `bid` of n_hb * nsp (head block, span).  CH
-// positions per chunk, KS = d_qk / 32 k-steps and NT = d_v / 16 output tiles (upper bounds;
-// EXACT: the shape matches them, so no step is skipped at run time), PMAX the largest row
-// pitch (elements) the launch may use.  The two chunk buffers are separate LDS arrays and the
-// chunk loop is unrolled by two, so that every LDS read names the buffer that is not being
-// filled -- the compiler then need not wait for the filling loads before reading.
-// The two chunk buffers of CH * PMAX elements (one LDS array each; every kernel that calls these
-// gets the same two arrays, so a kernel whose workgroups do other work can use them as well).
-template <int CH, int PMAX>
+// LDS of the attention workgroup.  Every kernel that calls these gets the same arrays, so a kernel
+// whose other workgroups do other work (the GEMV beside attention) can use them as well.
 __device__ __forceinline__ uint16_t* chunk_buffer_a() {
-    __shared__ __attribute__((aligned(16))) uint16_t kv_a[CH * PMAX];
+    __shared__ __attribute__((aligned(16))) uint16_t kv_a[kCh * kPitchMax];
     return kv_a;
 }
-template <int CH, int PMAX>
 __device__ __forceinline__ uint16_t* chunk_buffer_b() {
-    __shared__ __attribute__((aligned(16))) uint16_t kv_b[CH * PMAX];
+    __shared__ __attribute__((aligned(16))) uint16_t kv_b[kCh * kPitchMax];
     return kv_b;
 }
+__device__ __forceinline__ uint16_t* p_buffer() {
+    __shared__ __attribute__((aligned(16))) uint16_t pb[kMaxHt * 16 * kPPitch];
+    return pb;
+}
+__device__ __forceinline__ float* red_buffer() {
+    __shared__ __attribute__((aligned(16))) float red[4 * kMaxHt * 16];
+    return red;
+}
+__device__ __forceinline__ int* flag_buffer() {
+    __shared__ int flags[8];
+    return flags;
+}
 
-template <int CH, int KS, int NT, int PMAX, bool EXACT>
+// The (head block, span) of workgroup `bid`; false for the padding workgroups of an XCD-grouped
+// grid.  With xcd_map the workgroups of one span (every head block) are 8 ids apart, so they run
+// on one XCD and its L2 serves the span's cache rows to all of them.
+__device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int* hb, int* sp) {
+    if (p.xcd_map) {
+        *sp = (bid & 7) + 8 * (bid / (8 * p.n_hb));
+        *hb = (bid >> 3) % p.n_hb;
+        return *sp < p.nsp;
+    }
+    *hb = bid % p.n_hb;
+    *sp = bid / p.n_hb;
+    return true;
+}
+
+// One workgroup of the attention launch: HT * 16 heads (head block hb) over one span of positions,
+// with W = 4 or 8 waves.  Wave w has position group pw = w % 4 and head group hg = w / 4; with 4
+// waves a wave covers all HT head tiles, with 8 waves (two per SIMD, so that one wave's latency is
+// covered by the other's work) each wave covers HT / 2 of them.
+//  * Q.K^T: a wave computes the scores of positions 16 pw .. + 15 of each 64-position chunk for its
+//    head tiles (S^T = K . Q^T on the matrix cores, K fragments read from LDS and used for each of
+//    the wave's head tiles; Q held in registers as MFMA fragments).
+//  * softmax: each wave writes P = 2^(s - reference), rounded to bf16, against the running
+//    reference of each head, and posts its maxima.  Only when some wave's maximum exceeds a
+//    reference by more than kLazyTh (always on a span's first chunk, rarely after) do the waves
+//    take the chunk maximum, move the reference, rescale the output and write P again.  So
+//    P <= 2^kLazyTh.
+//  * P.V: a wave accumulates the output columns of tiles pw, pw + 4, ... for its head tiles
+//    (O^T = V^T . P^T, V^T fragments by ds_read_b64_tr_b16 from the same staged rows).
+//  * The result goes through LDS so that each store instruction writes 1 KB of one row.
+// KS = d_qk / 32 and NTW = column tiles per position group are upper bounds; EXACT: the shape
+// matches them.
+template <int HT, int W, int KS, int NTW, bool EXACT>
 __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
-    uint16_t* const kv_a = chunk_buffer_a<CH, PMAX>();
-    uint16_t* const kv_b = chunk_buffer_b<CH, PMAX>();
-    constexpr int SPR = EXACT ? (KS * 32 > NT * 16 ? KS * 32 : NT * 16) / 8 + 1 : 0;   // LDS slots per row
-    constexpr int CT = CH / 16;            // score tiles per chunk
-    constexpr int PK = CH / 32;            // P.V k-steps per chunk
+    constexpr int HB = 16 * HT;
+    constexpr int HTW = HT * 4 / W;            // head tiles per wave
+    static_assert((W == 4 || W == 8) && HTW >= 1 && HTW * W == 4 * HT, "4 or 8 waves over whole head tiles");
+    uint16_t* const kv_a = chunk_buffer_a();
+    uint16_t* const kv_b = chunk_buffer_b();
+    uint16_t* const pbuf = p_buffer();
+    float* const red = red_buffer();
+    int* const flags = flag_buffer();
 
     const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (W - 1);   // (the mask bounds it for the compiler)
+    const int pw = wave & 3, ht0 = (wave >> 2) * HTW;
     const int g = lane >> 4, j = lane & 15;
     const int ksteps = EXACT ? KS : p.dqk / 32;
-    const int ntiles = EXACT ? NT : p.dv / 16;
+    const int ntiles = EXACT ? 4 * NTW : p.dv / 16;
+    const int pitch = EXACT ? kPitchMax : p.pitch;
+    const int spr = pitch / 8;
+    const uint32_t row_bytes = uint32_t(p.ldkv) * 2;
 
     int hb, sp;
-    if (p.xcd_map) {
-        sp = (bid & 7) + 8 * (bid / (8 * p.n_hb));
-        hb = (bid >> 3) % p.n_hb;
-        if (sp >= p.nsp) return;    // padding of the grid to whole groups of 8 spans
-    } else {
-        hb = bid % p.n_hb;
-        sp = bid / p.n_hb;
-    }
-    const int hw = hb * kHB + 16 * wave;   // this wave's first head
+    if (!block_of(p, bid, &hb, &sp)) return;
+    const int h0 = hb * HB;
     const int s_begin = sp * p.span;
     const int s_end = min(p.seq, s_begin + p.span);
-    const int nchunks = (s_end - s_begin + CH - 1) / CH;
+    const int nchunks = (s_end - s_begin + kCh - 1) / kCh;
 
     const __amdgpu_buffer_rsrc_t kvr = make_rsrc(p.kv, p.kv_extent);
-    // ---- this wave's Q rows as A fragments (row j, dims 32u + 8g .. +7); heads past the end
-    // read zeros.  Then the first chunk goes to LDS.
-    i32x4 qf[KS];
+    Stage<W> stg;
+    stg.init(spr, p.ldkv, wave, lane);
+    // ---- the first chunk to buffer a and the block's Q rows to buffer b (LDS-direct loads of whole
+    // row pieces: fragment-shaped global loads, 16 rows x 64 bytes per instruction, ingest about
+    // four times slower).  Q rows past the last head and pieces past d_qk read zeros.
+#pragma unroll
+    for (int k = 0; k < Stage<W>::kIns; ++k) stg.piece(kv_a, kvr, k, spr, uint32_t(s_begin) * row_bytes, wave);
     {
         const __amdgpu_buffer_rsrc_t qr = make_rsrc(p.q, p.q_extent);
-        const bool ok = hw + j < p.heads;
-        const uint32_t base = uint32_t((int64_t(hw + j) * p.ldq + 8 * g) * 2);
-#pragma unroll
-        for (int u = 0; u < KS; ++u)
-            qf[u] = __builtin_amdgcn_raw_buffer_load_b128(qr, (ok && u < ksteps) ? base + 64 * u : kOutOfRange, 0, 0);
+        const int qcols = ksteps * 4;                  // 16-byte pieces of a Q row that are read
+        for (int ins = wave; ins * 64 < HB * spr; ins += W) {
+            const int sl = ins * 64 + lane;
+            const int row = sl / spr, c = sl - row * spr;
+            const bool ok = c < qcols && h0 + row < p.heads;
+            const uint32_t off = ok ? uint32_t((int64_t(h0 + row) * p.ldq + 8 * c) * 2) : kOutOfRange;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(qr, (lds_void*)(kv_b + ins * 64 * 8), 16, off, 0, 0, 0);
+        }
     }
-    stage_chunk<CH, SPR>(kv_a, kvr, p, s_begin, s_end, wave, lane);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-
-    f32x4 o[NT];                            // O^T tiles: lane (g, j) holds columns 16t + 4g + i of head j
+    // the Q fragments of the wave's head tiles: head 16 (ht0 + t) + j, dims 32 u + 8 g .. + 7; then
+    // buffer b is free for chunk 1
+    i32x4 qf[HTW][KS];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;   // this lane's head (column j), in log2 units
+    for (int t = 0; t < HTW; ++t)
+#pragma unroll
+        for (int u = 0; u < KS; ++u)
+            if (EXACT || u < ksteps)
+                qf[t][u] = *reinterpret_cast<const i32x4*>(kv_b + (16 * (ht0 + t) + j) * pitch + 8 * g + 32 * u);
+    lds_sync();
+
+    f32x4 o[NTW][HTW];      // O^T tiles: lane (g, j) holds columns 16 ct + 4 g .. + 3 of head 16 (ht0 + t) + j
+#pragma unroll
+    for (int i = 0; i < NTW; ++i)
+#pragma unroll
+        for (int t = 0; t < HTW; ++t) o[i][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_ref[HTW], l_acc[HTW];   // the head's reference maximum (log2 units); this lane's sum of P
+#pragma unroll
+    for (int t = 0; t < HTW; ++t) {
+        m_ref[t] = -INFINITY;
+        l_acc[t] = 0.f;
+    }
     const int a4 = j >> 2, b4 = j & 3;
 
-    // one chunk: computed from `cur`; the next chunk streams into `nxt` meanwhile
     auto chunk = [&](const uint16_t* cur, uint16_t* nxt, int ck) {
-        const int c0 = s_begin + ck * CH;
+        const int c0 = s_begin + ck * kCh;
+        // the next chunk streams into the other buffer while this one is computed (every wave
+        // finished reading that buffer before the last barrier); its loads are issued one per
+        // Q.K^T step, so their issue overlaps the MFMAs instead of stalling the wave
+        const bool stage_next = ck + 1 < nchunks;
+        const uint32_t next_off = uint32_t(c0 + kCh) * row_bytes;
 
-        // ---- S^T[CH positions][16 heads] = K . Q^T: lane (g, j) gets positions 16t + 4g + i of
-        // head j.  The K fragments of step u + 1 are read while step u multiplies.
-        f32x4 s[CT];
+        // ---- S^T[16 positions][16 heads] per head tile; two accumulators per tile (even and odd
+        // k-steps) keep two independent MFMA chains per tile in flight.  K fragments are read kKw
+        // k-steps ahead: step u's MFMAs consume slot u % kKw, whose register then takes the read
+        // of step u + kKw (kept next to them by a scheduling barrier), so LDS latency overlaps the
+        // MFMAs instead of stalling every step.
+        f32x4 s[HTW][2];
 #pragma unroll
-        for (int t = 0; t < CT; ++t) s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const uint16_t* krow = cur + j * p.pitch + 8 * g;
-        i32x4 kf[2][CT];
+        for (int t = 0; t < HTW; ++t) s[t][0] = s[t][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const uint16_t* krow = cur + (16 * pw + j) * pitch + 8 * g;
+        i32x4 kf[kKw];
 #pragma unroll
-        for (int t = 0; t < CT; ++t) kf[0][t] = *reinterpret_cast<const i32x4*>(krow + 16 * t * p.pitch);
+        for (int u = 0; u < kKw; ++u)
+            if (u < KS && (EXACT || u < ksteps)) kf[u] = *reinterpret_cast<const i32x4*>(krow + 32 * u);
 #pragma unroll
         for (int u = 0; u < KS; ++u) {
             if (EXACT || u < ksteps) {
-                if (u + 1 < KS && (EXACT || u + 1 < ksteps)) {
 #pragma unroll
-                    for (int t = 0; t < CT; ++t)
-                        kf[(u + 1) & 1][t] = *reinterpret_cast<const i32x4*>(krow + 16 * t * p.pitch + 32 * (u + 1));
+                for (int t = 0; t < HTW; ++t)
+                    s[t][u & 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[u % kKw]), as_bf16x8(qf[t][u]),
+                                                                        s[t][u & 1], 0, 0, 0);
+                if (u + kKw < KS && (EXACT || u + kKw < ksteps))
+                    kf[u % kKw] = *reinterpret_cast<const i32x4*>(krow + 32 * (u + kKw));
+                if (stage_next) stg.piece(nxt, kvr, u, spr, next_off, wave);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        // the staging pieces the Q.K^T steps did not issue
+        if (stage_next) {
+#pragma unroll
+            for (int k = 0; k < Stage<W>::kIns; ++k)
+                if (k >= KS || (!EXACT && k >= ksteps)) stg.piece(nxt, kvr, k, spr, next_off, wave);
+        }
+
+        // ---- scores in log2 units (positions past the span masked) and this wave's maximum per
+        // head over its 16 positions
+        const int pos0 = c0 + 16 * pw + 4 * g;
+        float mx[HTW];
+        bool need = false;
+#pragma unroll
+        for (int t = 0; t < HTW; ++t) {
+            mx[t] = -INFINITY;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float v = (pos0 + i < s_end) ? (s[t][0][i] + s[t][1][i]) * p.scale_log2 : -INFINITY;
+                s[t][0][i] = v;
+                mx[t] = fmaxf(mx[t], v);
+            }
+            mx[t] = cols4_max(mx[t]);
+            need |= !(mx[t] <= m_ref[t] + kLazyTh);
+        }
+        // ---- P = 2^(s - reference), rounded to bf16, to LDS as P[head][position]
+        float lc[HTW];
+        auto write_p = [&]() {
+#pragma unroll
+            for (int t = 0; t < HTW; ++t) {
+                float pv[4];
+                lc[t] = 0.f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float v = s[t][0][i];
+                    pv[i] = (v == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(v - m_ref[t]);
+                    lc[t] += pv[i];
                 }
+                *reinterpret_cast<uint2*>(pbuf + (16 * (ht0 + t) + j) * kPPitch + 16 * pw + 4 * g) =
+                    uint2{pack_bf16(pv[0], pv[1]), pack_bf16(pv[2], pv[3])};
+            }
+        };
+        // every wave posts its maxima and whether any moved past its reference by more than kLazyTh
+        if (g == 0) {
 #pragma unroll
-                for (int t = 0; t < CT; ++t)
-                    s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kf[u & 1][t]), as_bf16x8(qf[u]), s[t], 0, 0, 0);
+            for (int t = 0; t < HTW; ++t) red[pw * HB + 16 * (ht0 + t) + j] = mx[t];
+        }
+        if (ck > 0) {
+            write_p();
+            const bool wave_needs = __builtin_amdgcn_ballot_w64(need) != 0;
+            if (lane == 0) flags[wave] = wave_needs ? 1 : 0;
+            lds_sync();
+        } else {
+            lds_sync();   // a span's first chunk always sets the references
+        }
+        bool any = ck == 0;
+        if (ck > 0) {
+#pragma unroll
+            for (int w = 0; w < W; ++w) any |= flags[w] != 0;
+        }
+        // ---- a reference moves (the same decision in every wave: all read the same maxima): the
+        // chunk maximum of each head, the output rescaled, and P written again
+        if (any) {
+            bool resc = false;
+            float alpha[HTW];
+#pragma unroll
+            for (int t = 0; t < HTW; ++t) {
+                const int hh = 16 * (ht0 + t) + j;
+                const float mc = fmaxf(fmaxf(red[hh], red[HB + hh]), fmaxf(red[2 * HB + hh], red[3 * HB + hh]));
+                alpha[t] = 1.f;
+                if (mc > m_ref[t] + kLazyTh) {
+                    alpha[t] = (m_ref[t] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_ref[t] - mc);
+                    m_ref[t] = mc;
+                    l_acc[t] *= alpha[t];
+                    resc = true;
+                }
+            }
+            if (__builtin_amdgcn_ballot_w64(resc)) {
+#pragma unroll
+                for (int i = 0; i < NTW; ++i)
+#pragma unroll
+                    for (int t = 0; t < HTW; ++t) o[i][t] *= alpha[t];
+            }
+            write_p();
+            lds_sync();
+        }
+#pragma unroll
+        for (int t = 0; t < HTW; ++t) l_acc[t] += lc[t];
+
+        // ---- O^T += V^T . P^T over the chunk's two 32-position k-steps
+#pragma unroll
+        for (int kk = 0; kk < kCh / 32; ++kk) {
+            i32x4 pf[HTW];
+#pragma unroll
+            for (int t = 0; t < HTW; ++t)
+                pf[t] = *reinterpret_cast<const i32x4*>(pbuf + (16 * (ht0 + t) + j) * kPPitch + 32 * kk + 8 * g);
+            const uint16_t* vrow = cur + (32 * kk + 8 * g + a4) * pitch + 4 * b4;
+            i32x4 vf[NTW];
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) {
+                const int ct = pw + 4 * i;
+                if (EXACT || ct < ntiles) {
+                    const uint16_t* base = vrow + 16 * ct;
+                    const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base));
+                    const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + 4 * pitch));
+                    const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
+                    vf[i] = i32x4{int(ulo.x), int(ulo.y), int(uhi.x), int(uhi.y)};
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) {
+                const int ct = pw + 4 * i;
+                if (EXACT || ct < ntiles) {
+#pragma unroll
+                    for (int t = 0; t < HTW; ++t)
+                        o[i][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vf[i]), as_bf16x8(pf[t]), o[i][t], 0, 0, 0);
+                }
             }
         }
 
-        // the next chunk's rows stream into the other buffer during the softmax and P.V (every
-        // wave finished reading that buffer before the last barrier)
-        if (ck + 1 < nchunks) stage_chunk<CH, SPR>(nxt, kvr, p, c0 + CH, s_end, wave, lane);
-
-        // ---- online softmax of head j over the chunk
-        float mx = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < CT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                s[t][i] = (c0 + 16 * t + 4 * g + i < s_end) ? s[t][i] * p.scale_log2 : -INFINITY;
-                mx = fmaxf(mx, s[t][i]);
-            }
-        const float m_new = fmaxf(m_run, cols4_max(mx));
-        const float alpha = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-        float sum = 0.f;
-#pragma unroll
-        for (int t = 0; t < CT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                s[t][i] = (s[t][i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(s[t][i] - m_new);
-                sum += s[t][i];
-            }
-        l_run = alpha * l_run + cols4_sum(sum);
-        m_run = m_new;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) o[t] *= alpha;
-
-        // ---- O^T += V^T . P^T.  The B operand of k-step kk (positions 32kk + 8g + e of head j)
-        // is tiles 2kk and 2kk + 1 of P, rounded to bf16 and moved between rows by two swaps;
-        // tile t + 1's V^T fragment is read while tile t multiplies.
-#pragma unroll
-        for (int kk = 0; kk < PK; ++kk) {
-            const f32x4 p0 = s[2 * kk], p1 = s[2 * kk + 1];
-            const u32x2 x0 = swap32(pack_bf16(p0[0], p0[1]), pack_bf16(p1[0], p1[1]));
-            const u32x2 x1 = swap32(pack_bf16(p0[2], p0[3]), pack_bf16(p1[2], p1[3]));
-            const u32x2 y0 = swap16(x0[0], x0[1]);
-            const u32x2 y1 = swap16(x1[0], x1[1]);
-            const i32x4 pb = i32x4{int(y0[0]), int(y1[0]), int(y0[1]), int(y1[1])};
-            const uint16_t* vrow = cur + (32 * kk + 8 * g + a4) * p.pitch + 4 * b4;
-            auto vfrag = [&](int t) {
-                const uint16_t* base = vrow + 16 * t;
-                const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base));
-                const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + 4 * p.pitch));
-                const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
-                return i32x4{int(ulo.x), int(ulo.y), int(uhi.x), int(uhi.y)};
-            };
-            i32x4 vb[2];
-            vb[0] = vfrag(0);
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                if (EXACT || t < ntiles) {
-                    if (t + 1 < NT && (EXACT || t + 1 < ntiles)) vb[(t + 1) & 1] = vfrag(t + 1);
-                    o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vb[t & 1]), as_bf16x8(pb), o[t], 0, 0, 0);
-                }
-            }
-        }
-
-        // ---- the next chunk must have landed in LDS (this wave's loads, then every wave's)
+        // ---- the next chunk must have landed (this wave's loads, then every wave's), and every
+        // wave must be done with this chunk's rows and P
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     };
@@ -265,45 +424,72 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
         if (ck + 1 < nchunks) chunk(kv_b, kv_a, ck + 1);
     }
 
-    // ---- this span's result: lane (g, j) holds columns 16t + 4g .. +3 of head hw + j
-    const int h = hw + j;
-    if (p.nsp == 1) {
-        if (h < p.heads) {
-            const float inv = 1.f / l_run;
+    // ---- the span's probability sums: this lane's positions, the wave's four rows, then the
+    // four position groups in order
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
-                if (EXACT || t < ntiles) {
-                    const f32x4 r = o[t] * inv;
-                    *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + 16 * t + 4 * g) = r;
-                    if (p.outb) {
-                        uint16_t* ob = p.outb + int64_t(h) * p.ldob + 16 * t + 4 * g;
-                        ob[0] = to_bf16_bits(r[0]);
-                        ob[1] = to_bf16_bits(r[1]);
-                        ob[2] = to_bf16_bits(r[2]);
-                        ob[3] = to_bf16_bits(r[3]);
-                    }
-                }
+    for (int t = 0; t < HTW; ++t) {
+        const float lw = cols4_sum(l_acc[t]);
+        if (g == 0) red[pw * HB + 16 * (ht0 + t) + j] = lw;
+    }
+    __syncthreads();
+    float lsum[HTW];
+#pragma unroll
+    for (int t = 0; t < HTW; ++t) {
+        const int hh = 16 * (ht0 + t) + j;
+        lsum[t] = ((red[hh] + red[HB + hh]) + red[2 * HB + hh]) + red[3 * HB + hh];
+    }
+
+    // ---- the block's [HB][d_v] result into LDS (buffer a, free after the last chunk; rows padded
+    // by 4 floats to spread the banks), normalised when the span is the whole sequence
+    const int dvp = p.dv + 4;
+    float* const ob = reinterpret_cast<float*>(kv_a);
+    const bool whole = p.nsp == 1;
+#pragma unroll
+    for (int t = 0; t < HTW; ++t) {
+        const float scl = whole ? 1.f / lsum[t] : 1.f;
+#pragma unroll
+        for (int i = 0; i < NTW; ++i) {
+            const int ct = pw + 4 * i;
+            if (EXACT || ct < ntiles)
+                *reinterpret_cast<f32x4*>(ob + (16 * (ht0 + t) + j) * dvp + 16 * ct + 4 * g) = o[i][t] * scl;
         }
-        return;
     }
     const int64_t pidx = int64_t(hb) * p.nsp + sp;
-    float* po = p.part_o + (pidx * kHB + 16 * wave + j) * int64_t(p.dv);
+    if (!whole && pw == 0 && g == 0) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t)
-        if (EXACT || t < ntiles) *reinterpret_cast<f32x4*>(po + 16 * t + 4 * g) = o[t];
-    if (g == 0) {
-        float* pml = p.part_ml + (pidx * kHB + 16 * wave + j) * 2;
-        pml[0] = m_run;
-        pml[1] = l_run;
+        for (int t = 0; t < HTW; ++t) {
+            float* pml = p.part_ml + (pidx * HB + 16 * (ht0 + t) + j) * 2;
+            *reinterpret_cast<float2*>(pml) = float2{m_ref[t], lsum[t]};
+        }
+    }
+    __syncthreads();
+    // ---- rows out: each store instruction writes 1 KB of one row
+    const int c4 = p.dv / 4;                         // 16-byte pieces per row
+    for (int idx = tid; idx < HB * c4; idx += 64 * W) {
+        const int row = idx / c4, c = idx - row * c4;
+        const int h = h0 + row;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(ob + row * dvp + 4 * c);
+        if (whole) {
+            if (h < p.heads) {
+                *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + 4 * c) = v;
+                if (p.outb) {
+                    uint16_t* d = p.outb + int64_t(h) * p.ldob + 4 * c;
+                    d[0] = to_bf16_bits(v[0]);
+                    d[1] = to_bf16_bits(v[1]);
+                    d[2] = to_bf16_bits(v[2]);
+                    d[3] = to_bf16_bits(v[3]);
+                }
+            }
+        } else {
+            *reinterpret_cast<f32x4*>(p.part_o + (pidx * HB + row) * int64_t(p.dv) + 4 * c) = v;
+        }
     }
 }
 
 // A prepared attention call: kernel arguments, the attention grid (0: nothing to launch), the
 // merge grid (0: one span, no merge) and the kernel variant.
-constexpr int kAttnExact64 = 1;     // d_qk 576, d_v 512, 64-position chunks
-constexpr int kAttnExact32 = 2;     // the same shape, 32-position chunks
-constexpr int kAttnGeneral64 = 3;
-constexpr int kAttnGeneral32 = 4;
+constexpr int kAttnExact = 1;      // d_qk 576, d_v 512
+constexpr int kAttnGeneral = 2;    // d_qk <= 576, d_v <= 512
 struct AttnLaunch {
     AttnParams p{};
     int64_t grid = 0;

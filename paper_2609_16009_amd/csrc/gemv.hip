@@ -506,17 +506,18 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
 // Section III-A); here the overlap is fixed by the launch itself -- the GEMV's workgroups stream
 // the weight while attention's run on the compute units the GEMV leaves free -- instead of
 // depending on how two streams are scheduled.
-constexpr int kAttnCh = 64, kAttnPitch = 584;
 static_assert(kThreads == attn::kAThreads, "the two kinds of workgroup have the same size");
+static_assert(size_t(attn::kCh) * attn::kPitchMax * 2 >= size_t(kXStageBytes) && size_t(attn::kCh) * attn::kPitchMax * 2 >= size_t(kRedBytes),
+              "the GEMV's x slice and reduction fit the first chunk buffer");
 template <int U>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemv_attention_kernel(const KParams p, const attn::AttnParams a, uint32_t gemv_grid) {
     __shared__ int s_last;
     if (blockIdx.x < gemv_grid) {
-        float* lds = reinterpret_cast<float*>(attn::chunk_buffer_a<kAttnCh, kAttnPitch>());
+        float* lds = reinterpret_cast<float*>(attn::chunk_buffer_a());
         gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
     } else {
-        attn::attention_block<kAttnCh, 18, 32, kAttnPitch, true>(a, static_cast<int>(blockIdx.x - gemv_grid));
+        attn::attention_block<attn::kHt, 4, attn::kMaxKs, attn::kMaxNtw, true>(a, static_cast<int>(blockIdx.x - gemv_grid));
     }
 }
 
@@ -1241,10 +1242,10 @@ nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned
     nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
     if (st != NMM_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool fuse = al.grid > 0 && al.variant == attn::kAttnExact64 && al.p.pitch <= kAttnPitch &&
+    const bool fuse = al.grid > 0 && al.variant == attn::kAttnExact && al.p.pitch <= attn::kPitchMax &&
                       g.dt == NMM_BF16 && g.batch == 1 && g.M == 1 && g.K > 0 && g.N > 0 && g.y && gp.mt == 1 &&
                       (gp.unroll == 8 || gp.unroll == 16) &&
-                      gemv_lds_bytes(gp) <= size_t(kAttnCh) * kAttnPitch * 2 && gp.grid + al.grid < (int64_t(1) << 31);
+                      gemv_lds_bytes(gp) <= size_t(attn::kCh) * attn::kPitchMax * 2 && gp.grid + al.grid < (int64_t(1) << 31);
     if (!fuse) {
         st = launch_gemv(g, gp, tickets, part, stream);
         if (st != NMM_OK) return st;

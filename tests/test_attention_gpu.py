@@ -37,13 +37,35 @@ def test_decode_step_attention_full_size():
     check(q, kv, scale, 576, 512, "attention 128x4096x576/512")
 
 
-@pytest.mark.parametrize("splits,chunk", [("1", "64"), ("8", "32"), ("8", "64"), ("64", "32"), ("64", "64"), ("21", "64")])
-def test_decode_step_attention_every_partition(monkeypatch, splits, chunk):
-    # the span count and chunk size change the summation order, never the result beyond tolerance
-    monkeypatch.setenv("NMM_ATTN_SPLITS", splits)
-    monkeypatch.setenv("NMM_ATTN_CHUNK", chunk)
+@pytest.mark.parametrize("splits", [1, 8, 16, 21, 64])
+def test_decode_step_attention_every_partition(splits):
+    # the span count changes the summation order, never the result beyond tolerance
     q, kv, scale = syn.attention_case(14, 128, 4096)
-    check(q, kv, scale, 576, 512, f"attention 128x4096, {splits} spans, {chunk}-position chunks")
+    out = torch.full((128, 512), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, scale, splits=splits)
+    torch.cuda.synchronize()
+    ref, ref_abs = oracle.latent_attention(q, kv, scale)
+    assert_parity(out, ref, ref_abs, what=f"attention 128x4096, {splits} spans")
+
+
+@pytest.mark.parametrize("splits", [1, 4])
+def test_attention_rising_scores_rescale_every_chunk(splits):
+    # scores that grow along the cache: each 64-position chunk's maximum exceeds the running one by
+    # far more than the lazy-rescale threshold, so the running output is rescaled at every chunk
+    rng = np.random.default_rng(77)
+    heads, seq, dqk, dv = 40, 700, 576, 512
+    qf = rng.standard_normal((heads, dqk), dtype=np.float32)
+    u = np.sign(rng.standard_normal(dqk)).astype(np.float32)
+    qf[:, :] = np.abs(qf) * u                       # every head leans towards u
+    t = np.linspace(0.0, 3.0, seq, dtype=np.float32)
+    kvf = rng.standard_normal((seq, dqk), dtype=np.float32) * 0.5 + t[:, None] * u[None, :]
+    q, kv = syn.bits_from_f32(qf, syn.BF16), syn.bits_from_f32(kvf, syn.BF16)
+    scale = 0.05
+    out = torch.full((heads, dv), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, scale, splits=splits, d_v=dv)
+    torch.cuda.synchronize()
+    ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=dqk, dv=dv)
+    assert_parity(out, ref, ref_abs, what=f"rising scores, {splits} spans")
 
 
 @pytest.mark.parametrize("heads,seq,dqk,dv,ldkv", [
@@ -78,6 +100,7 @@ def test_attention_rejects_bad_arguments():
                                             a["ldkv"], a["scale"], a["out"], a["ldo"], None, 0, s)
     assert call(args(seq=0)) == nmm.NMM_ERR_SHAPE
     assert call(args(dqk=100)) == nmm.NMM_ERR_SHAPE
+    assert call(args(dqk=608, ldq=608, ldkv=608)) == nmm.NMM_ERR_SHAPE   # d_qk above 576
     assert call(args(dv=520)) == nmm.NMM_ERR_SHAPE
     assert call(args(scale=float("inf"))) == nmm.NMM_ERR_ARG
     assert call(args(q=None)) == nmm.NMM_ERR_NULL
