@@ -27,7 +27,7 @@ import sys
 import time
 
 
-ATTN_OVERLAP_SPLITS = 12
+ATTN_OVERLAP_SPLITS = 8
 
 
 def mean_gain(t_opt: float, t_base: float) -> float:
