@@ -99,6 +99,24 @@ nmm_status nmm_gemv(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
                     void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * nmm_gemv_noalloc -- nmm_gemv without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that forbid it).  It
+ * allocates nothing on any call: the split-K counters and partial sums live in a scratch array of
+ * NMM_NOALLOC_SCRATCH_BYTES in the library's device code, one per GPU, held until the process
+ * ends.  Its counters are zeroed by a fill kernel on `stream` at the first call on each device and
+ * every launch leaves them at zero.  Same arguments, rules and results as nmm_gemv (the same plan
+ * and kernels, so the same bits); NMM_ERR_WORKSPACE when the plan needs more scratch than the
+ * array holds (nmm_gemv_workspace_size(M, K, N, dt, path) > NMM_NOALLOC_SCRATCH_BYTES, e.g. the
+ * streaming path at 16 rows of a [16384, 7168] weight), before anything is enqueued.  All calls
+ * on one GPU share its array: calls that may overlap on one GPU (other streams, other host
+ * threads) race and must not be made.
+ */
+#define NMM_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+nmm_status nmm_gemv_noalloc(int64_t M, int64_t K, int64_t N, nmm_dtype dt,
+                            const void* x, int64_t ldx, const void* W, int64_t ldw,
+                            float* y, int64_t ldy, nmm_path path, void* stream);
+
+/*
  * nmm_batched_gemv -- for b < batch: y_b = x_b . W_b with
  *   x_b = x + b*stride_x,  W_b = W + b*stride_w,  y_b = y + b*stride_y   (strides in elements).
  * The per-head absorbed MLA matmuls (q_nope . W_UK and latent . W_UV, one W per head).  Same

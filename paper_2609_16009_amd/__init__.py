@@ -22,6 +22,7 @@ NMM_OK, NMM_ERR_NULL, NMM_ERR_SHAPE, NMM_ERR_DTYPE, NMM_ERR_ALIGN, NMM_ERR_WORKS
 NMM_F16, NMM_BF16 = 1, 2
 NMM_PATH_AUTO, NMM_PATH_GEMV, NMM_PATH_MFMA = 0, 1, 2
 NMM_ROUND_EVEN, NMM_ROUND_AWAY = 0, 1
+NMM_NOALLOC_SCRATCH_BYTES = 8 << 20   # nmm_gemv_noalloc's scratch per GPU
 
 _i64 = ctypes.c_int64
 _p = ctypes.c_void_p
@@ -83,6 +84,7 @@ class nmm_mla_query_path(ctypes.Structure):
 EXPORTS = {
     "nmm_gemv": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
                                 ctypes.c_int, _p, _sz, _p]),
+    "nmm_gemv_noalloc": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64, ctypes.c_int, _p]),
     "nmm_batched_gemv": (ctypes.c_int, [_i64, _i64, _i64, _i64, ctypes.c_int, _p, _i64, _i64, _p,
                                         _i64, _i64, _p, _i64, _i64, ctypes.c_int, _p, _sz, _p]),
     "nmm_gemv_bf16": (ctypes.c_int, [_i64, _i64, _i64, ctypes.c_int, _p, _i64, _p, _i64, _p, _i64,
@@ -209,6 +211,17 @@ def nmm_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None
     wp, wb = _workspace(workspace, need, x.device)
     _check(lib().nmm_gemv(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y.data_ptr(),
                           _ld(y), path, wp, wb, _stream(stream)), "nmm_gemv")
+    return y
+
+
+def nmm_gemv_noalloc(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None = None,
+                     path: int = NMM_PATH_AUTO, dt: int | None = None, stream=None) -> torch.Tensor:
+    """nmm_gemv with the library's own scratch instead of a workspace (allocates nothing)."""
+    code = _dtype_code(x, dt)
+    M, K = x.shape[0], W.shape[0]
+    N = W.shape[1] if N is None else N
+    _check(lib().nmm_gemv_noalloc(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y.data_ptr(), _ld(y),
+                                  path, _stream(stream)), "nmm_gemv_noalloc")
     return y
 
 

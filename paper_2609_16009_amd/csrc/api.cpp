@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 #include "nmm_internal.h"
 
@@ -57,6 +58,14 @@ int chain_workgroups() {
     return device_cus();
 }
 
+// The launches of one validated, planned GEMV on the workspace `ws`.
+nmm_status gemv_launch(const GemvArgs& a, const GemvPlan& p, void* ws, void* stream) {
+    unsigned* tickets = static_cast<unsigned*>(ws);
+    float* part = ws ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kTicketBytes) : nullptr;
+    if (p.path == NMM_PATH_MFMA && a.K > 0) return launch_mfma(a, p, tickets, part, stream);
+    return launch_gemv(a, p, tickets, part, stream);
+}
+
 nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, void* stream) {
     nmm_status st = validate_gemv(a, path);
     if (st != NMM_OK) return st;
@@ -68,10 +77,34 @@ nmm_status gemv_common(const GemvArgs& a, int path, void* ws, size_t ws_bytes, v
         st = validate_workspace(ws, ws_bytes, p.ws_bytes);
         if (st != NMM_OK) return st;
     }
-    unsigned* tickets = static_cast<unsigned*>(ws);
-    float* part = ws ? reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + kTicketBytes) : nullptr;
-    if (p.path == NMM_PATH_MFMA && a.K > 0) return launch_mfma(a, p, tickets, part, stream);
-    return launch_gemv(a, p, tickets, part, stream);
+    return gemv_launch(a, p, ws, stream);
+}
+
+// ---------------------------------------------------------------------------------------------
+// The allocation-free GEMV's scratch: one array per GPU in the library's device code, resolved to
+// a device address once per device (hipGetSymbolAddress, with that device current) and kept.  Its
+// first kTicketBytes are the split-K arrival counters: zeroed by a fill kernel on the first call
+// on each device, and left at zero by every launch after it.
+// ---------------------------------------------------------------------------------------------
+constexpr size_t kScratchBytes = NMM_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+
+nmm_status scratch_of_current_device(void** out, hipStream_t s) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return NMM_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return NMM_ERR_HIP;
+        const nmm_status st = launch_zero_fill(ptr, kTicketBytes, s);
+        if (st != NMM_OK) return st;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return NMM_OK;
 }
 
 // The five narrow MatMuls of one decode chain, with their fused bf16 hand-offs.  All steps
@@ -217,6 +250,26 @@ nmm_status nmm_gemv(int64_t M, int64_t K, int64_t N, nmm_dtype dt, const void* x
     a.M = M; a.K = K; a.N = N; a.dt = dt;
     a.x = x; a.ldx = ldx; a.w = W; a.ldw = ldw; a.y = y; a.ldy = ldy;
     return gemv_common(a, path, workspace, workspace_bytes, stream);
+}
+
+nmm_status nmm_gemv_noalloc(int64_t M, int64_t K, int64_t N, nmm_dtype dt, const void* x, int64_t ldx,
+                            const void* W, int64_t ldw, float* y, int64_t ldy, nmm_path path, void* stream) {
+    GemvArgs a;
+    a.M = M; a.K = K; a.N = N; a.dt = dt;
+    a.x = x; a.ldx = ldx; a.w = W; a.ldw = ldw; a.y = y; a.ldy = ldy;
+    nmm_status st = validate_gemv(a, path);
+    if (st != NMM_OK) return st;
+    GemvPlan p;
+    st = plan_gemv(1, M, K, N, dt, path, &p);
+    if (st != NMM_OK) return st;
+    if (M == 0 || N == 0) return NMM_OK;
+    void* ws = nullptr;
+    if (K > 0 && p.ws_bytes > 0) {
+        if (p.ws_bytes > kScratchBytes) return NMM_ERR_WORKSPACE;
+        st = scratch_of_current_device(&ws, static_cast<hipStream_t>(stream));
+        if (st != NMM_OK) return st;
+    }
+    return gemv_launch(a, p, ws, stream);
 }
 
 nmm_status nmm_batched_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dtype dt,
