@@ -2,7 +2,8 @@
  * nmm.h -- narrow MatMul on AMD MI355X (gfx950): the C ABI.
  *
  * The library computes narrow matrix multiplications y = x . W in which x has only a few rows
- * (1..16 on the streaming path, more on the matrix-core path), at the shapes of DeepSeek-V3
+ * (any M on either path; AUTO streams W on the vector units for one row and uses the matrix
+ * cores from two rows on, see nmm_gemv), at the shapes of DeepSeek-V3
  * Multi-head Latent Attention single-token decode.  The operation is the paper's problem
  * statement C = A x B with A in R^{M x K}, B in R^{K x N}, narrow when min(M, N) = 1
  * (Section II-E "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"), widened to
@@ -310,9 +311,9 @@ nmm_status nmm_mla_kv_update(const nmm_mla_kv* kv, void* workspace, size_t works
  * hipEvent_t handles; event i is recorded on `stream` before step i (i < 5) and event 5 after
  * the last step -- optional instrumentation for per-step timing.  When kv_lora = 512,
  * v_head = 128 and nope is a multiple of 64 up to 512, the two per-head steps run as one
- * launch (one workgroup per head; the environment variable NMM_CHAIN_PAIR=0 keeps two) and
- * events 2 and 3 are both recorded before it.  Either way every output is the fp32 sum of the
- * same products; only the order of the additions differs between the two forms.
+ * launch (one workgroup per head) and events 2 and 3 are both recorded before it; other
+ * dimensions take two batched launches.  Either way every output is the fp32 sum of the same
+ * products; only the order of the additions differs between the two forms.
  *
  * Optionally (kv_cache not NULL) the chain also builds the latent cache entry from the
  * down-projection's kv_lora | rope columns, computed as nmm_mla_kv_update computes it:
@@ -404,8 +405,7 @@ nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, i
  * attention must be independent of the chain: its q, kv, out and out_bf16 may not overlap any
  * buffer the chain writes (the cache row included), and out / out_bf16 no buffer the chain reads
  * (NMM_ERR_ARG).  Same limits as the two calls; `events` as in nmm_mla_decode_chain (event 4 is
- * recorded before the shared launch, event 5 after the merge).  The chain runs as separate
- * launches (not the persistent form).  Workspace: nmm_mla_decode_step_workspace_size.
+ * recorded before the shared launch, event 5 after the merge).  Workspace: nmm_mla_decode_step_workspace_size.
  */
 typedef struct {
     int64_t heads, seq, d_qk, d_v;   /* DeepSeek-V3: 128 heads, 576, 512 */

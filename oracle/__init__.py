@@ -16,7 +16,7 @@ Functions (each cites the passage it follows in ``nmm_oracle.c``):
 * ``latent_attention``-- textbook softmax attention in fp64 (the decode step's independent work).
 * ``mla_chain``       -- the decode step's narrow chain composed from the above.
 
-``alg2_schedule`` (a separate module) models the partition of Algorithm 2 in the paper's notation.
+``alg2_schedule`` (a separate module) models the MatMul 2 work split of Section IV-E.
 """
 from __future__ import annotations
 

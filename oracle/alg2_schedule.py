@@ -1,28 +1,28 @@
-"""Model of the paper's specialised MatMul 2 partition (Algorithm 2, Section IV-E) -- TEST ONLY.
+"""The paper's MatMul 2 work split (Section IV-E, Algorithm 2), as a partition model -- TEST ONLY.
 
-This is the oracle's model of *how the paper splits the work*, written in the paper's notation
-(fractalSize, kSplitSize, kParts, fractalNum, S, V, nPart_W, groupSize, off_T, fracId, tmpBuf,
-Acc).  It is used to pin the reading of Algorithm 2's indexing and its worked constants; the HIP
-path does not follow it (its partition is sized for 256 compute units, not 2P vector units).
+Test infrastructure: used by tests/ only, never by the product path, which partitions for 256
+compute units instead (its own plan, in the library).
 
-Steps, in the order Algorithm 2 takes them:
+What the section describes, restated here in this module's own terms:
 
-* Init: fractalSize = 16, kSplitSize = 1024, kParts = K DIV kSplitSize,
-  fractalNum = N DIV fractalSize, S = fractalNum * kParts; V is the largest divisor of S that is
-  at most 2P; nPart_W = S DIV V; groupSize = V DIV kParts.
-* Compute: executor v processes fracId = v * nPart_W + w for w < nPart_W.  Each fracId is one
-  block of kSplitSize rows by fractalSize columns; the block's 16 partial sums are fp32 dot
-  products of the token slice with the block's columns (Transpose + Cast + Mul + ReduceSum).
-  They are stored to the fp32 partial-sum buffer tmpBuf.
-* Gather (after WaitAllVectors): executor v < fractalNum sums the kParts partials of column
-  fractal v in order i = 0..kParts-1 into the fp32 accumulator Acc, then casts Acc to bf16.
+* The weight [K, N] is cut into blocks of ``k_slice`` = 1024 rows by ``col_block`` = 16
+  columns: ``n_slices`` = K // k_slice row slices times ``n_col_blocks`` = N // col_block column
+  blocks, ``n_blocks`` blocks in all.
+* The blocks are dealt to ``n_units`` vector units -- the largest count not above two per core
+  (2P) that divides ``n_blocks`` evenly -- each unit taking one contiguous run of
+  ``blocks_per_unit`` blocks, numbered slice-major (block b is column block b % n_col_blocks of
+  row slice b // n_col_blocks).  ``units_per_slice`` = n_units // n_slices is how many units
+  share one row slice when the runs line up with slices.
+* Each block yields 16 fp32 partial dot products of the token's row slice with the block's
+  columns; they go to a [n_slices, N] fp32 buffer.  After every unit has stored its blocks,
+  each column block sums its partials over the row slices in slice order, and the sum is cast
+  to bf16.
 
-Reading of the garbled/ambiguous indexing (Algorithm 2): the printed token offset
-off_T = (v DIV groupSize) * kSplitSize only holds when every executor's nPart_W blocks sit in one
-k-part (true for the paper's N = 576, false e.g. for N = 2112 where V = 44 is not a multiple of
-kParts = 7).  The reading used here: block fracId has k-part ``fracId DIV fractalNum`` and column
-fractal ``fracId MOD fractalNum``; tmpBuf is laid out [kParts][N] in fp32, so block fracId's 16
-floats start at element fracId * fractalSize, which is the gather's ``off_C + i * N``.
+Reading of the section's indexing: the listing gives a unit one token offset, derived from its
+unit number.  That is only well defined when a unit's run of blocks stays inside one row slice,
+which holds at the paper's N = 576 but not at N = 2112 (44 units over 7 slices).  This model
+takes the block numbering above, under which a run may straddle two slices, and every block
+reads its own slice of the token.
 """
 from __future__ import annotations
 
@@ -30,76 +30,64 @@ from dataclasses import dataclass
 
 import numpy as np
 
-FRACTAL_SIZE = 16
-K_SPLIT_SIZE = 1024
+COL_BLOCK = 16
+K_SLICE = 1024
 
 
 @dataclass(frozen=True)
-class Alg2Plan:
+class Partition:
     K: int
     N: int
-    P: int
-    fractalSize: int
-    kSplitSize: int
-    kParts: int
-    fractalNum: int
-    S: int
-    V: int
-    nPart_W: int
-    groupSize: int
+    cores: int            # P
+    col_block: int
+    k_slice: int
+    n_slices: int
+    n_col_blocks: int
+    n_blocks: int
+    n_units: int
+    blocks_per_unit: int
+    units_per_slice: int
 
-    def frac_ids(self, v: int) -> list[int]:
-        """Blocks of executor v (compute stage)."""
-        return [v * self.nPart_W + w for w in range(self.nPart_W)]
+    def blocks_of(self, unit: int) -> range:
+        """The contiguous run of block numbers that ``unit`` computes."""
+        return range(unit * self.blocks_per_unit, (unit + 1) * self.blocks_per_unit)
 
-    def block(self, fracId: int) -> tuple[int, int]:
-        """(k-part, column fractal) of a block under the reading above."""
-        return fracId // self.fractalNum, fracId % self.fractalNum
+    def slice_and_cols(self, block: int) -> tuple[int, int]:
+        """(row slice, column block) of a block number."""
+        return divmod(block, self.n_col_blocks)
 
-    def literal_off_T(self, v: int) -> int:
-        """The token offset exactly as printed: (v DIV groupSize) * kSplitSize."""
-        return (v // self.groupSize) * self.kSplitSize
-
-
-def plan(K: int, N: int, P: int = 24) -> Alg2Plan:
-    """Init stage of Algorithm 2 for T[1,K] x W[K,N] on P cores (2P vector units)."""
-    kParts = K // K_SPLIT_SIZE
-    fractalNum = N // FRACTAL_SIZE
-    S = fractalNum * kParts
-    if S == 0:
-        raise ValueError("Algorithm 2 needs K >= kSplitSize and N >= fractalSize")
-    V = max(d for d in range(1, 2 * P + 1) if S % d == 0)
-    nPart_W = S // V
-    groupSize = V // kParts
-    return Alg2Plan(K, N, P, FRACTAL_SIZE, K_SPLIT_SIZE, kParts, fractalNum, S, V, nPart_W,
-                    groupSize)
+    def slices_of(self, unit: int) -> set[int]:
+        """The row slices that ``unit``'s run touches."""
+        return {self.slice_and_cols(b)[0] for b in self.blocks_of(unit)}
 
 
-def run(T: np.ndarray, W: np.ndarray, p: Alg2Plan, decode) -> tuple[np.ndarray, np.ndarray]:
-    """Execute the compute and gather stages in fp32.
+def partition(K: int, N: int, cores: int = 24) -> Partition:
+    """The split of T[1, K] x W[K, N] over ``cores`` cores (two vector units each)."""
+    n_slices, n_col_blocks = K // K_SLICE, N // COL_BLOCK
+    n_blocks = n_slices * n_col_blocks
+    if n_blocks == 0:
+        raise ValueError("the split needs K >= 1024 and N >= 16")
+    n_units = next(u for u in range(2 * cores, 0, -1) if n_blocks % u == 0)
+    return Partition(K, N, cores, COL_BLOCK, K_SLICE, n_slices, n_col_blocks, n_blocks, n_units,
+                     n_blocks // n_units, n_units // n_slices)
 
-    ``T`` is [1,K] and ``W`` is [K,N] bf16 bit patterns; ``decode`` turns bits into float64 (the
-    oracle's decoder).  Returns (Acc as fp32 [N'], tmpBuf [kParts, N']) where
-    N' = fractalNum * fractalSize.
-    """
-    fs, ks = p.fractalSize, p.kSplitSize
-    Tf = decode(T, 2).astype(np.float32).reshape(-1)          # Cast (exact widening)
-    Wf = decode(W, 2).astype(np.float32)
-    Np = p.fractalNum * fs
-    tmpBuf = np.full((p.kParts, Np), np.nan, dtype=np.float32)
-    for v in range(p.V):                                       # compute stage, executor v
-        for fracId in p.frac_ids(v):
-            kpart, cf = p.block(fracId)
-            Tv = Tf[kpart * ks:(kpart + 1) * ks]
-            Wvw = Wf[kpart * ks:(kpart + 1) * ks, cf * fs:(cf + 1) * fs]
-            partSum = np.array([np.dot(Tv, Wvw[:, j]) for j in range(fs)], dtype=np.float32)
-            tmpBuf.reshape(-1)[fracId * fs:(fracId + 1) * fs] = partSum
-    # WaitAllVectors: every block above has been stored.
-    Acc = np.zeros(Np, dtype=np.float32)
-    for v in range(p.fractalNum):                              # gather stage, executor v
-        off_C = v * fs
-        acc = np.zeros(fs, dtype=np.float32)
-        for i in range(p.kParts):
-            acc = acc + tmpBuf.reshape(-1)[off_C + i * Np: off_C + i * Np + fs]
-        Acc[off_C:off_C + fs] = acc
-    return Acc, tmpBuf
+
+def evaluate(T: np.ndarray, W: np.ndarray, part: Partition, decode) -> tuple[np.ndarray, np.ndarray]:
+    """Run the split in fp32.  ``T`` [1, K] and ``W`` [K, N] are bf16 bit patterns and ``decode``
+    turns bits into float64.  Returns (the gathered fp32 sums [N'], the partial-sum buffer
+    [n_slices, N']) for the N' = n_col_blocks * 16 columns the split covers."""
+    t = decode(T, 2).astype(np.float32).reshape(-1)            # widening is exact
+    w = decode(W, 2).astype(np.float32)
+    width = part.n_col_blocks * part.col_block
+    partials = np.full((part.n_slices, width), np.nan, dtype=np.float32)
+    for unit in range(part.n_units):
+        for block in part.blocks_of(unit):
+            s, c = part.slice_and_cols(block)
+            rows = slice(s * part.k_slice, (s + 1) * part.k_slice)
+            cols = slice(c * part.col_block, (c + 1) * part.col_block)
+            partials[s, cols] = np.dot(t[rows], w[rows, cols]).astype(np.float32)
+    # every unit has stored its blocks: sum each column's partials over the slices, in order
+    total = np.zeros(width, dtype=np.float32)
+    for s in range(part.n_slices):
+        total = total + partials[s]
+    return total, partials

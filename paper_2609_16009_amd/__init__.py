@@ -175,30 +175,66 @@ def _ld(t: torch.Tensor) -> int:
 
 
 class Workspace:
-    """A zeroed device buffer that grows on demand (one per device and user)."""
+    """Device memory for split-K partial sums and arrival counters, grown on demand.
+
+    A workspace serves one stream at a time: calls that may overlap need different workspaces.
+    A new buffer is zeroed on the stream of the call that needs it (allocated there too, so that
+    torch's allocator orders its reuse with that stream); the buffers it replaces are kept until
+    the Workspace is dropped, because kernels enqueued earlier may still be using them."""
 
     def __init__(self, device=None):
         self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
         self.buf = None
+        self._retired = []
 
-    def get(self, nbytes: int) -> tuple[int, int]:
+    def get(self, nbytes: int, stream=None) -> tuple[int, int]:
         if nbytes == 0:
             return 0, 0
         if self.buf is None or self.buf.numel() < nbytes:
-            self.buf = torch.zeros(max(nbytes, 1 << 20), dtype=torch.uint8, device=self.device)
+            ts = _torch_stream(stream, self.device)
+            size = max(nbytes, 1 << 20, 2 * self.buf.numel() if self.buf is not None else 0)
+            with torch.cuda.stream(ts):
+                buf = torch.empty(size, dtype=torch.uint8, device=self.device)
+            _check(lib().nmm_workspace_init(buf.data_ptr(), size, ts.cuda_stream), "nmm_workspace_init")
+            if self.buf is not None:
+                self._retired.append(self.buf)
+            self.buf = buf
         return self.buf.data_ptr(), self.buf.numel()
+
+
+def _torch_stream(stream, device) -> torch.cuda.Stream:
+    if stream is None:
+        return torch.cuda.current_stream(device)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=device)
 
 
 _default_ws: dict = {}
 
 
-def _workspace(ws, nbytes: int, device) -> tuple[int, int]:
+def _workspace(ws, nbytes: int, device, stream=None) -> tuple[int, int]:
+    """The workspace of one call.  Without one given, each (device, stream) pair has its own, so
+    calls on different streams never share partial sums or counters."""
     if ws is None:
-        key = torch.device(device).index
-        ws = _default_ws.setdefault(key, Workspace(device))
+        dev = torch.device(device)
+        key = (dev.index, _stream(stream))
+        ws = _default_ws.get(key)
+        if ws is None:
+            ws = _default_ws[key] = Workspace(dev)
     if isinstance(ws, Workspace):
-        return ws.get(nbytes)
+        return ws.get(nbytes, stream)
     return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def _prepared_workspace(ws, nbytes: int, device):
+    """The workspace of a prepared call, which is launched later on any stream: without one
+    given, a private one.  Either way it is sized and zeroed before this returns.  Returns the
+    (pointer, bytes) pair and the private Workspace (None for a given one) to keep alive."""
+    own = Workspace(device) if ws is None else None
+    out = _workspace(own if ws is None else ws, nbytes, device)
+    torch.cuda.current_stream(torch.device(device)).synchronize()
+    return out, own
 
 
 def nmm_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None = None,
@@ -208,7 +244,7 @@ def nmm_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: int | None
     M, K = x.shape[0], W.shape[0]
     N = W.shape[1] if N is None else N
     need = lib().nmm_gemv_workspace_size(M, K, N, code, path)
-    wp, wb = _workspace(workspace, need, x.device)
+    wp, wb = _workspace(workspace, need, x.device, stream)
     _check(lib().nmm_gemv(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y.data_ptr(),
                           _ld(y), path, wp, wb, _stream(stream)), "nmm_gemv")
     return y
@@ -233,7 +269,7 @@ def nmm_gemv_bf16(x: torch.Tensor, W: torch.Tensor, y_bf16: torch.Tensor, *, rou
     M, K = x.shape[0], W.shape[0]
     N = W.shape[1] if N is None else N
     need = lib().nmm_gemv_workspace_size(M, K, N, code, path)
-    wp, wb = _workspace(workspace, need, x.device)
+    wp, wb = _workspace(workspace, need, x.device, stream)
     _check(lib().nmm_gemv_bf16(M, K, N, code, x.data_ptr(), _ld(x), W.data_ptr(), _ld(W), y_bf16.data_ptr(),
                                _ld(y_bf16), round, y.data_ptr() if y is not None else None,
                                _ld(y) if y is not None else 0, path, wp, wb, _stream(stream)), "nmm_gemv_bf16")
@@ -248,7 +284,7 @@ def nmm_batched_gemv_bf16(x: torch.Tensor, W: torch.Tensor, y_bf16: torch.Tensor
     B, M, K = x.shape[0], x.shape[1], W.shape[1]
     N = W.shape[2] if N is None else N
     need = lib().nmm_batched_gemv_workspace_size(B, M, K, N, code, path)
-    wp, wb = _workspace(workspace, need, x.device)
+    wp, wb = _workspace(workspace, need, x.device, stream)
     _check(lib().nmm_batched_gemv_bf16(B, M, K, N, code, x.data_ptr(), _ld(x), x.stride(0), W.data_ptr(), _ld(W),
                                        W.stride(0), y_bf16.data_ptr(), _ld(y_bf16), y_bf16.stride(0), round,
                                        y.data_ptr() if y is not None else None, _ld(y) if y is not None else 0,
@@ -263,7 +299,7 @@ def nmm_mla_query(q: torch.Tensor, q_bf16: torch.Tensor, w_uk: torch.Tensor, qla
     q_bf16 its bf16 rounding, w_uk [heads, nope, kv_lora]; qlat [heads, kv_lora] fp32 receives the products."""
     heads, kv_lora = w_uk.shape[0], w_uk.shape[2]
     need = lib().nmm_mla_query_workspace_size(heads, nope, kv_lora)
-    wp, wb = _workspace(workspace, need, q.device)
+    wp, wb = _workspace(workspace, need, q.device, stream)
     _check(lib().nmm_mla_query(heads, nope, rope, kv_lora, q.data_ptr(), q_bf16.data_ptr(), w_uk.data_ptr(),
                                int(position), float(theta), qlat.data_ptr(), q_out.data_ptr(), _ld(q_out), wp, wb,
                                _stream(stream)), "nmm_mla_query")
@@ -289,7 +325,7 @@ class PreparedQueryPath:
         c.ldq = _ld(bufs["query"])
         self._c = c
         need = lib().nmm_mla_query_path_workspace_size(ctypes.byref(c))
-        self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
+        (self._wp, self._wb), self._ws = _prepared_workspace(workspace, need, bufs["x"].device)
 
     def launch(self, stream=None) -> None:
         _check(lib().nmm_mla_query_path_run(ctypes.byref(self._c), self._wp, self._wb, _stream(stream)),
@@ -303,7 +339,7 @@ def nmm_gemv_nt(x: torch.Tensor, Wt: torch.Tensor, y: torch.Tensor, *, K: int | 
     M, N = x.shape[0], Wt.shape[0]
     K = Wt.shape[1] if K is None else K
     need = lib().nmm_gemv_nt_workspace_size(M, K, N, code)
-    wp, wb = _workspace(workspace, need, x.device)
+    wp, wb = _workspace(workspace, need, x.device, stream)
     _check(lib().nmm_gemv_nt(M, K, N, code, x.data_ptr(), _ld(x), Wt.data_ptr(), _ld(Wt), y.data_ptr(), _ld(y),
                              wp, wb, _stream(stream)), "nmm_gemv_nt")
     return y
@@ -331,7 +367,7 @@ def nmm_mla_kv_update(h: torch.Tensor, w: torch.Tensor, gamma: torch.Tensor, mm:
     k = _kv_struct(h, w, gamma, mm, cache, kv_lora=kv_lora, rope=rope, eps=eps, theta=theta,
                    position=position, round=round)
     need = lib().nmm_mla_kv_update_workspace_size(ctypes.byref(k))
-    wp, wb = _workspace(workspace, need, h.device)
+    wp, wb = _workspace(workspace, need, h.device, stream)
     _check(lib().nmm_mla_kv_update(ctypes.byref(k), wp, wb, _stream(stream)), "nmm_mla_kv_update")
 
 
@@ -343,7 +379,7 @@ def nmm_batched_gemv(x: torch.Tensor, W: torch.Tensor, y: torch.Tensor, *, N: in
     B, M, K = x.shape[0], x.shape[1], W.shape[1]
     N = W.shape[2] if N is None else N
     need = lib().nmm_batched_gemv_workspace_size(B, M, K, N, code, path)
-    wp, wb = _workspace(workspace, need, x.device)
+    wp, wb = _workspace(workspace, need, x.device, stream)
     _check(lib().nmm_batched_gemv(B, M, K, N, code, x.data_ptr(), _ld(x), x.stride(0), W.data_ptr(),
                                   _ld(W), W.stride(0), y.data_ptr(), _ld(y), y.stride(0), path, wp,
                                   wb, _stream(stream)), "nmm_batched_gemv")
@@ -417,7 +453,7 @@ class PreparedChain:
             c, keep = _chain_struct(dims, bufs, evs, kv)
             self._slots.append((c, keep))
         need = lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(self._slots[0][0]))
-        self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
+        (self._wp, self._wb), self._ws = _prepared_workspace(workspace, need, bufs["x"].device)
 
     def launch(self, slot: int = 0, stream=None) -> None:
         c = self._slots[slot][0]
@@ -457,7 +493,7 @@ class PreparedStep:
         need = lib().nmm_mla_decode_step_workspace_size(ctypes.byref(self._slots[0][0]), ctypes.byref(self._a))
         if need == 0:
             raise ValueError("nmm_mla_decode_step: invalid chain or attention sizes")
-        self._wp, self._wb = _workspace(workspace, need, bufs["x"].device)
+        (self._wp, self._wb), self._ws = _prepared_workspace(workspace, need, bufs["x"].device)
 
     def launch(self, slot: int = 0, stream=None) -> None:
         c = self._slots[slot][0]
@@ -491,7 +527,7 @@ def nmm_mla_decode_chain(dims: dict, bufs: dict, *, workspace=None, stream=None,
     optional cache entry (see _chain_struct)."""
     c, keep = _chain_struct(dims, bufs, events, kv)
     need = lib().nmm_mla_decode_chain_workspace_size(ctypes.byref(c))
-    wp, wb = _workspace(workspace, need, bufs["x"].device)
+    wp, wb = _workspace(workspace, need, bufs["x"].device, stream)
     _check(lib().nmm_mla_decode_chain(ctypes.byref(c), wp, wb, _stream(stream)), "nmm_mla_decode_chain")
     del keep
 
@@ -506,7 +542,7 @@ def nmm_latent_attention(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, s
     heads, seq = q.shape[0], kv.shape[0]
     d_qk = q.shape[1] if d_qk is None else d_qk
     need = lib().nmm_latent_attention_workspace_size(heads, seq, d_qk, d_v)
-    wp, wb = _workspace(workspace, need, q.device)
+    wp, wb = _workspace(workspace, need, q.device, stream)
     _check(lib().nmm_latent_attention(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(),
                                       _ld(kv), float(scale), out.data_ptr(), _ld(out), wp, wb,
                                       _stream(stream)), "nmm_latent_attention")
@@ -520,7 +556,7 @@ def nmm_latent_attention_bf16(q: torch.Tensor, kv: torch.Tensor, out: torch.Tens
     heads, seq = q.shape[0], kv.shape[0]
     d_qk = q.shape[1] if d_qk is None else d_qk
     need = lib().nmm_latent_attention_workspace_size(heads, seq, d_qk, d_v)
-    wp, wb = _workspace(workspace, need, q.device)
+    wp, wb = _workspace(workspace, need, q.device, stream)
     _check(lib().nmm_latent_attention_bf16(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(), _ld(kv),
                                            float(scale), out.data_ptr(), _ld(out), out_bf16.data_ptr(), _ld(out_bf16),
                                            wp, wb, _stream(stream)), "nmm_latent_attention_bf16")
@@ -535,7 +571,7 @@ def nmm_latent_attention_ex(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor
     heads, seq = q.shape[0], kv.shape[0]
     d_qk = q.shape[1] if d_qk is None else d_qk
     need = lib().nmm_latent_attention_ex_workspace_size(heads, seq, d_qk, d_v, splits)
-    wp, wb = _workspace(workspace, need, q.device)
+    wp, wb = _workspace(workspace, need, q.device, stream)
     _check(lib().nmm_latent_attention_ex(heads, seq, d_qk, d_v, q.data_ptr(), _ld(q), kv.data_ptr(), _ld(kv),
                                          float(scale), out.data_ptr(), _ld(out),
                                          out_bf16.data_ptr() if out_bf16 is not None else None,

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -17,46 +18,23 @@ namespace {
 size_t rup256(size_t v) { return (v + 255) / 256 * 256; }
 int64_t rup8(int64_t v) { return (v + 7) / 8 * 8; }
 
-// Workgroups of the persistent chain launch: one per compute unit of the current device, so
-// that all of them are resident together even beside other kernels (NMM_CHAIN_WGS overrides).
-// Row-steps in flight per lane in the fused chain (NMM_CHAIN_UNROLL overrides).
-int chain_unroll() {
-    if (const char* s = std::getenv("NMM_CHAIN_UNROLL")) {
-        const long v = std::strtol(s, nullptr, 10);
-        if (v == 4 || v == 8 || v == 16) return static_cast<int>(v);
-    }
-    return 16;
-}
-
-bool chain_pair_enabled() {
-    const char* e = std::getenv("NMM_CHAIN_PAIR");
-    return !(e && e[0] == '0');
-}
-
-bool chain_fused_requested() {
-    const char* fe = std::getenv("NMM_CHAIN_FUSED");
-    return fe && fe[0] == '1';
-}
-
 }  // namespace
 
-// Compute units of the current device (256 on MI355X; also the answer when no device is visible).
+// Compute units of the current device (256 on MI355X; also the answer when no device is visible),
+// queried once per device and kept.
 int nmm::device_cus() {
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-        cus = 256;
+    constexpr int kDevices = 64;
+    static std::atomic<int> cached[kDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kDevices) return 256;
+    int cus = cached[dev].load(std::memory_order_relaxed);
+    if (cus > 0) return cus;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
+    cached[dev].store(cus, std::memory_order_relaxed);
     return cus;
 }
 
 namespace {
-
-int chain_workgroups() {
-    if (const char* s = std::getenv("NMM_CHAIN_WGS")) {
-        const long v = std::strtol(s, nullptr, 10);
-        if (v > 0 && v < (1 << 20)) return static_cast<int>(v);
-    }
-    return device_cus();
-}
 
 // The launches of one validated, planned GEMV on the workspace `ws`.
 nmm_status gemv_launch(const GemvArgs& a, const GemvPlan& p, void* ws, void* stream) {
@@ -113,7 +91,6 @@ nmm_status scratch_of_current_device(void** out, hipStream_t s) {
 struct Chain {
     GemvArgs step[5];
     GemvPlan plan[5];
-    int64_t flag_off;      // first completion flag of the fused launch
     int64_t tick_off[5];   // first counter of each step
     size_t part_off[5];    // byte offset of each step's partial sums (from the workspace start)
     size_t ws_total;
@@ -126,7 +103,7 @@ bool chain_dims_ok(const nmm_mla_chain& c) {
     return c.nope + c.rope < (int64_t(1) << 31) / c.heads;
 }
 
-nmm_status build_chain(const nmm_mla_chain& c, Chain* out, int unroll = 0) {
+nmm_status build_chain(const nmm_mla_chain& c, Chain* out) {
     if (!chain_dims_ok(c)) return NMM_ERR_SHAPE;
     const int64_t n_down = c.q_lora + c.kv_lora + c.rope;
     const int64_t qk = c.nope + c.rope;
@@ -158,26 +135,21 @@ nmm_status build_chain(const nmm_mla_chain& c, Chain* out, int unroll = 0) {
     s[4].K = c.heads * c.v_head; s[4].N = c.hidden; s[4].x = c.o_bf16; s[4].ldx = c.heads * c.v_head;
     s[4].w = c.w_o; s[4].ldw = c.hidden; s[4].y = c.y; s[4].ldy = c.hidden;
     size_t off = kTicketBytes;
-    int64_t ticks = kChainSyncWords;   // the fused chain's queue and completion words come first
-    bool any_split = false;
+    int64_t ticks = 0;
     for (int i = 0; i < 5; ++i) {
         s[i].M = 1;
         s[i].dt = NMM_BF16;
-        nmm_status st = plan_gemv(s[i].batch, 1, s[i].K, s[i].N, NMM_BF16, NMM_PATH_GEMV, &ch.plan[i], unroll);
+        nmm_status st = plan_gemv(s[i].batch, 1, s[i].K, s[i].N, NMM_BF16, NMM_PATH_GEMV, &ch.plan[i]);
         if (st != NMM_OK) return st;
         ch.tick_off[i] = ticks;
         ch.part_off[i] = off;
         if (ch.plan[i].split()) {
-            any_split = true;
             ticks += ch.plan[i].n_tickets;
             off += rup256(static_cast<size_t>(ch.plan[i].part_floats) * 4);
         }
     }
-    ch.flag_off = ticks;
-    ticks += chain_flags(ch.step, ch.plan, 5);
     if (ticks > kMaxTickets) return NMM_ERR_SHAPE;
-    (void)any_split;
-    ch.ws_total = off;   // the counter block is always needed: the fused chain keeps its queue there
+    ch.ws_total = off;   // the counter block is always part of it
     *out = ch;
     return NMM_OK;
 }
@@ -576,10 +548,8 @@ nmm_status nmm_gemv_plan(int64_t batch, int64_t M, int64_t K, int64_t N, nmm_dty
 
 size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain) {
     if (!chain) return 0;
-    // enough for either form of the chain (separate launches or the fused launch)
-    Chain a, b;
-    if (build_chain(*chain, &a) != NMM_OK || build_chain(*chain, &b, chain_unroll()) != NMM_OK) return 0;
-    return std::max(a.ws_total, b.ws_total);
+    Chain ch;
+    return build_chain(*chain, &ch) == NMM_OK ? ch.ws_total : 0;
 }
 
 }  // extern "C"
@@ -596,8 +566,7 @@ nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* work
         !c.lat_f32 || !c.o_f32 || !c.y || !c.cq_bf16 || !c.qnope_bf16 || !c.lat_bf16 || !c.o_bf16)
         return NMM_ERR_NULL;
     Chain ch;
-    const bool want_fused = !att && chain_fused_requested();
-    nmm_status st = build_chain(c, &ch, want_fused ? chain_unroll() : 0);
+    nmm_status st = build_chain(c, &ch);
     if (st != NMM_OK) return st;
     for (int i = 0; i < 5; ++i) {
         st = validate_gemv(ch.step[i], NMM_PATH_GEMV);
@@ -631,29 +600,9 @@ nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* work
             if (!c.events[i]) return NMM_ERR_NULL;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // One launch per MatMul by default; NMM_CHAIN_FUSED=1 selects the persistent launch that runs
-    // all five MatMuls with per-panel dependencies.
-    const bool fused = want_fused && !c.kv_cache && chain_fusable(ch.step, ch.plan, 5);
-    if (fused) {
-        unsigned* sync = static_cast<unsigned*>(workspace);
-        unsigned* tickets[5];
-        float* part[5];
-        for (int i = 0; i < 5; ++i) {
-            tickets[i] = ch.plan[i].split() ? sync + ch.tick_off[i] : nullptr;
-            part[i] = ch.plan[i].split() ? reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + ch.part_off[i]) : nullptr;
-        }
-        if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[0]), s) != hipSuccess) return NMM_ERR_HIP;
-        st = launch_chain(ch.step, ch.plan, 5, sync, sync + ch.flag_off, tickets, part, chain_workgroups(), stream);
-        if (st != NMM_OK) return st;
-        if (c.events) {
-            for (int i = 1; i < 6; ++i)
-                if (hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess) return NMM_ERR_HIP;
-        }
-        return NMM_OK;
-    }
-    // W_UK and W_UV run as one launch, one workgroup per head, where the dimensions allow it
-    // (NMM_CHAIN_PAIR=0 keeps two launches); events 2 and 3 are then recorded together before it
-    const bool pair = chain_pair_enabled() && head_pair_ok(c.heads, c.nope, c.kv_lora, c.v_head);
+    // W_UK and W_UV run as one launch, one workgroup per head, where the dimensions allow it;
+    // events 2 and 3 are then recorded together before it
+    const bool pair = head_pair_ok(c.heads, c.nope, c.kv_lora, c.v_head);
     for (int i = 0; i < 5; ++i) {
         if (c.events && hipEventRecord(static_cast<hipEvent_t>(c.events[i]), s) != hipSuccess)
             return NMM_ERR_HIP;

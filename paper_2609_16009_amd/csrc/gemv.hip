@@ -167,16 +167,10 @@ __device__ __forceinline__ void stream_rows(float (&acc)[MT][8], i32x4 (&buf)[U]
     for (int u = 0; u < U; ++u) fma_chunk<DT, MT>(acc, buf[u], xs + (s + u) * xs_step);
 }
 
-// Cache policy of x loads inside the fused chain: device-coherent (sc1), because x was written
-// by other workgroups of the same launch and this XCD's L2 may hold older copies.
-constexpr int kLoadCoherent = 16;
-
-// How y and its bf16 copy are stored.  Inside the fused chain the bf16 copy is the next
-// MatMul's operand, read by other workgroups during the same launch; after MatMul 2 the fp32 y
-// is read by the launch's last workgroup (the cache-entry epilogue).  Those stores are
-// device-scope atomic stores (coherent at memory).
-constexpr int kStorePlain = 0;   // separate launch: plain stores
-constexpr int kStoreChain = 1;   // the bf16 copy coherent
+// How y and its bf16 copy are stored.  After MatMul 2 the fp32 y is read by the launch's last
+// workgroup (the cache-entry epilogue), so there y goes out as device-scope atomic stores
+// (coherent at memory).
+constexpr int kStorePlain = 0;   // plain stores
 constexpr int kStoreEpi = 2;     // y coherent
 constexpr int kStoreNoY = 3;     // separate launch with the bf16 copy only (y is null)
 
@@ -192,8 +186,7 @@ __device__ __forceinline__ void store_out(const KParams& p, int64_t b, int m, in
         const int64_t g = n / p.ybf_group, r = n - g * p.ybf_group;
         if (r < p.ybf_keep) {
             uint16_t* dst = p.ybf + b * p.ybf_sb + int64_t(m) * p.ybf_ldm + g * p.ybf_keep + r;
-            if constexpr (SM == kStoreChain) __hip_atomic_store(dst, to_bf16_bits(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            else *dst = to_bf16_mode(v, p.ybf_away);
+            *dst = to_bf16_mode(v, p.ybf_away);
         }
     }
 }
@@ -927,175 +920,6 @@ __global__ __launch_bounds__(kThreads) void gemv_entry_kernel(const KParams p, c
     gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
 }
 
-// ---------------------------------------------------------------------------------------------
-// The fused decode chain: one persistent launch runs the MatMuls of the chain back to back
-// (bf16, one row).  The work items of all MatMuls form one ordered list (every item of MatMul s
-// precedes every item of MatMul s+1); workgroup w takes items w, w + G, w + 2G, ... in order.
-//
-//  * Dependencies are per panel: when a panel's outputs (fp32 y and the bf16 hand-off) are
-//    complete, the workgroup that wrote them raises the panel's flag.  An item of MatMul s+1
-//    waits only for the panels of MatMul s that produce its own K-slice of x, so the next
-//    weight stream starts as soon as the inputs it needs exist, not when the whole previous
-//    MatMul has finished -- the paper's point of starting independent work earlier, here
-//    between consecutive narrow MatMuls.
-//  * Each item issues the first U row-steps of the NEXT item's W (which depend on nothing)
-//    right after its own partial sums are out, so that the split-K ticket round trip, the
-//    gather and the next dependency wait all overlap with weight loads in flight.
-//
-// Progress: a workgroup takes its items in list order, and an item only waits on items placed
-// earlier in the list, so the earliest unfinished item can always run once all G workgroups are
-// resident.  The launch is clamped to the number that the device can hold at once.  Every wait
-// is also bounded (spin_limit polls): if one ever gave up, the error word is raised instead of
-// the GPU hanging.  The last workgroup out clears the flags for the next launch.
-// ---------------------------------------------------------------------------------------------
-constexpr int kChainMax = 5;
-
-struct ChainArgs {
-    KParams step[kChainMax];
-    int first_item[kChainMax + 1];   // list position of each MatMul's first item; [n] = total
-    int flag_off[kChainMax + 1];     // first completion flag of each MatMul's panels; [n] = total
-    unsigned* sync;                  // [1] exited workgroups, [2] error word
-    unsigned* flags;                 // one per panel (batch entry x column panel) of every MatMul
-    int n_steps;
-    int spin_limit;
-    int sleep_reps;
-};
-
-// The panel (flattened over batch entries) of the producing MatMul that wrote element j of its
-// bf16 hand-off buffer: j = b * ybf_sb + g * keep + r holds output column g * group + r.
-__device__ __forceinline__ int producer_panel(const KParams& pp, int64_t j) {
-    int64_t b = 0, rem = j;
-    if (pp.ybf_sb > 0) {
-        b = j / pp.ybf_sb;
-        rem = j - b * pp.ybf_sb;
-    }
-    const int64_t g = rem / pp.ybf_keep, r = rem - g * pp.ybf_keep;
-    const int64_t n = g * pp.ybf_group + r;
-    const int pan = static_cast<int>(min(n >> (3 + pp.full_lg), int64_t(pp.n_full)));
-    return static_cast<int>(b) * pp.n_panels + pan;
-}
-
-// Wait until every producer panel covering this item's x slice has raised its flag.  Wave 0
-// polls up to 64 flags at once; bounded by spin_limit polls.
-__device__ __forceinline__ void wait_panels(const ChainArgs& a, int st, const Item& it, int tid) {
-    const KParams& pc = a.step[st];
-    const KParams& pp = a.step[st - 1];
-    const int64_t jb = it.b * pc.sx;
-    const int qa = producer_panel(pp, jb + it.k0);
-    const int qb = producer_panel(pp, jb + min(it.k0 + it.rows, pc.K) - 1);
-    if (tid < 64) {
-        const unsigned* f = a.flags + a.flag_off[st - 1];
-        for (int q0 = qa; q0 <= qb; q0 += 64) {
-            const int q = q0 + tid;
-            bool ok = q > qb;
-            int spins = 0;
-            while (true) {
-                if (!ok) ok = __hip_atomic_load(f + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-                if (__all(ok)) break;
-                if (++spins > a.spin_limit) {
-                    if (tid == 0) __hip_atomic_store(a.sync + 2, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
-                }
-                for (int r = 0; r < a.sleep_reps; ++r) __builtin_amdgcn_s_sleep(2);
-            }
-        }
-    }
-    __syncthreads();
-}
-
-__device__ __forceinline__ void raise_flag(const ChainArgs& a, int st, const Item& it) {
-    const KParams& p = a.step[st];
-    __hip_atomic_store(a.flags + a.flag_off[st] + it.b * p.n_panels + it.panel, 1u, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-}
-
-template <int U>
-__global__ __launch_bounds__(kThreads) void chain_kernel(const ChainArgs a) {
-    extern __shared__ float lds[];
-    __shared__ int s_last;
-    const int tid = threadIdx.x;
-    const int total = a.first_item[a.n_steps];
-    int item = blockIdx.x;
-    int st = 0;
-    Item it;
-    Stream ss;
-    i32x4 buf[U];
-    if (item < total) {
-        while (st + 1 < a.n_steps && item >= a.first_item[st + 1]) ++st;
-        it = item_of<1>(a.step[st], item - a.first_item[st], tid);
-        ss = stream_of(a.step[st], it);
-        prefetch<U, true>(buf, ss);
-    }
-    while (item < total) {
-        const KParams& p = a.step[st];
-        if (st > 0) wait_panels(a, st, it, tid);
-        {
-            i32x4 xv[kXPer];
-            stage_x_issue<1, kLoadCoherent>(xv, p, it.b, it.m0, it.k0, it.rows, tid);
-            stage_x_commit<NMM_BF16, 1>(lds, xv, p, it.k0, it.rows, tid);
-        }
-        __syncthreads();
-        float acc[1][8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) acc[0][j] = 0.f;
-        stream_rows<NMM_BF16, 1, U, true>(acc, buf, ss, it.rows / it.rstep, lds + it.rin, it.rstep);
-        __syncthreads();
-        reduce_item<1, kStoreChain>(p, it, acc, lds, tid);
-        __builtin_amdgcn_s_waitcnt(0);   // this item's stores are complete
-        __syncthreads();
-        unsigned prev = 0;
-        if (tid == 0) {
-            if (it.ks == 1) raise_flag(a, st, it);
-            else prev = __hip_atomic_fetch_add(ticket_of(p, it), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        // the next item's first loads go out before anything waits on the ticket
-        const int nitem = item + static_cast<int>(gridDim.x);
-        int nst = st;
-        Item nit = it;
-        Stream nss = ss;
-        if (nitem < total) {
-            while (nst + 1 < a.n_steps && nitem >= a.first_item[nst + 1]) ++nst;
-            nit = item_of<1>(a.step[nst], nitem - a.first_item[nst], tid);
-            nss = stream_of(a.step[nst], nit);
-            prefetch<U, true>(buf, nss);
-        }
-        if (it.ks > 1) {
-            if (tid == 0) {
-                const int last = prev == unsigned(it.ks - 1);
-                if (last) __hip_atomic_store(ticket_of(p, it), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                s_last = last;
-            }
-            __syncthreads();
-            if (s_last) {
-                gather_panel<1, kStoreChain>(p, it, tid);
-                __builtin_amdgcn_s_waitcnt(0);
-                __syncthreads();
-                if (tid == 0) raise_flag(a, st, it);
-            }
-        }
-        __syncthreads();   // LDS is reused by the next item
-        item = nitem;
-        st = nst;
-        it = nit;
-        ss = nss;
-    }
-    // leave: the last workgroup out clears the completion flags for the next launch
-    __syncthreads();
-    if (tid == 0) {
-        __builtin_amdgcn_s_waitcnt(0);
-        const unsigned prev = __hip_atomic_fetch_add(a.sync + 1, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = prev == gridDim.x - 1;
-    }
-    __syncthreads();
-    if (s_last) {
-        for (int i = tid; i < a.flag_off[a.n_steps]; i += kThreads)
-            __hip_atomic_store(a.flags + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (tid == 0) __hip_atomic_store(a.sync + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-}
-
 // y = 0 (and its bf16 copy) for K == 0: the empty sum.
 __global__ void zero_output_kernel(float* y, int64_t ldy, int64_t sy, uint16_t* ybf, int64_t group,
                                    int64_t keep, int64_t ldm, int64_t sb, int64_t M, int64_t N,
@@ -1414,39 +1238,7 @@ size_t gemv_kv_lds_bytes(const GemvPlan& p, int kv, int rope) {
     return std::max(gemv_lds_bytes(p), size_t(2 * kv + rope + kWaves) * 4);
 }
 
-bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n) {
-    if (n < 1 || n > kChainMax) return false;
-    for (int i = 0; i < n; ++i)
-        if (a[i].dt != NMM_BF16 || a[i].M != 1 || a[i].K == 0 || a[i].N == 0 || a[i].batch == 0 ||
-            p[i].mt != 1 || p[i].unroll != p[0].unroll ||
-            (p[i].unroll != 4 && p[i].unroll != 8 && p[i].unroll != 16))
-            return false;
-    return true;
-}
-
-int chain_flags(const GemvArgs* a, const GemvPlan* p, int n) {
-    int64_t total = 0;
-    for (int i = 0; i < n; ++i) total += a[i].batch * p[i].mblocks * (p[i].n_full + (p[i].tail_chunks ? 1 : 0));
-    return static_cast<int>(std::min<int64_t>(total, int64_t(1) << 30));
-}
-
 namespace {
-
-template <int U>
-nmm_status launch_chain_u(const ChainArgs& ca, int grid, size_t lds, hipStream_t s) {
-    // never more workgroups than the device holds at once: the dependency waits rely on it
-    int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, chain_kernel<U>, kThreads, lds) != hipSuccess ||
-        per_cu < 1)
-        return NMM_ERR_HIP;
-    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus < 1)
-        return NMM_ERR_HIP;
-    grid = std::max(1, std::min(grid, per_cu * cus));
-    hipLaunchKernelGGL(chain_kernel<U>, dim3(static_cast<uint32_t>(grid)), dim3(kThreads), lds, s, ca);
-    return last_launch_status();
-}
-
 
 // ---------------------------------------------------------------------------------------------
 // The decode chain's per-head pair W_UK -> W_UV in one launch (bf16, M = 1).  Head h's two
@@ -1594,37 +1386,6 @@ nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, con
     hipLaunchKernelGGL(head_pair_kernel<kPairUnroll>, dim3(static_cast<uint32_t>(heads)), dim3(kThreads), 0,
                        static_cast<hipStream_t>(stream), pp);
     return last_launch_status();
-}
-
-namespace {
-}  // namespace
-
-nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
-                        unsigned* const* tickets, float* const* part, int grid, void* stream) {
-    ChainArgs ca{};
-    ca.n_steps = n;
-    ca.sync = sync;
-    ca.flags = flags;
-    ca.spin_limit = 1 << 22;   // ~ a second of polling: far beyond any legitimate wait
-    ca.sleep_reps = 1;
-    if (const char* e = std::getenv("NMM_CHAIN_SLEEP")) ca.sleep_reps = std::max(1, std::atoi(e));
-    size_t lds = 0;
-    int first = 0, fo = 0;
-    for (int i = 0; i < n; ++i) {
-        ca.step[i] = make_params(a[i], p[i], tickets[i], part[i]);
-        ca.first_item[i] = first;
-        ca.flag_off[i] = fo;
-        first += static_cast<int>(p[i].grid);
-        fo += static_cast<int>(a[i].batch * p[i].mblocks * (p[i].n_full + (p[i].tail_chunks ? 1 : 0)));
-        lds = std::max(lds, gemv_lds_bytes(p[i]));
-    }
-    ca.first_item[n] = first;
-    ca.flag_off[n] = fo;
-    grid = std::max(1, std::min(grid, first));
-    const hipStream_t s = static_cast<hipStream_t>(stream);
-    if (p[0].unroll == 16) return launch_chain_u<16>(ca, grid, lds, s);
-    if (p[0].unroll == 8) return launch_chain_u<8>(ca, grid, lds, s);
-    return launch_chain_u<4>(ca, grid, lds, s);
 }
 
 }  // namespace nmm

@@ -105,7 +105,7 @@ nmm_status plan_gemv_nt(int64_t M, int64_t K, int64_t N, NtPlan* p);
 // Pure host functions (no HIP calls): argument checks and the partition.
 nmm_status validate_gemv(const GemvArgs& a, int path);
 // unroll > 0 requests that many row-steps in flight (2, 4, 8, or 16 for tiles of <= 2 rows);
-// 0 takes the default (NMM_GEMV_UNROLL overrides it).
+// 0 takes the default.
 nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int path, GemvPlan* p,
                      int unroll = 0);
 nmm_status validate_workspace(const void* ws, size_t bytes, size_t need);
@@ -131,13 +131,6 @@ nmm_status launch_gemv_qrope(const GemvArgs& a, const GemvPlan& p, unsigned* tic
                              float theta, void* stream);
 size_t gemv_kv_lds_bytes(const GemvPlan& p, int kv, int rope);
 
-// The fused decode chain: n (<= 5) M = 1 bf16 GEMVs in one persistent launch.  `sync` points to
-// the chain's words in the counter block: [1] exited workgroups, [2] error word (sticky);
-// `flags` to chain_flags() completion flags, one per panel of every MatMul.  [1] and the flags
-// are zero before and after a launch.
-constexpr int kChainSyncWords = 8;
-int chain_flags(const GemvArgs* a, const GemvPlan* p, int n);
-bool chain_fusable(const GemvArgs* a, const GemvPlan* p, int n);
 nmm_status launch_mfma(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, float* part, void* stream);
 size_t mfma_lds_bytes(const GemvPlan& p);
 int device_cus();   // compute units of the current device
@@ -148,8 +141,6 @@ constexpr int kPairUnroll = 16;
 bool head_pair_ok(int64_t heads, int64_t nope, int64_t kv_lora, int64_t v_head);
 nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
                             float* lat, void* lat_bf16, float* o, void* o_bf16, void* stream);
-nmm_status launch_chain(const GemvArgs* a, const GemvPlan* p, int n, unsigned* sync, unsigned* flags,
-                        unsigned* const* tickets, float* const* part, int grid, void* stream);
 
 // One latent-attention call (the arguments of nmm_latent_attention_ex).
 struct AttnArgs {

@@ -25,13 +25,29 @@ int next_pow2(int64_t v) {
     return p;
 }
 
-// Tuning overrides (read once per call; unset in normal use).
-int64_t env_int(const char* name, int64_t dflt) {
+// The partition's tuning constants are fixed in the library, so a plan (and with it the order of
+// every sum) depends on the shape alone.  Only a library built with -DNMM_TUNING_ENV, for tuning
+// sweeps, lets the environment override them; the library as built for use reads no environment.
+int64_t tuned(const char* name, int64_t dflt) {
+#ifdef NMM_TUNING_ENV
     const char* s = std::getenv(name);
     if (!s || !*s) return dflt;
     char* end = nullptr;
     long long v = std::strtoll(s, &end, 10);
     return (end && *end == '\0' && v > 0) ? v : dflt;
+#else
+    (void)name;
+    return dflt;
+#endif
+}
+
+bool tuned_set(const char* name) {
+#ifdef NMM_TUNING_ENV
+    return std::getenv(name) != nullptr;
+#else
+    (void)name;
+    return false;
+#endif
 }
 
 int m_tile_for(int64_t M) {
@@ -98,8 +114,8 @@ nmm_status plan_mfma(int64_t M, int64_t K, int64_t N, GemvPlan* p) {
         return NMM_OK;
     }
     const int64_t panels = int64_t(q.mblocks) * q.n_full;
-    const int64_t want = env_int("NMM_GEMV_TARGET", kMfmaTargetGrid);
-    const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", 16);
+    const int64_t want = tuned("NMM_GEMV_TARGET", kMfmaTargetGrid);
+    const int64_t ks_cap = tuned("NMM_GEMV_MAXSPLIT", 16);
     int64_t ks_want = 1;
     const double ratio = double(want) / double(panels);
     while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;
@@ -133,7 +149,7 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     GemvPlan q;
     // AUTO: the streaming GEMV up to the measured crossover, the matrix cores above it (single
     // matrices only; batched calls always stream).
-    const int64_t mfma_min_m = env_int("NMM_MFMA_MIN_M", kMfmaMinMDefault);
+    const int64_t mfma_min_m = tuned("NMM_MFMA_MIN_M", kMfmaMinMDefault);
     if (path == NMM_PATH_AUTO) path = (batch <= 1 && M >= mfma_min_m) ? NMM_PATH_MFMA : NMM_PATH_GEMV;
     if (path == NMM_PATH_MFMA) {
         if (batch > 1) return NMM_ERR_PATH;
@@ -152,7 +168,7 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     // flight and more workgroups.
     const bool narrow_m = q.mt <= 2;
     const bool deep = narrow_m && w_bytes <= int64_t(100) << 20;
-    q.unroll = unroll > 0 ? unroll : static_cast<int>(env_int("NMM_GEMV_UNROLL", deep ? 16 : narrow_m ? 8 : 4));
+    q.unroll = unroll > 0 ? unroll : static_cast<int>(tuned("NMM_GEMV_UNROLL", deep ? 16 : narrow_m ? 8 : 4));
     if (q.unroll != 2 && q.unroll != 4 && q.unroll != 8 && q.unroll != 16) q.unroll = 8;
     if (q.unroll == 16 && q.mt > 2) q.unroll = 8;                  // 16 only for 1- and 2-row tiles
     const int U = q.unroll;
@@ -160,21 +176,21 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     // chunks (64 for 16-row tiles and for 1-2-row tiles of weights over 100 MB), while the launch
     // still has >= 24 panels in total and every row is split into >= 2 panels; never narrower
     // than 8 chunks (128-byte row segments).
-    int min_cw = static_cast<int>(env_int("NMM_GEMV_MINCW", 8));
+    int min_cw = static_cast<int>(tuned("NMM_GEMV_MINCW", 8));
     if (min_cw > kPanelChunks || (min_cw & (min_cw - 1))) min_cw = 8;
-    int cw = static_cast<int>(env_int("NMM_GEMV_MAXCW", (q.mt >= 16 || (narrow_m && !deep)) ? 64 : 32));
+    int cw = static_cast<int>(tuned("NMM_GEMV_MAXCW", (q.mt >= 16 || (narrow_m && !deep)) ? 64 : 32));
     if (cw > kPanelChunks || (cw & (cw - 1)) || cw < min_cw) cw = std::max(min_cw, 32);
     // Workgroups wanted: one per ~100 KB of W, between 256 and 768 (fewer leave HBM idle; more
     // only add split-K gather work); 256 for the deep-prefetch plans.
-    const int64_t want = env_int("NMM_GEMV_TARGET",
+    const int64_t want = tuned("NMM_GEMV_TARGET",
                                  narrow_m ? 256 : std::max<int64_t>(256, std::min<int64_t>(768, w_bytes / 100000)));
     while (cw > min_cw && (mats * cdiv(chunks, cw) < 24 || chunks < 2 * cw)) cw /= 2;
     // deep plans trade K-slices for narrower panels while twice the panels still fit the target
-    if (deep && U == 16 && !std::getenv("NMM_GEMV_MAXCW"))
+    if (deep && U == 16 && !tuned_set("NMM_GEMV_MAXCW"))
         while (cw > min_cw && 2 * mats * cdiv(chunks, cw) <= want) cw /= 2;
     // K-slices per panel: the power of two nearest want / panels, capped (fewer for tall row
     // tiles, whose partial sums are MT times larger)
-    const int64_t ks_cap = env_int("NMM_GEMV_MAXSPLIT", q.mt >= 8 ? 8 : 16);
+    const int64_t ks_cap = tuned("NMM_GEMV_MAXSPLIT", q.mt >= 8 ? 8 : 16);
     q.cw_full = cw;
     q.n_full = static_cast<int>(chunks / cw);
     q.tail_chunks = static_cast<int>(chunks % cw);
@@ -201,7 +217,7 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     int64_t ks_want = 1;
     {
         const double ratio = double(want) / double(std::max<int64_t>(panels_all, 1));
-        if (env_int("NMM_GEMV_KS_ANY", 0) > 0) {
+        if (tuned("NMM_GEMV_KS_ANY", 0) > 0) {
             ks_want = std::max<int64_t>(1, std::min<int64_t>(ks_cap, int64_t(ratio + 0.5)));
         } else {
             while (ks_want < ks_cap && double(ks_want) * 1.41421356 < ratio) ks_want *= 2;   // nearest power of two
@@ -289,11 +305,11 @@ nmm_status plan_gemv_nt(int64_t M, int64_t K, int64_t N, NtPlan* p) {
     // at most 8 rows per wave: short rows (small K) then spread over more workgroups, which
     // measured faster for W_UQ's [24576, 1536] (768 workgroups) than 24 rows per wave
     int r = static_cast<int>(std::min<int64_t>(8, std::max<int64_t>(1, N / (4 * target_rb))));
-    r = static_cast<int>(std::min<int64_t>(32, std::max<int64_t>(1, env_int("NMM_NT_ROWS", r))));
+    r = static_cast<int>(std::min<int64_t>(32, std::max<int64_t>(1, tuned("NMM_NT_ROWS", r))));
     q.rgroup = r >= 8 ? 8 : r >= 4 ? 4 : r >= 2 ? 2 : 1;
-    const int rg = env_int("NMM_NT_GROUP", q.rgroup);
+    const int rg = tuned("NMM_NT_GROUP", q.rgroup);
     if (rg == 1 || rg == 2 || rg == 4 || rg == 8) q.rgroup = rg;
-    q.depth = (q.mt == 1 && env_int("NMM_NT_DEPTH", 8) == 16) ? 16 : 8;
+    q.depth = (q.mt == 1 && tuned("NMM_NT_DEPTH", 8) == 16) ? 16 : 8;
     q.r = (r + q.rgroup - 1) / q.rgroup * q.rgroup;
     const int64_t rb = cdiv(N, 4 * q.r);
     if (rb >= kLimit) return NMM_ERR_SHAPE;

@@ -180,15 +180,3 @@ def test_step_with_no_attention_heads_is_the_chain():
     for k in OUTPUTS:
         assert torch.equal(bufs[k].view(torch.int16) if bufs[k].dtype == torch.bfloat16 else bufs[k],
                            sep[k].view(torch.int16) if sep[k].dtype == torch.bfloat16 else sep[k]), k
-
-
-def test_step_with_the_pair_off_matches_the_chain_with_the_pair_off(monkeypatch):
-    # W_UK and W_UV as two batched launches (NMM_CHAIN_PAIR=0): the step follows the chain
-    monkeypatch.setenv("NMM_CHAIN_PAIR", "0")
-    step = syn.decode_step()
-    q, kv, out, outb = attn_bufs(step.q, step.kv, syn.ATTN_DV)
-    bufs = alloc_chain(step)
-    nmm.nmm_mla_decode_step(step.dims, bufs, dict(q=q, kv=kv, out=out, out_bf16=outb, scale=step.scale, splits=16))
-    torch.cuda.synchronize()
-    sep, out2, outb2 = run_separately(step, q, kv, step.scale, 16, syn.ATTN_DQK, syn.ATTN_DV)
-    assert_same(bufs, sep, out, out2, outb, outb2)

@@ -148,61 +148,6 @@ def test_mfma_launch_stays_in_bounds(M, K, N, ldx, ldw):
     assert p["grid"] == p["m_blocks"] * panels * ks
 
 
-def chain_steps(d):
-    """The fused chain's five MatMuls: (batch, K, N, x batch stride, hand-off group, keep, hand-off
-    batch stride), as nmm_mla_decode_chain builds them."""
-    n_down, qk, H = d["q_lora"] + d["kv_lora"] + d["rope"], d["nope"] + d["rope"], d["heads"]
-    return [
-        (1, d["hidden"], n_down, 0, n_down, d["q_lora"], 0),
-        (1, d["q_lora"], H * qk, 0, qk, d["nope"], 0),
-        (H, d["nope"], d["kv_lora"], d["nope"], d["kv_lora"], d["kv_lora"], d["kv_lora"]),
-        (H, d["kv_lora"], d["v_head"], d["kv_lora"], d["v_head"], d["v_head"], d["v_head"]),
-        (1, d["heads"] * d["v_head"], d["hidden"], 0, 0, 0, 0),
-    ]
-
-
-def producer_panel(plan, group, keep, sb, j):
-    # chain_kernel's inverse of the hand-off layout: bf16 element j -> producer panel
-    b, rem = (j // sb, j % sb) if sb > 0 else (0, j)
-    n = (rem // keep) * group + rem % keep
-    full_lg = (plan["panel_width"] - 1).bit_length()
-    n_panels = plan["n_full_panels"] + (1 if plan["tail_chunks"] else 0)
-    return b * n_panels + min(n >> (3 + full_lg), plan["n_full_panels"]), n_panels
-
-
-@pytest.mark.parametrize("dims", [
-    dict(hidden=7168, q_lora=1536, kv_lora=512, rope=64, heads=128, nope=128, v_head=128),
-    dict(hidden=1032, q_lora=264, kv_lora=136, rope=24, heads=6, nope=40, v_head=24),
-])
-@pytest.mark.parametrize("unroll", ["4", "16"])
-def test_chain_dependencies_cover_every_input(dims, unroll, monkeypatch):
-    # Every item of MatMul s+1 waits on the producer panels [qa, qb] derived from its K-slice;
-    # those must exist and must include every panel that wrote an element of the slice.
-    monkeypatch.setenv("NMM_GEMV_UNROLL", unroll)
-    steps = chain_steps(dims)
-    plans = [nmm.nmm_gemv_plan(1, K, N, nmm.NMM_BF16, nmm.NMM_PATH_GEMV, batch=B) for B, K, N, *_ in steps]
-    flags = [B * (p["n_full_panels"] + (1 if p["tail_chunks"] else 0)) for (B, *_), p in zip(steps, plans)]
-    assert sum(flags) + 8 + sum(B * (p["n_full_panels"] + (1 if p["tail_chunks"] else 0))
-                                for (B, *_), p in zip(steps, plans) if max(p["split_k_full"], p["split_k_tail"]) > 1) <= 16384
-    for s in range(1, 5):
-        B, K, N, sx, *_ = steps[s]
-        _, _, _, _, group, keep, sb = steps[s - 1]
-        pp, p = plans[s - 1], plans[s]
-        for b in range(B):
-            for item in range(p["items"]):
-                n_full_items = p["n_full_panels"] * p["split_k_full"]
-                sl, rows = ((item % p["split_k_full"], p["rows_full"]) if item < n_full_items
-                            else (item - n_full_items, p["rows_tail"]))
-                k0 = sl * rows
-                k1 = min(k0 + rows, K)
-                assert k0 < k1
-                qa, _ = producer_panel(pp, group, keep, sb, b * sx + k0)
-                qb, npan = producer_panel(pp, group, keep, sb, b * sx + k1 - 1)
-                assert 0 <= qa <= qb < flags[s - 1]
-                needed = {producer_panel(pp, group, keep, sb, b * sx + k)[0] for k in range(k0, k1)}
-                assert needed <= set(range(qa, qb + 1))
-
-
 @pytest.mark.parametrize("nope", [64, 128, 192, 512])
 def test_head_pair_loads_stay_in_bounds(nope):
     # head_pair_kernel: W_UK[h] is nope rows of 1 KB, W_UV[h] 512 rows of 256 B; 16 row-steps
