@@ -3,7 +3,7 @@
  *
  * The library computes narrow matrix multiplications y = x . W in which x has only a few rows
  * (any M on either path; AUTO streams W on the vector units for one row and uses the matrix
- * cores from two rows on, see nmm_gemv), at the shapes of DeepSeek-V3
+ * cores from three rows on, and from two where that needs no K-split), at the shapes of DeepSeek-V3
  * Multi-head Latent Attention single-token decode.  The operation is the paper's problem
  * statement C = A x B with A in R^{M x K}, B in R^{K x N}, narrow when min(M, N) = 1
  * (Section II-E "Problem Statement"; Section III-A, Condition 2 "Narrow Dimension"), widened to
@@ -68,9 +68,11 @@ typedef enum {
 
 typedef enum { NMM_F16 = 1, NMM_BF16 = 2 } nmm_dtype;
 
-/* Which kernel family computes the product.  AUTO picks the streaming GEMV for M below the
- * measured crossover and the MFMA (matrix-core) path from it on (single matrices; batched calls
- * always stream); GEMV and MFMA force a family.  NMM_PATH_MFMA with batch > 1 is NMM_ERR_PATH. */
+/* Which kernel family computes the product.  AUTO picks from measured crossovers: the
+ * streaming GEMV for M = 1, the MFMA (matrix-core) path for M >= 3, and at M = 2 the MFMA path
+ * where its plan has a single K-slice (e.g. W_UQ [1536, 24576]), the GEMV otherwise (single
+ * matrices; batched calls always stream).  GEMV and MFMA force a family.  NMM_PATH_MFMA with
+ * batch > 1 is NMM_ERR_PATH.  The choice depends on the shape only. */
 typedef enum { NMM_PATH_AUTO = 0, NMM_PATH_GEMV = 1, NMM_PATH_MFMA = 2 } nmm_path;
 
 /*

@@ -29,6 +29,7 @@
 
 #include "attention_core.h"
 #include "bf16_cast.h"
+#include "handoff.h"
 #include "nmm_internal.h"
 
 namespace nmm {
@@ -420,8 +421,7 @@ __device__ __forceinline__ void gather_panel(const KParams& p, const Item& it, i
     }
 }
 
-// The panel's arrival counter.  The caller has waited for its partial stores (s_waitcnt 0) and
-// synchronised; the device-scope ticket then orders the hand-off without flushing the L2.
+// The panel's arrival counter (see arrive()).
 __device__ __forceinline__ unsigned* ticket_of(const KParams& p, const Item& it) {
     return p.tickets + (it.b * p.mblocks + it.mb) * p.n_panels + it.panel;
 }
@@ -462,11 +462,7 @@ __device__ __forceinline__ bool finish_panel(const KParams& p, const Item& it, i
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-        unsigned* t = ticket_of(p, it);
-        const unsigned prev = __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int last = prev == unsigned(it.ks - 1);
-        if (last) __hip_atomic_store(t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        *s_last = last;
+        *s_last = arrive(ticket_of(p, it), unsigned(it.ks));
     }
     __syncthreads();
     if (!*s_last) return false;
@@ -738,11 +734,7 @@ __global__ __launch_bounds__(kThreads) void gemv_nt_kernel(const NtParams p) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-        unsigned* tk = p.tickets + int64_t(mb) * p.row_blocks + rb;
-        const unsigned prev = __hip_atomic_fetch_add(tk, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int last = prev == unsigned(p.ks - 1);
-        if (last) __hip_atomic_store(tk, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = last;
+        s_last = arrive(p.tickets + int64_t(mb) * p.row_blocks + rb, unsigned(p.ks));
     }
     __syncthreads();
     if (!s_last) return;
@@ -862,10 +854,7 @@ __global__ __launch_bounds__(kThreads) void gemv_kv_kernel(const KParams p, cons
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-        const unsigned prev = __hip_atomic_fetch_add(e.done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int last = prev == unsigned(e.n_panels - 1);
-        if (last) __hip_atomic_store(e.done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = last;
+        s_last = arrive(e.done, unsigned(e.n_panels));
     }
     __syncthreads();
     if (s_last) kv_entry(p.y + e.c_off, e, lds, sn, cs);

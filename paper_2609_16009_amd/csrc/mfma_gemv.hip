@@ -25,6 +25,7 @@
 #include <cstdint>
 
 #include "bf16_cast.h"
+#include "handoff.h"
 #include "nmm_internal.h"
 
 namespace nmm {
@@ -233,11 +234,7 @@ __global__ __launch_bounds__(kThreads) void mfma_gemv_kernel(const MParams p) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) {
-        unsigned* t = p.tickets + int64_t(mb) * p.panels + panel;
-        const unsigned prev = __hip_atomic_fetch_add(t, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const int last = prev == unsigned(p.ks - 1);
-        if (last) __hip_atomic_store(t, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = last;
+        s_last = arrive(p.tickets + int64_t(mb) * p.panels + panel, unsigned(p.ks));
     }
     __syncthreads();
     if (!s_last) return;

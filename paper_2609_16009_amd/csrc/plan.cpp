@@ -147,10 +147,22 @@ nmm_status plan_gemv(int64_t batch, int64_t M, int64_t K, int64_t N, int dt, int
     if (batch < 0 || M < 0 || K < 0 || N < 0 || M >= kLimit || K >= kLimit || N >= kLimit)
         return NMM_ERR_SHAPE;
     GemvPlan q;
-    // AUTO: the streaming GEMV up to the measured crossover, the matrix cores above it (single
-    // matrices only; batched calls always stream).
-    const int64_t mfma_min_m = tuned("NMM_MFMA_MIN_M", kMfmaMinMDefault);
-    if (path == NMM_PATH_AUTO) path = (batch <= 1 && M >= mfma_min_m) ? NMM_PATH_MFMA : NMM_PATH_GEMV;
+    // AUTO (single matrices; batched calls always stream): the streaming GEMV for one row, the
+    // matrix cores from kMfmaMinMDefault rows on.  At two rows the matrix-core launch wins only
+    // where its plan needs no K-split: its split-K tail (16-row partials) costs more than the
+    // GEMV's second row.  Measured on MI355X: W_UQ [1536, 24576] (one slice) 15.8 against
+    // 16.3 us; W_O [16384, 7168] (4 slices) 42.2 against 41.1; down [7168, 2112] (16 slices)
+    // 14.0 against 10.3.
+    if (path == NMM_PATH_AUTO) {
+        const int64_t mfma_min_m = tuned("NMM_MFMA_MIN_M", kMfmaMinMDefault);
+        path = NMM_PATH_GEMV;
+        if (batch <= 1 && M >= mfma_min_m) {
+            path = NMM_PATH_MFMA;
+        } else if (batch <= 1 && M == 2 && K > 0 && N > 0) {
+            GemvPlan m;
+            if (plan_mfma(M, K, N, &m) == NMM_OK && m.ks_full == 1) path = NMM_PATH_MFMA;
+        }
+    }
     if (path == NMM_PATH_MFMA) {
         if (batch > 1) return NMM_ERR_PATH;
         return plan_mfma(M, K, N, p);

@@ -511,3 +511,13 @@ def test_prepared_step_refuses_invalid_sizes_before_any_launch():
     a = nmm._attn_struct(dict(attn, d_qk=576, splits=12))
     assert (a.heads, a.seq, a.d_qk, a.d_v, a.ldq, a.ld_kv, a.ldo, a.splits) == (4, 16, 576, 512, 577, 577, 512, 12)
     assert not a.out_bf16 and a.ldob == 0
+
+
+@pytest.mark.parametrize("M,K,N,want", [
+    (1, 1536, 24576, "gemv"), (2, 1536, 24576, "mfma"), (2, 16384, 7168, "gemv"), (2, 7168, 2112, "gemv"),
+    (3, 7168, 2112, "mfma"), (4, 16384, 7168, "mfma"), (1, 16384, 7168, "gemv")])
+def test_auto_path_per_shape(M, K, N, want):
+    # the measured crossovers: matrix cores from 3 rows, and at 2 rows where their plan has a
+    # single K-slice; the choice depends on the shape alone
+    code = {"gemv": nmm.NMM_PATH_GEMV, "mfma": nmm.NMM_PATH_MFMA}[want]
+    assert nmm.nmm_gemv_plan(M, K, N)["path"] == code

@@ -116,6 +116,32 @@ def test_deterministic_and_workspace_reuse():
     assert int(tickets.abs().sum()) == 0
 
 
+@pytest.mark.parametrize("K,N", [(7168, 2112), (16384, 7168), (7168, 576)], ids=["down", "w_o", "matmul2"])
+def test_split_k_soak_bit_identical(K, N):
+    # 1000 launches of a split-K shape on one workspace: every result equals the first bit for
+    # bit (the gather sums the slices in a fixed order, whichever XCD finishes first), and the
+    # arrival counters are back at zero after the last
+    c = syn.gemv_case(50, 1, K, N, syn.BF16, name=f"soak_{K}x{N}")
+    x, W = dev16(c.x, c.dt), dev16(c.W, c.dt)
+    ws = nmm.Workspace()
+    assert nmm.nmm_gemv_plan(1, K, N, syn.BF16, nmm.NMM_PATH_AUTO)["split_k_full"] > 1
+    ref = torch.empty((1, N), dtype=torch.float32, device="cuda")
+    nmm.nmm_gemv(x, W, ref, workspace=ws)
+    torch.cuda.synchronize()
+    y_ref, a_ref = oracle.gemv(c.x, c.W, c.dt)
+    assert_parity(ref, y_ref, a_ref, what=c.name)
+    ys = torch.empty((20, 1, N), dtype=torch.float32, device="cuda")
+    for batch in range(50):
+        ys.fill_(float("nan"))
+        for i in range(20):
+            nmm.nmm_gemv(x, W, ys[i], workspace=ws)
+        same = (ys == ref).all(dim=2).view(-1)
+        if not bool(same.all()):
+            first = batch * 20 + int((~same).nonzero()[0])
+            raise AssertionError(f"{c.name}: launch {first} differs from the first result")
+    assert int(ws.buf[:65536].view(torch.int32).abs().sum()) == 0
+
+
 def test_k_zero_writes_zeros_and_empty_is_noop():
     x = torch.zeros((2, 8), dtype=torch.bfloat16, device="cuda")
     W = torch.zeros((1, 16), dtype=torch.bfloat16, device="cuda")
@@ -211,7 +237,7 @@ def test_batched_ragged(B, M, K, N):
 
 # ------------------------------------------------------------------ matrix-core path
 
-@pytest.mark.parametrize("M", [1, 4, 5, 8, 16, 17, 32])
+@pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 8, 16, 17, 32])
 def test_uq_sweep_mfma_path(M):
     check_case(syn.uq_sweep(min(M, 32)) if M <= 32 else None, path=nmm.NMM_PATH_MFMA)
 
