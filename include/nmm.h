@@ -394,20 +394,23 @@ nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, i
 /*
  * nmm_mla_decode_step -- one decode step: the chain of nmm_mla_decode_chain and an independent
  * latent attention (the arguments of nmm_latent_attention_ex) on one stream, with the attention
- * run beside the chain's last MatMul instead of after it.  The paper's decode overlaps the narrow
+ * run beside the chain's MatMuls instead of after them.  The paper's decode overlaps the narrow
  * MatMuls with matrix-unit work that does not depend on them (Condition 1 "Data Independence",
- * Section III-A; Section IV-A).  Here the overlap is fixed by one launch: W_O's GEMV workgroups and
- * the attention's workgroups (splits position spans per block of 64 heads) share a grid, the
- * GEMV's streaming the weight while attention's use the compute units the GEMV leaves free; the
- * attention's merge follows.  This needs d_qk = 576, d_v = 512 and the chain's W_O in its
- * single-row bf16 form; other shapes run the attention after W_O (same results).
+ * Section III-A; Section IV-A).  Here the overlap is fixed by the launches: the attention's
+ * workgroups (splits position spans per block of 32 heads) share W_UQ's grid, the GEMV's streaming
+ * the weight while attention's use the compute units it leaves free, and the merge of the spans
+ * rides on extra workgroups of W_O's launch.  With the cache entry (kv_cache), whose workgroup
+ * takes W_UQ's launch, the attention and its merge share W_O's launch instead.  This needs
+ * d_qk = 576, d_v = 512 and the chain's MatMuls in their single-row bf16 form; other shapes run the
+ * attention in its own launches (same results).
  *
  * Results: every chain output as nmm_mla_decode_chain writes it, and out / out_bf16 as
  * nmm_latent_attention_ex writes them for the same splits (the same kernels' arithmetic).  The
  * attention must be independent of the chain: its q, kv, out and out_bf16 may not overlap any
  * buffer the chain writes (the cache row included), and out / out_bf16 no buffer the chain reads
- * (NMM_ERR_ARG).  Same limits as the two calls; `events` as in nmm_mla_decode_chain (event 4 is
- * recorded before the shared launch, event 5 after the merge).  Workspace: nmm_mla_decode_step_workspace_size.
+ * (NMM_ERR_ARG).  Same limits as the two calls; `events` as in nmm_mla_decode_chain (each is
+ * recorded before the launch that carries its MatMul, event 5 after the last launch).  Workspace:
+ * nmm_mla_decode_step_workspace_size.
  */
 typedef struct {
     int64_t heads, seq, d_qk, d_v;   /* DeepSeek-V3: 128 heads, 576, 512 */

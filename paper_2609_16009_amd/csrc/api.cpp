@@ -556,8 +556,10 @@ size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain) {
 
 namespace {
 
-// The chain's launches; with `att`, W_O and the attention share one launch (launch_gemv_attention)
-// and the attention's workspace follows the chain's at a 256-byte boundary.
+// The chain's launches.  With `att`, the attention's workgroups share W_UQ's launch and its merge
+// shares W_O's (with the cache entry, which takes a spare workgroup of W_UQ's launch, attention and
+// merge both share W_O's instead); the attention's workspace follows the chain's at a 256-byte
+// boundary.
 nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* workspace, size_t workspace_bytes,
                      void* stream) {
     if (!chain) return NMM_ERR_NULL;
@@ -600,6 +602,7 @@ nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* work
             if (!c.events[i]) return NMM_ERR_NULL;
     }
     hipStream_t s = static_cast<hipStream_t>(stream);
+    void* const att_mem = att_ws ? static_cast<uint8_t*>(workspace) + att_off : nullptr;
     // W_UK and W_UV run as one launch, one workgroup per head, where the dimensions allow it;
     // events 2 and 3 are then recorded together before it
     const bool pair = head_pair_ok(c.heads, c.nope, c.kv_lora, c.v_head);
@@ -625,9 +628,14 @@ nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* work
             const KvEpilogue e = kv_epilogue(c.kv_gamma, c.kv_eps, c.rope_theta, c.position, c.kv_cache, c.ld_cache,
                                              c.q_lora, c.kv_lora, c.rope, c.round, nullptr);
             st = launch_gemv_entry(ch.step[1], ch.plan[1], tickets, part, e, c.down_f32 + c.q_lora, stream);
+        } else if (i == 1 && att) {
+            // attention's workgroups on the compute units W_UQ leaves free; its merge rides in
+            // W_O's launch
+            st = launch_gemv_beside_attention(ch.step[1], ch.plan[1], tickets, part, *att, att_mem, att_ws, stream);
+        } else if (i == 4 && att && c.kv_cache) {
+            st = launch_gemv_attention(ch.step[4], ch.plan[4], tickets, part, *att, att_mem, att_ws, stream);
         } else if (i == 4 && att) {
-            st = launch_gemv_attention(ch.step[4], ch.plan[4], tickets, part, *att,
-                                       att_ws ? static_cast<uint8_t*>(workspace) + att_off : nullptr, att_ws, stream);
+            st = launch_gemv_merge(ch.step[4], ch.plan[4], tickets, part, *att, att_mem, att_ws, stream);
         } else {
             st = launch_gemv(ch.step[i], ch.plan[i], tickets, part, stream);
         }

@@ -50,51 +50,8 @@ void attention_kernel(const AttnParams p) {
     attention_block<HT, 8, KS, NTW, EXACT>(p, blockIdx.x);
 }
 
-// Merge the spans of each head in span order:
-//   out = sum_s w_s O_s / sum_s w_s l_s,  w_s = 2^(m_s - M),  M = max_s m_s.
-// A workgroup owns one head and 256 of its columns.  Lane s of every wave loads span s's (m, l)
-// (at most 64 spans), so M and the normaliser come from one load and fixed-order butterflies;
-// each thread then loads its column of every span at once and sums them in span order, the
-// weights taken from lane s.  The merge waits for about two memory round trips.
-constexpr int kMergeThreads = 256;
-constexpr int kMergeBatch = 32;
 __global__ __launch_bounds__(kMergeThreads) void attention_merge_kernel(const AttnParams p) {
-    const int n_cb = (p.dv + kMergeThreads - 1) / kMergeThreads;
-    const int h = blockIdx.x / n_cb, cb = blockIdx.x - h * n_cb;
-    const int n = cb * kMergeThreads + threadIdx.x;
-    const int lane = threadIdx.x & 63;
-    const int hb = h / p.hbh, hl = h - hb * p.hbh;
-    const int64_t base = int64_t(hb) * p.nsp * p.hbh + hl;      // (block, span 0, head) row
-    const float* src = p.part_o + base * p.dv + n;
-    const int64_t o_step = int64_t(p.hbh) * p.dv;
-    const bool active = n < p.dv;
-    // the partial outputs first (their loads are independent of the weights)
-    float v[kMergeBatch];
-#pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u) v[u] = (active && u < p.nsp) ? src[u * o_step] : 0.f;
-    float2 m_l = float2{-INFINITY, 0.f};
-    if (lane < p.nsp) m_l = *reinterpret_cast<const float2*>(p.part_ml + (base + int64_t(lane) * p.hbh) * 2);
-    float M = m_l.x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
-    const float w = (m_l.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_l.x - M);
-    float den = w * m_l.y;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) den += __shfl_xor(den, off);
-    float acc = 0.f;
-    for (int s0 = 0; s0 < p.nsp; s0 += kMergeBatch) {
-        if (s0 > 0) {
-#pragma unroll
-            for (int u = 0; u < kMergeBatch; ++u) v[u] = (active && s0 + u < p.nsp) ? src[(s0 + u) * o_step] : 0.f;
-        }
-#pragma unroll
-        for (int u = 0; u < kMergeBatch; ++u)
-            if (s0 + u < p.nsp) acc += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u)) * v[u];
-    }
-    if (!active) return;
-    const float r = acc / den;
-    p.out[int64_t(h) * p.ldo + n] = r;
-    if (p.outb) p.outb[int64_t(h) * p.ldob + n] = to_bf16_bits(r);
+    merge_block(p, static_cast<int>(blockIdx.x));
 }
 
 struct AttnPlan {
@@ -238,10 +195,13 @@ nmm_status launch_attention_merge(const AttnLaunch& l, hipStream_t s) {
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
 }
 
-nmm_status launch_prepared_attention(const AttnLaunch& l, hipStream_t s) {
+nmm_status launch_attention_kernel(const AttnLaunch& l, hipStream_t s) {
     if (l.grid == 0) return NMM_OK;
-    const nmm_status st = l.variant == kAttnExact ? launch_attention<true>(l.p, l.grid, s)
-                                                  : launch_attention<false>(l.p, l.grid, s);
+    return l.variant == kAttnExact ? launch_attention<true>(l.p, l.grid, s) : launch_attention<false>(l.p, l.grid, s);
+}
+
+nmm_status launch_prepared_attention(const AttnLaunch& l, hipStream_t s) {
+    const nmm_status st = launch_attention_kernel(l, s);
     if (st != NMM_OK) return st;
     return launch_attention_merge(l, s);
 }

@@ -486,6 +486,58 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     }
 }
 
+// Merge the spans of each head in span order:
+//   out = sum_s w_s O_s / sum_s w_s l_s,  w_s = 2^(m_s - M),  M = max_s m_s.
+// Merge block `blk` owns one head and kMergeThreads of its columns (heads x ceil(d_v / 256)
+// blocks in all).  Lane s of every wave loads span s's (m, l) (at most 64 spans), so M and the
+// normaliser come from one load and fixed-order butterflies; each thread then loads its column of
+// every span at once and sums them in span order, the weights taken from lane s.  A block waits
+// for about two memory round trips.  Called by 256-thread workgroups: the merge launch, or the
+// workgroups of a GEMV launch that carry the merge beside the GEMV.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeBatch = 32;
+__device__ __forceinline__ void merge_block(const AttnParams& p, int blk) {
+    // no contraction of its own: every translation unit that inlines this rounds alike (the
+    // products of the sum are explicit fused multiply-adds)
+#pragma clang fp contract(off)
+    const int n_cb = (p.dv + kMergeThreads - 1) / kMergeThreads;
+    const int h = blk / n_cb, cb = blk - h * n_cb;
+    const int n = cb * kMergeThreads + static_cast<int>(threadIdx.x);
+    const int lane = threadIdx.x & 63;
+    const int hb = h / p.hbh, hl = h - hb * p.hbh;
+    const int64_t base = int64_t(hb) * p.nsp * p.hbh + hl;      // (block, span 0, head) row
+    const float* src = p.part_o + base * p.dv + n;
+    const int64_t o_step = int64_t(p.hbh) * p.dv;
+    const bool active = n < p.dv;
+    // the partial outputs first (their loads are independent of the weights)
+    float v[kMergeBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) v[u] = (active && u < p.nsp) ? src[u * o_step] : 0.f;
+    float2 m_l = float2{-INFINITY, 0.f};
+    if (lane < p.nsp) m_l = *reinterpret_cast<const float2*>(p.part_ml + (base + int64_t(lane) * p.hbh) * 2);
+    float M = m_l.x;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+    const float w = (m_l.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_l.x - M);
+    float den = w * m_l.y;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) den += __shfl_xor(den, off);
+    float acc = 0.f;
+    for (int s0 = 0; s0 < p.nsp; s0 += kMergeBatch) {
+        if (s0 > 0) {
+#pragma unroll
+            for (int u = 0; u < kMergeBatch; ++u) v[u] = (active && s0 + u < p.nsp) ? src[(s0 + u) * o_step] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u)
+            if (s0 + u < p.nsp) acc = __builtin_fmaf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u)), v[u], acc);
+    }
+    if (!active) return;
+    const float r = acc / den;
+    p.out[int64_t(h) * p.ldo + n] = r;
+    if (p.outb) p.outb[int64_t(h) * p.ldob + n] = to_bf16_bits(r);
+}
+
 // A prepared attention call: kernel arguments, the attention grid (0: nothing to launch), the
 // merge grid (0: one span, no merge) and the kernel variant.
 constexpr int kAttnExact = 1;      // d_qk 576, d_v 512
@@ -502,5 +554,6 @@ struct AttnLaunch {
 nmm_status prepare_attention(const AttnArgs& a, void* workspace, size_t workspace_bytes, attn::AttnLaunch* out);
 nmm_status launch_prepared_attention(const attn::AttnLaunch& l, hipStream_t s);   // attention, then merge
 nmm_status launch_attention_merge(const attn::AttnLaunch& l, hipStream_t s);
+nmm_status launch_attention_kernel(const attn::AttnLaunch& l, hipStream_t s);      // attention alone, no merge
 
 }  // namespace nmm

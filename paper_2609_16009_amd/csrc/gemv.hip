@@ -510,6 +510,23 @@ void gemv_attention_kernel(const KParams p, const attn::AttnParams a, uint32_t g
     }
 }
 
+// A bf16 single-row GEMV with the merge of an attention launched earlier beside it: workgroups
+// [0, gemv_grid) are the GEMV's (exactly as in its own launch), the rest take the merge's blocks
+// in turn.  The merge reads only the attention's span partials, so it runs under the GEMV's
+// weight stream instead of after it.
+template <int U>
+__global__ __launch_bounds__(kThreads) void gemv_merge_kernel(const KParams p, const attn::AttnParams a,
+                                                             uint32_t gemv_grid, uint32_t merge_blocks) {
+    extern __shared__ float lds[];
+    __shared__ int s_last;
+    if (blockIdx.x < gemv_grid) {
+        gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
+    } else {
+        const uint32_t n = gridDim.x - gemv_grid;
+        for (uint32_t b = blockIdx.x - gemv_grid; b < merge_blocks; b += n) attn::merge_block(a, static_cast<int>(b));
+    }
+}
+
 // ---------------------------------------------------------------------------------------------
 // The transposed-weight GEMV: y[m, n] = sum_k x[m, k] * Wt[n, k] for Wt row-major [N, K] (the
 // layout of a torch Linear weight, and the one a dense y = x Wt^T GEMM reads).  Each output is
@@ -1049,20 +1066,26 @@ nmm_status launch_gemv(const GemvArgs& a, const GemvPlan& p, unsigned* tickets, 
     return last_launch_status();
 }
 
-nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
-                                 const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream) {
-    attn::AttnLaunch al;
-    nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
-    if (st != NMM_OK) return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+namespace {
+
+// Whether the GEMV can share a launch with attention's or the merge's workgroups: bf16, one row,
+// one batch entry, 8 or 16 row-steps in flight.
+bool shareable(const GemvArgs& g, const GemvPlan& gp) {
+    return g.dt == NMM_BF16 && g.batch == 1 && g.M == 1 && g.K > 0 && g.N > 0 && g.y && gp.mt == 1 &&
+           (gp.unroll == 8 || gp.unroll == 16);
+}
+
+// The GEMV and attention's workgroups in one launch where both fit it (the 576 / 512 attention,
+// the GEMV's LDS within one attention chunk buffer), else the two launches in order; no merge.
+nmm_status gemv_beside_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                                 const attn::AttnLaunch& al, hipStream_t s) {
     const bool fuse = al.grid > 0 && al.variant == attn::kAttnExact && al.p.pitch <= attn::kPitchMax &&
-                      g.dt == NMM_BF16 && g.batch == 1 && g.M == 1 && g.K > 0 && g.N > 0 && g.y && gp.mt == 1 &&
-                      (gp.unroll == 8 || gp.unroll == 16) &&
-                      gemv_lds_bytes(gp) <= size_t(attn::kCh) * attn::kPitchMax * 2 && gp.grid + al.grid < (int64_t(1) << 31);
+                      shareable(g, gp) && gemv_lds_bytes(gp) <= size_t(attn::kCh) * attn::kPitchMax * 2 &&
+                      gp.grid + al.grid < (int64_t(1) << 31);
     if (!fuse) {
-        st = launch_gemv(g, gp, tickets, part, stream);
+        nmm_status st = launch_gemv(g, gp, tickets, part, s);
         if (st != NMM_OK) return st;
-        return launch_prepared_attention(al, s);
+        return launch_attention_kernel(al, s);
     }
     const KParams kp = make_params(g, gp, tickets, part);
     const dim3 grid(static_cast<uint32_t>(gp.grid + al.grid));
@@ -1070,9 +1093,52 @@ nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned
         hipLaunchKernelGGL(gemv_attention_kernel<16>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(gp.grid));
     else
         hipLaunchKernelGGL(gemv_attention_kernel<8>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(gp.grid));
-    st = last_launch_status();
+    return last_launch_status();
+}
+
+}  // namespace
+
+nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                                 const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream) {
+    attn::AttnLaunch al;
+    nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
+    if (st != NMM_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    st = gemv_beside_attention(g, gp, tickets, part, al, s);
     if (st != NMM_OK) return st;
     return launch_attention_merge(al, s);
+}
+
+nmm_status launch_gemv_beside_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                                        const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream) {
+    attn::AttnLaunch al;
+    nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
+    if (st != NMM_OK) return st;
+    return gemv_beside_attention(g, gp, tickets, part, al, static_cast<hipStream_t>(stream));
+}
+
+nmm_status launch_gemv_merge(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                             const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream) {
+    attn::AttnLaunch al;
+    nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
+    if (st != NMM_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (al.merge_grid == 0 || !shareable(g, gp)) {
+        st = launch_gemv(g, gp, tickets, part, stream);
+        if (st != NMM_OK) return st;
+        return launch_attention_merge(al, s);
+    }
+    // one workgroup per merge block: they take the compute units the GEMV leaves free and share
+    // the others with its workgroups (no LDS of their own), so each waits only for its own loads
+    // -- under the GEMV's weight stream a memory round trip takes microseconds
+    const int64_t extra = al.merge_grid;
+    const KParams kp = make_params(g, gp, tickets, part);
+    const dim3 grid(static_cast<uint32_t>(gp.grid + extra));
+    const size_t lds = gemv_lds_bytes(gp);
+    const uint32_t gg = static_cast<uint32_t>(gp.grid), mb = static_cast<uint32_t>(al.merge_grid);
+    if (gp.unroll == 16) hipLaunchKernelGGL(gemv_merge_kernel<16>, grid, dim3(kThreads), lds, s, kp, al.p, gg, mb);
+    else hipLaunchKernelGGL(gemv_merge_kernel<8>, grid, dim3(kThreads), lds, s, kp, al.p, gg, mb);
+    return last_launch_status();
 }
 
 namespace {

@@ -163,5 +163,13 @@ nmm_status validate_attention_args(const AttnArgs& a, void* workspace, size_t wo
 // order.  The two must not touch each other's buffers.
 nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
                                  const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
+// The same shared launch without the merge (the attention's span partials stay in its workspace),
+// and a later GEMV launch that carries the merge: one extra workgroup per merge block in the
+// GEMV's launch where the GEMV allows it, else the merge launch after the GEMV.  Between the two,
+// nothing may write the attention's workspace or read its outputs.
+nmm_status launch_gemv_beside_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                                        const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
+nmm_status launch_gemv_merge(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
+                             const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
 
 }  // namespace nmm
