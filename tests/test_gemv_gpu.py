@@ -258,9 +258,11 @@ def test_mfma_ragged(M, K, N, dt, ldx, ldw):
 
 
 def test_auto_path_switches_at_crossover():
-    for M in (1, 2):
-        assert nmm.nmm_gemv_plan(M, 1536, 24576)["path"] == nmm.NMM_PATH_GEMV
-    for M in (3, 4, 16, 32):
+    # one row streams; W_UQ's matrix-core plan has a single K-slice, so two rows take the matrix
+    # cores there, while W_O's (split K) keeps the streaming GEMV at two rows
+    assert nmm.nmm_gemv_plan(1, 1536, 24576)["path"] == nmm.NMM_PATH_GEMV
+    assert nmm.nmm_gemv_plan(2, 16384, 7168)["path"] == nmm.NMM_PATH_GEMV
+    for M in (2, 3, 4, 16, 32):
         assert nmm.nmm_gemv_plan(M, 1536, 24576)["path"] == nmm.NMM_PATH_MFMA
     assert nmm.nmm_gemv_plan(16, 128, 512, batch=8)["path"] == nmm.NMM_PATH_GEMV
 
