@@ -106,6 +106,7 @@ __device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
 template <int W>
 struct Stage {
     static constexpr int kIns = (kPitchMax / 8 + W - 1) / W;   // instructions per wave
+    static constexpr int kMinPieces = (kPitchMax / 8 - (W - 1) + W - 1) / W;   // the fewest any wave issues
     uint32_t off[kIns];
     __device__ __forceinline__ void init(int spr, int64_t ldkv, int wave, int lane) {
 #pragma unroll
@@ -134,6 +135,14 @@ __device__ __forceinline__ void lds_sync() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Wait until at most N vector-memory operations of this wave are outstanding (N < 64).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(N >= 0 && N < 64, "vmcnt holds 6 bits");
+    // gfx9 encoding: vmcnt in bits 3:0 and 15:14; expcnt (6:4) and lgkmcnt (11:8) left at their maxima
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // LDS of the attention workgroup.  Every kernel that calls these gets the same arrays, so a kernel
 // whose other workgroups do other work (the GEMV beside attention) can use them as well.
 __device__ __forceinline__ uint16_t* chunk_buffer_a() {
@@ -153,7 +162,7 @@ __device__ __forceinline__ float* red_buffer() {
     return red;
 }
 __device__ __forceinline__ int* flag_buffer() {
-    __shared__ int flags[8];
+    __shared__ __attribute__((aligned(16))) int flags[8];
     return flags;
 }
 
@@ -219,11 +228,10 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     const __amdgpu_buffer_rsrc_t kvr = make_rsrc(p.kv, p.kv_extent);
     Stage<W> stg;
     stg.init(spr, p.ldkv, wave, lane);
-    // ---- the first chunk to buffer a and the block's Q rows to buffer b (LDS-direct loads of whole
-    // row pieces: fragment-shaped global loads, 16 rows x 64 bytes per instruction, ingest about
-    // four times slower).  Q rows past the last head and pieces past d_qk read zeros.
-#pragma unroll
-    for (int k = 0; k < Stage<W>::kIns; ++k) stg.piece(kv_a, kvr, k, spr, uint32_t(s_begin) * row_bytes, wave);
+    // ---- the block's Q rows to buffer b, then the first chunk to buffer a (LDS-direct loads of
+    // whole row pieces: fragment-shaped global loads, 16 rows x 64 bytes per instruction, ingest
+    // about four times slower).  Q rows past the last head and pieces past d_qk read zeros.  Q goes
+    // first so that its fragments can be read while the chunk is still landing.
     {
         const __amdgpu_buffer_rsrc_t qr = make_rsrc(p.q, p.q_extent);
         const int qcols = ksteps * 4;                  // 16-byte pieces of a Q row that are read
@@ -235,8 +243,14 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
             __builtin_amdgcn_raw_ptr_buffer_load_lds(qr, (lds_void*)(kv_b + ins * 64 * 8), 16, off, 0, 0, 0);
         }
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < Stage<W>::kIns; ++k) stg.piece(kv_a, kvr, k, spr, uint32_t(s_begin) * row_bytes, wave);
+    // this wave's Q pieces have landed once at most its chunk pieces are outstanding (loads
+    // complete in order; every wave issues at least kMinPieces of them at the full pitch), then
+    // every wave's
+    if constexpr (EXACT) wait_vm<Stage<W>::kMinPieces>();
+    else __builtin_amdgcn_s_waitcnt(0);
+    lds_sync();
     // the Q fragments of the wave's head tiles: head 16 (ht0 + t) + j, dims 32 u + 8 g .. + 7; then
     // buffer b is free for chunk 1
     i32x4 qf[HTW][KS];
@@ -246,6 +260,8 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
         for (int u = 0; u < KS; ++u)
             if (EXACT || u < ksteps)
                 qf[t][u] = *reinterpret_cast<const i32x4*>(kv_b + (16 * (ht0 + t) + j) * pitch + 8 * g + 32 * u);
+    // the first chunk has landed: this wave's pieces, then every wave's
+    __builtin_amdgcn_s_waitcnt(0);
     lds_sync();
 
     f32x4 o[NTW][HTW];      // O^T tiles: lane (g, j) holds columns 16 ct + 4 g .. + 3 of head 16 (ht0 + t) + j
@@ -351,8 +367,13 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
         }
         bool any = ck == 0;
         if (ck > 0) {
-#pragma unroll
-            for (int w = 0; w < W; ++w) any |= flags[w] != 0;
+            // every wave's flag in one or two 16-byte LDS reads
+            const i32x4 f0 = *reinterpret_cast<const i32x4*>(flags);
+            any = (f0[0] | f0[1] | f0[2] | f0[3]) != 0;
+            if constexpr (W == 8) {
+                const i32x4 f1 = *reinterpret_cast<const i32x4*>(flags + 4);
+                any |= (f1[0] | f1[1] | f1[2] | f1[3]) != 0;
+            }
         }
         // ---- a reference moves (the same decision in every wave: all read the same maxima): the
         // chunk maximum of each head, the output rescaled, and P written again
@@ -439,49 +460,43 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
         lsum[t] = ((red[hh] + red[HB + hh]) + red[2 * HB + hh]) + red[3 * HB + hh];
     }
 
-    // ---- the block's [HB][d_v] result into LDS (buffer a, free after the last chunk; rows padded
-    // by 4 floats to spread the banks), normalised when the span is the whole sequence
-    const int dvp = p.dv + 4;
-    float* const ob = reinterpret_cast<float*>(kv_a);
+    // ---- the block's [HB][d_v] result straight from the accumulators: lane (g, j) holds columns
+    // 16 ct + 4 g .. + 3 of its head, so each store instruction writes 64 contiguous bytes of 16
+    // rows; normalised when the span is the whole sequence, else the span's partial
     const bool whole = p.nsp == 1;
+    const int64_t pidx = int64_t(hb) * p.nsp + sp;
 #pragma unroll
     for (int t = 0; t < HTW; ++t) {
-        const float scl = whole ? 1.f / lsum[t] : 1.f;
-#pragma unroll
-        for (int i = 0; i < NTW; ++i) {
-            const int ct = pw + 4 * i;
-            if (EXACT || ct < ntiles)
-                *reinterpret_cast<f32x4*>(ob + (16 * (ht0 + t) + j) * dvp + 16 * ct + 4 * g) = o[i][t] * scl;
-        }
-    }
-    const int64_t pidx = int64_t(hb) * p.nsp + sp;
-    if (!whole && pw == 0 && g == 0) {
-#pragma unroll
-        for (int t = 0; t < HTW; ++t) {
-            float* pml = p.part_ml + (pidx * HB + 16 * (ht0 + t) + j) * 2;
-            *reinterpret_cast<float2*>(pml) = float2{m_ref[t], lsum[t]};
-        }
-    }
-    __syncthreads();
-    // ---- rows out: each store instruction writes 1 KB of one row
-    const int c4 = p.dv / 4;                         // 16-byte pieces per row
-    for (int idx = tid; idx < HB * c4; idx += 64 * W) {
-        const int row = idx / c4, c = idx - row * c4;
+        const int row = 16 * (ht0 + t) + j;
         const int h = h0 + row;
-        const f32x4 v = *reinterpret_cast<const f32x4*>(ob + row * dvp + 4 * c);
         if (whole) {
             if (h < p.heads) {
-                *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + 4 * c) = v;
-                if (p.outb) {
-                    uint16_t* d = p.outb + int64_t(h) * p.ldob + 4 * c;
-                    d[0] = to_bf16_bits(v[0]);
-                    d[1] = to_bf16_bits(v[1]);
-                    d[2] = to_bf16_bits(v[2]);
-                    d[3] = to_bf16_bits(v[3]);
+                const float scl = 1.f / lsum[t];
+#pragma unroll
+                for (int i = 0; i < NTW; ++i) {
+                    const int ct = pw + 4 * i;
+                    if (EXACT || ct < ntiles) {
+                        const f32x4 v = o[i][t] * scl;
+                        const int c = 16 * ct + 4 * g;
+                        *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + c) = v;
+                        if (p.outb) {
+                            uint16_t* d = p.outb + int64_t(h) * p.ldob + c;
+                            d[0] = to_bf16_bits(v[0]);
+                            d[1] = to_bf16_bits(v[1]);
+                            d[2] = to_bf16_bits(v[2]);
+                            d[3] = to_bf16_bits(v[3]);
+                        }
+                    }
                 }
             }
         } else {
-            *reinterpret_cast<f32x4*>(p.part_o + (pidx * HB + row) * int64_t(p.dv) + 4 * c) = v;
+            float* const dst = p.part_o + (pidx * HB + row) * int64_t(p.dv) + 4 * g;
+#pragma unroll
+            for (int i = 0; i < NTW; ++i) {
+                const int ct = pw + 4 * i;
+                if (EXACT || ct < ntiles) *reinterpret_cast<f32x4*>(dst + 16 * ct) = o[i][t];
+            }
+            if (pw == 0 && g == 0) *reinterpret_cast<float2*>(p.part_ml + (pidx * HB + row) * 2) = float2{m_ref[t], lsum[t]};
         }
     }
 }
