@@ -1302,9 +1302,11 @@ namespace {
 //   o_h   = lat'_h . W_UV[h]    ([512] x [512, 128]),    o'_h   = bf16(o_h)
 // It streams W_UK[h] and then W_UV[h] as one sequence of row-steps with U steps in flight, so
 // W_UV's first loads are out while W_UK's sums are reduced; no second launch, no split-K.
-//  * W_UK step t: wave w reads row 4t + w (1 KB, 16 bytes per lane).
-//  * W_UV step t: wave w reads rows 16t + 4w .. + 3 (256 bytes each, 16 lanes per row).
-// One workgroup per head leaves the rest of the device to the other stream's work.
+// With NW waves (8 where nope allows it, else 4):
+//  * W_UK step t: wave w reads row NW t + w (1 KB, 16 bytes per lane).
+//  * W_UV step t: wave w reads rows 4 NW t + 4w .. + 3 (256 bytes each, 16 lanes per row).
+// One workgroup per head covers half the device, so its bytes in flight decide the rate: 8 waves
+// of 16 row-steps keep all of W_UK[h] (128 KB at nope 128) in flight at once.
 // ---------------------------------------------------------------------------------------------
 constexpr int kPairLat = 512;     // kv_lora
 constexpr int kPairV = 128;       // v_head
@@ -1322,22 +1324,23 @@ struct PairParams {
     int nope;
 };
 
-template <int U>
-__global__ __launch_bounds__(kThreads) void head_pair_kernel(const PairParams p) {
+template <int U, int NW>
+__global__ __launch_bounds__(64 * NW) void head_pair_kernel(const PairParams p) {
     __shared__ __attribute__((aligned(16))) float xs[kPairMaxNope];   // q_nope of the head
-    __shared__ __attribute__((aligned(16))) float red[kWaves * kPairLat];
+    __shared__ __attribute__((aligned(16))) float red[NW * kPairLat];
     __shared__ float lat_s[kPairLat];                                 // lat'_h, widened
+    constexpr int kT = 64 * NW;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t h = blockIdx.x;
-    const int ta = p.nope / 4;                          // W_UK row-steps (a multiple of U)
-    constexpr int kTb = kPairLat / 16;                  // W_UV row-steps
+    const int ta = p.nope / NW;                         // W_UK row-steps (a multiple of U)
+    constexpr int kTb = kPairLat / (4 * NW);            // W_UV row-steps
     const __amdgpu_buffer_rsrc_t uk =
         make_rsrc(p.wuk + h * int64_t(p.nope) * kPairLat, uint32_t(p.nope) * kPairLat * 2);
     const __amdgpu_buffer_rsrc_t uv = make_rsrc(p.wuv + h * int64_t(kPairLat) * kPairV, kPairLat * kPairV * 2);
-    auto off_a = [&](int t) { return uint32_t((4 * t + wave) * (kPairLat * 2) + lane * 16); };
+    auto off_a = [&](int t) { return uint32_t((NW * t + wave) * (kPairLat * 2) + lane * 16); };
     auto off_b = [&](int t) {
-        return t < kTb ? uint32_t((16 * t + 4 * wave + (lane >> 4)) * (kPairV * 2) + (lane & 15) * 16) : kOutOfRange;
+        return t < kTb ? uint32_t((4 * NW * t + 4 * wave + (lane >> 4)) * (kPairV * 2) + (lane & 15) * 16) : kOutOfRange;
     };
 
     // q_nope_h first (8 values per lane), then the first U row-steps, then q to LDS
@@ -1364,25 +1367,25 @@ __global__ __launch_bounds__(kThreads) void head_pair_kernel(const PairParams p)
     for (; t0 + U < ta; t0 += U) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            fma_chunk<NMM_BF16, 1>(acc, buf[u], xs + 4 * (t0 + u) + wave);
+            fma_chunk<NMM_BF16, 1>(acc, buf[u], xs + NW * (t0 + u) + wave);
             buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uk, off_a(t0 + u + U), 0, kLoadNT);
             __builtin_amdgcn_sched_barrier(0);
         }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {   // the last U steps reload with W_UV's first U
-        fma_chunk<NMM_BF16, 1>(acc, buf[u], xs + 4 * (t0 + u) + wave);
+        fma_chunk<NMM_BF16, 1>(acc, buf[u], xs + NW * (t0 + u) + wave);
         buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uv, off_b(u), 0, kLoadNT);
         __builtin_amdgcn_sched_barrier(0);
     }
-    // the four waves' row sums, in wave order; lat and its bf16 rounding out, lat' to LDS
+    // the waves' row sums, in wave order; lat and its bf16 rounding out, lat' to LDS
     *reinterpret_cast<f32x4*>(red + wave * kPairLat + 8 * lane) = f32x4{acc[0][0], acc[0][1], acc[0][2], acc[0][3]};
     *reinterpret_cast<f32x4*>(red + wave * kPairLat + 8 * lane + 4) = f32x4{acc[0][4], acc[0][5], acc[0][6], acc[0][7]};
     lds_barrier();
-    for (int c = tid; c < kPairLat; c += kThreads) {
+    for (int c = tid; c < kPairLat; c += kT) {
         float v = red[c];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) v += red[w * kPairLat + c];
+        for (int w = 1; w < NW; ++w) v += red[w * kPairLat + c];
         const uint16_t b = to_bf16_bits(v);
         p.lat[h * kPairLat + c] = v;
         p.latb[h * kPairLat + c] = b;
@@ -1390,14 +1393,14 @@ __global__ __launch_bounds__(kThreads) void head_pair_kernel(const PairParams p)
     }
     lds_barrier();
 
-    // ---- o_h: rows 16t + 4 wave + lane / 16, columns 8 (lane % 16) .. + 7
+    // ---- o_h: rows 4 NW t + 4 wave + lane / 16, columns 8 (lane % 16) .. + 7
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[0][e] = 0.f;
     const int rsub = 4 * wave + (lane >> 4);
     for (int t = 0; t < kTb; t += U) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            fma_chunk<NMM_BF16, 1>(acc, buf[u], lat_s + 16 * (t + u) + rsub);
+            fma_chunk<NMM_BF16, 1>(acc, buf[u], lat_s + 4 * NW * (t + u) + rsub);
             buf[u] = __builtin_amdgcn_raw_buffer_load_b128(uv, off_b(t + u + U), 0, kLoadNT);
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -1413,7 +1416,7 @@ __global__ __launch_bounds__(kThreads) void head_pair_kernel(const PairParams p)
     if (tid < kPairV) {
         float v = red[tid];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) v += red[w * kPairV + tid];
+        for (int w = 1; w < NW; ++w) v += red[w * kPairV + tid];
         p.o[h * kPairV + tid] = v;
         p.ob[h * kPairV + tid] = to_bf16_bits(v);
     }
@@ -1438,8 +1441,12 @@ nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, con
     pp.o = o;
     pp.ob = static_cast<uint16_t*>(o_bf16);
     pp.nope = static_cast<int>(nope);
-    hipLaunchKernelGGL(head_pair_kernel<kPairUnroll>, dim3(static_cast<uint32_t>(heads)), dim3(kThreads), 0,
-                       static_cast<hipStream_t>(stream), pp);
+    if (nope % (8 * kPairUnroll) == 0)
+        hipLaunchKernelGGL((head_pair_kernel<kPairUnroll, 8>), dim3(static_cast<uint32_t>(heads)), dim3(8 * 64), 0,
+                           static_cast<hipStream_t>(stream), pp);
+    else
+        hipLaunchKernelGGL((head_pair_kernel<kPairUnroll, 4>), dim3(static_cast<uint32_t>(heads)), dim3(4 * 64), 0,
+                           static_cast<hipStream_t>(stream), pp);
     return last_launch_status();
 }
 
