@@ -656,9 +656,8 @@ def main() -> int:
     t = time.perf_counter()
     two_stream_graphs = [capture(decode_step, s) for s in range(args.copies)]
     one_launch_graphs = [capture(one_launch, s) for s in range(args.copies)]
-    alone = {name: [capture(fn, s) for s in range(args.copies)]
-             for name, fn in (("chain", chain_only), ("attention", attn_only), ("serial", serial))}
-    log(f"[bench] captured {5 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
+    alone = {name: [capture(fn, s) for s in range(args.copies)] for name, fn in (("serial", serial),)}
+    log(f"[bench] captured {3 * args.copies} HIP graphs in {time.perf_counter() - t:.1f}s")
 
     def timed(graphs, n):
         """Mean time per replay of n replays (graphs rotated), events on the replay stream."""
@@ -718,21 +717,22 @@ def main() -> int:
     segments = {n: round(sum(ev_slots[i][a].elapsed_time(ev_slots[i][b]) for i in range(K)) / K * 1e3, 2)
                 for n, a, b in seg}
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager)
-    log(f"[bench] decode step (one launch for W_O + attention): {step_ms * 1e3:.1f} us issued back to back "
+    log(f"[bench] decode step (attention beside W_UQ, its merge in W_O's launch): {step_ms * 1e3:.1f} us issued back to back "
         f"(host {host_ms * 1e3:.1f} us per call), {graph_ms * 1e3:.1f} us as graph replays; two streams: "
         f"{two_graph_ms * 1e3:.1f} us graph replays, {two_eager_ms * 1e3:.1f} us issued")
 
-    # ---- the overlap experiment: each stream alone, then both serially on one stream
-    timed(alone["chain"], W)
-    t_a = timed(alone["chain"], K)
-    timed(alone["attention"], W)
-    t_b = timed(alone["attention"], K)
-    # attention alone over the partitions it can take (0: the library's default), graph replays
+    # ---- the overlap experiment: each stream alone, then both serially on one stream.  Chain and
+    # attention alone are timed under the protocol (graphs of several calls, so a graph launch's
+    # own cost is spread over them): their GPU time per call
+    cur = torch.cuda.current_stream
+    t_a = protocol_us(torch, lambda i: chains[i % args.copies].launch(stream=cur()), args.copies,
+                      runs=21, iters=10)["mean"] * 1e-3
+    # attention alone over the partitions it can take (0: the library's default)
     t_b_by_splits = {}
     for sp in (0, 8, 16, 32, 64):
-        gs = [capture(lambda s, sp=sp: attention(s, cap, splits=sp), s) for s in range(args.copies)]
-        timed(gs, W)
-        t_b_by_splits[sp] = timed(gs, K)
+        t_b_by_splits[sp] = protocol_us(torch, lambda i, sp=sp: attention(i, cur(), splits=sp), args.copies,
+                                        runs=21, iters=20)["mean"] * 1e-3
+    t_b = t_b_by_splits[ATTN_OVERLAP_SPLITS]
     t_b_default = t_b_by_splits[0]
     best_splits = min(t_b_by_splits, key=t_b_by_splits.get)
     t_b_best = t_b_by_splits[best_splits]
