@@ -36,8 +36,10 @@
  *  - Results are deterministic: the same inputs give bit-identical outputs on every run.
  *  - Errors: every call validates all arguments before enqueueing anything.  On an error it
  *    returns a non-zero nmm_status, enqueues nothing and leaves the outputs untouched.  No
- *    exception crosses the ABI and nothing aborts.  NMM_ERR_HIP reports a failed launch; a
- *    device-side fault surfaces at the caller's next synchronisation.
+ *    exception crosses the ABI and nothing aborts.  NMM_ERR_HIP reports that the HIP runtime
+ *    returned an error after the call's launches (hipGetLastError): a failed launch, or an error
+ *    an earlier runtime call on this thread left unread, which the call reads and so clears.
+ *    A device-side fault surfaces at the caller's next synchronisation.
  *  - Empty problems: M == 0 or N == 0 is a no-op returning NMM_OK; K == 0 writes zeros (the
  *    empty sum).
  *  - Limits: every size and leading dimension must be < 2^31, each W matrix's extent must be

@@ -167,6 +167,34 @@ def test_invalid_call_enqueues_nothing():
     assert st == nmm.NMM_ERR_ALIGN and torch.all(y == 3.0)
 
 
+def _loaded_hip_runtime():
+    """The HIP runtime library this process has loaded (the one libnmm's calls go to)."""
+    import ctypes
+    with open("/proc/self/maps") as f:
+        paths = {line.split()[-1] for line in f if "libamdhip64.so" in line}
+    assert paths, "no HIP runtime loaded"
+    return ctypes.CDLL(sorted(paths)[0])
+
+
+def test_hip_error_reaches_the_caller_as_nmm_err_hip():
+    # NMM_ERR_HIP reports what the HIP runtime says after the launch: here an error left unread
+    # by an earlier runtime call on this thread (an invalid device ordinal, refused on the host;
+    # nothing reaches the GPU), which the call reports once and so clears
+    c = syn.gemv_case(5, 1, 256, 256, syn.BF16)
+    x, W = dev16(c.x, c.dt), dev16(c.W, c.dt)
+    y = torch.empty((1, 256), device="cuda")
+    torch.cuda.synchronize()
+    hip = _loaded_hip_runtime()
+    assert hip.hipSetDevice(1 << 20) != 0
+    args = (1, 256, 256, nmm.NMM_BF16, x.data_ptr(), 256, W.data_ptr(), 256, y.data_ptr(), 256, 0, None, 0, None)
+    assert nmm.lib().nmm_gemv(*args) == nmm.NMM_ERR_HIP
+    torch.cuda.synchronize()
+    assert nmm.lib().nmm_gemv(*args) == nmm.NMM_OK
+    torch.cuda.synchronize()
+    y_ref, a_ref = oracle.gemv(c.x, c.W, c.dt)
+    assert_parity(y, y_ref, a_ref)
+
+
 def test_infinity_propagates_to_its_column_only():
     c = syn.gemv_case(6, 1, 3000, 700, syn.BF16, ldw=704)
     W = c.W.copy()
