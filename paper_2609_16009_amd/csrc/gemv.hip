@@ -489,9 +489,10 @@ __global__ __launch_bounds__(kThreads) void gemv_kernel(const KParams p) {
 }
 
 // A bf16 single-row GEMV and an independent latent attention in one launch: workgroups
-// [0, gemv_grid) are the GEMV's (exactly as in its own launch, its x slice staged in the first of
-// attention's two chunk buffers), the rest are attention's, each a workgroup of the attention
-// launch.  The paper overlaps narrow MatMuls with independent matrix-core work (Condition 1 of
+// [0, attn_grid) are attention's, each a workgroup of the attention launch (dispatched first, so
+// they start as early as the GEMV's), the rest are the GEMV's, exactly as in its own launch (item
+// id = workgroup id - attn_grid, a multiple of 8, so every item keeps its XCD), the x slice
+// staged in the first of attention's two chunk buffers.  The paper overlaps narrow MatMuls with independent matrix-core work (Condition 1 of
 // Section III-A); here the overlap is fixed by the launch itself -- the GEMV's workgroups stream
 // the weight while attention's run on the compute units the GEMV leaves free -- instead of
 // depending on how two streams are scheduled.
@@ -500,13 +501,13 @@ static_assert(size_t(attn::kCh) * attn::kPitchMax * 2 >= size_t(kXStageBytes) &&
               "the GEMV's x slice and reduction fit the first chunk buffer");
 template <int U>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gemv_attention_kernel(const KParams p, const attn::AttnParams a, uint32_t gemv_grid) {
+void gemv_attention_kernel(const KParams p, const attn::AttnParams a, uint32_t attn_grid) {
     __shared__ int s_last;
-    if (blockIdx.x < gemv_grid) {
-        float* lds = reinterpret_cast<float*>(attn::chunk_buffer_a());
-        gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
+    if (blockIdx.x < attn_grid) {
+        attn::attention_block<attn::kHt, 4, attn::kMaxKs, attn::kMaxNtw, true>(a, static_cast<int>(blockIdx.x));
     } else {
-        attn::attention_block<attn::kHt, 4, attn::kMaxKs, attn::kMaxNtw, true>(a, static_cast<int>(blockIdx.x - gemv_grid));
+        float* lds = reinterpret_cast<float*>(attn::chunk_buffer_a());
+        gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x - attn_grid, lds, &s_last);
     }
 }
 
@@ -1090,9 +1091,9 @@ nmm_status gemv_beside_attention(const GemvArgs& g, const GemvPlan& gp, unsigned
     const KParams kp = make_params(g, gp, tickets, part);
     const dim3 grid(static_cast<uint32_t>(gp.grid + al.grid));
     if (gp.unroll == 16)
-        hipLaunchKernelGGL(gemv_attention_kernel<16>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(gp.grid));
+        hipLaunchKernelGGL(gemv_attention_kernel<16>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(al.grid));
     else
-        hipLaunchKernelGGL(gemv_attention_kernel<8>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(gp.grid));
+        hipLaunchKernelGGL(gemv_attention_kernel<8>, grid, dim3(kThreads), 0, s, kp, al.p, static_cast<uint32_t>(al.grid));
     return last_launch_status();
 }
 
