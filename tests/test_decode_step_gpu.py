@@ -1,5 +1,6 @@
 """GPU parity of the decode step (nmm_mla_decode_step: the MLA chain and an independent latent
-attention, the attention's workgroups sharing W_O's launch), through the C ABI.
+attention, the attention's workgroups sharing W_UQ's launch and its merge W_O's, or with a cache
+entry the attention in W_O's launch), through the C ABI.
 
 The step must reproduce, bit for bit, what the chain (nmm_mla_decode_chain) and the attention
 (nmm_latent_attention_ex with the same partition) write when run on their own: the shared launch
