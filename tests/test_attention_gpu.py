@@ -80,6 +80,28 @@ def test_attention_ragged(heads, seq, dqk, dv, ldkv):
     check(q, kv, scale, dqk, dv, f"attention {heads}x{seq}x{dqk}/{dv}")
 
 
+@pytest.mark.parametrize("splits", [1, 3, 16])
+def test_attention_identical_keys_give_the_value_row(splits):
+    # a closed form, independent of the oracle: when every cache row is the same, every score of
+    # a head is the same, P = 2^0 = 1 at every position and the output is that row's first d_v
+    # values.  The sums are exact (integer multiples of bf16 values below 2^24), so a merge of
+    # spans returns the row bit for bit; one span multiplies by the rounded 1 / l, within one ulp.
+    rng = np.random.default_rng(91)
+    heads, seq, dqk, dv = 40, 1000, 576, 512
+    q = syn.bits_from_f32(rng.standard_normal((heads, dqk), dtype=np.float32), syn.BF16)
+    row = syn.bits_from_f32(rng.standard_normal(dqk, dtype=np.float32), syn.BF16)
+    kv = np.ascontiguousarray(np.broadcast_to(row, (seq, dqk)))
+    out = torch.full((heads, dv), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, 0.07, splits=splits)
+    torch.cuda.synchronize()
+    v = np.broadcast_to(oracle.decode(row[:dv], syn.BF16).astype(np.float32), (heads, dv))
+    got = out.cpu().numpy()
+    if splits == 1:
+        assert np.all(np.abs(got - v) <= np.abs(v) * 2.0 ** -23), "one span: within one ulp of the row"
+    else:
+        assert np.array_equal(got, v), f"{splits} spans: the row bit for bit"
+
+
 def test_attention_sharp_softmax_and_determinism():
     # a large scale makes the softmax nearly one-hot: stresses the running max and rescaling
     q, kv, _ = syn.attention_case(9, 32, 2000, dqk=128, dv=64)
