@@ -64,6 +64,22 @@ def padded(a: np.ndarray, ld: int, fill: int = 0x7FC0) -> np.ndarray:
     return out
 
 
+def large_int_case(seed: int, M: int, K: int, N: int, ldw: int, dt: int = BF16) -> "GemvCase":
+    """Integer-valued x[M, K] and W[K, N] (values -3..3, as 16-bit float bits) for weights of up to
+    2 GiB: drawn as int8 row blocks and mapped through a table, so no wider temporary of W's size
+    exists.  x rows are padded to a multiple of 8; W's padding columns [N, ldw) hold a NaN
+    pattern."""
+    rng = np.random.default_rng(seed)
+    table = bits_from_f32(np.arange(-3, 4, dtype=np.float32), dt)
+    x = padded(table[rng.integers(0, 7, size=(M, K), dtype=np.int8)], (K + 7) // 8 * 8)
+    W = np.empty((K, ldw), dtype=np.uint16)
+    for r0 in range(0, K, 4096):
+        r1 = min(K, r0 + 4096)
+        W[r0:r1, :N] = table[rng.integers(0, 7, size=(r1 - r0, N), dtype=np.int8)]
+    W[:, N:] = 0x7FC0
+    return GemvCase(M, K, N, dt, x, W, True, f"int_{M}x{K}x{N}")
+
+
 @dataclass
 class GemvCase:
     """One narrow MatMul y[M,N] = x[M,K] . W[K,N] (row-major, 16-bit inputs, fp32 output)."""

@@ -89,6 +89,35 @@ def test_ragged_integer_exact(M, K, N, dt):
     check_case(c, path=nmm.NMM_PATH_GEMV)
 
 
+def test_largest_weight_extent_on_every_path():
+    # one weight [65521, 16384] bf16 whose extent, 65521 * 16384 * 2 = 2^31 - 491,520 bytes, is just
+    # under the 2^31-byte limit, so the 32-bit buffer offsets take their largest values.  As W
+    # [65521, 16383] (padding column NaN) it feeds the GEMV (one row, every output) and the matrix
+    # cores (16 rows, sampled columns); the same bytes as Wt [65521 rows, 16383 + 1] feed the
+    # transposed path (sampled rows).  Values are small integers, so every sum is exact in fp32.
+    K, N, ldw = 65521, 16383, 16384
+    c = syn.large_int_case(61, 16, K, N, ldw)
+    x, W = dev16(c.x, c.dt), dev16(c.W, c.dt)
+    rng = np.random.default_rng(5)
+    y1 = torch.full((1, N), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_gemv(x[:1], W, y1, N=N, path=nmm.NMM_PATH_GEMV)
+    y16 = torch.full((16, N), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_gemv(x, W, y16, N=N, path=nmm.NMM_PATH_MFMA)
+    Kt, Nt = ldw - 1, K
+    yt = torch.full((1, Nt), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_gemv_nt(x[:1, :Kt], W, yt, K=Kt)
+    torch.cuda.synchronize()
+    y_ref, a_ref = oracle.gemv(c.x[:1], c.W, c.dt, K=K, N=N)
+    assert_parity(y1, y_ref, a_ref, integer=True, what="GEMV at the largest extent")
+    cols = np.unique(np.r_[0, 1, 127, 128, 8191, 8192, N - 129, N - 2, N - 1, rng.choice(N, 119, replace=False)])
+    y_ref, a_ref = oracle.gemv(c.x, np.ascontiguousarray(c.W[:, cols]), c.dt, K=K, N=len(cols))
+    assert_parity(y16[:, cols], y_ref, a_ref, integer=True, what="MFMA at the largest extent")
+    rows = np.unique(np.r_[0, 1, 31, 32, Nt // 2, Nt - 33, Nt - 2, Nt - 1, rng.choice(Nt, 120, replace=False)])
+    Ws = np.ascontiguousarray(c.W[rows, :Kt].T)           # [Kt, len(rows)]: the sampled rows of Wt as W
+    y_ref, a_ref = oracle.gemv(c.x[:1], Ws, c.dt, K=Kt, N=len(rows))
+    assert_parity(yt[:, rows], y_ref, a_ref, integer=True, what="transposed path at the largest extent")
+
+
 def test_output_padding_untouched():
     c = syn.gemv_case(3, 2, 500, 70, syn.BF16, ldx=504, ldw=72)
     y = run_gemv(c, ldy=80, fill=-7.0)

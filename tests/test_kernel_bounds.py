@@ -90,6 +90,7 @@ SHAPES = [  # batch, M, K, N, ldx, ldw
     (1, 2, 500, 70, 504, 72), (1, 1, 4000, 1000, 4000, 1000), (1, 1, 3000, 700, 3000, 704),
     (128, 1, 128, 512, 128, 512), (128, 1, 512, 128, 512, 128), (3, 2, 1000, 72, 1000, 72),
     (5, 16, 96, 1000, 96, 1000), (2, 1, 20000, 40, 20000, 40),
+    (1, 1, 65521, 16383, 65528, 16384),   # W's extent 2^31 - 491,520 bytes: the largest offsets
 ]
 
 
@@ -106,7 +107,8 @@ def test_strided_query_slice_in_bounds():
 @pytest.mark.parametrize("M,K,N,ldx,ldw", [(1, 1536, 24576, 1536, 24576), (16, 1536, 24576, 1536, 24576),
                                            (32, 1536, 24576, 1536, 24576), (5, 1021, 1031, 1024, 1032),
                                            (33, 4099, 520, 4104, 520), (17, 16384, 7168, 16384, 7168),
-                                           (8, 100, 8, 104, 8), (32, 20000, 300, 20000, 304)])
+                                           (8, 100, 8, 104, 8), (32, 20000, 300, 20000, 304),
+                                           (16, 65521, 16383, 65528, 16384)])
 def test_mfma_launch_stays_in_bounds(M, K, N, ldx, ldw):
     p = nmm.nmm_gemv_plan(M, K, N, nmm.NMM_BF16, nmm.NMM_PATH_MFMA)
     mt, rows, ks, panels = p["m_tile"], p["rows_full"], p["split_k_full"], p["n_full_panels"]
@@ -211,6 +213,7 @@ NT_SHAPES = [  # M, K, N, ldx, ldwt
     (1, 1021, 1031, 1024, 1024), (1, 13, 8, 16, 16), (2, 20000, 40, 20000, 20000), (3, 4099, 520, 4104, 4104),
     (4, 9000, 4200, 9000, 9000), (5, 777, 300, 784, 784), (16, 1536, 3000, 1536, 1536), (1, 1, 1, 8, 8),
     (1, 100000, 64, 100000, 100000),
+    (1, 16383, 65521, 65528, 16384),      # Wt's extent 2^31 - 491,520 bytes: the largest offsets
 ]
 
 
