@@ -209,6 +209,19 @@ def attention_case(seed: int, heads: int, seq: int, dqk: int = ATTN_DQK, dv: int
     return q, kv, 1.0 / math.sqrt(QK_HEAD)
 
 
+def attention_case_large(seed: int, heads: int, seq: int, ldkv: int, dqk: int = ATTN_DQK) -> tuple[np.ndarray, np.ndarray, float]:
+    """attention_case's distributions in a cache of rows padded to ``ldkv`` (the padding holds a
+    NaN pattern), for caches of up to 2 GiB: the rows are drawn in blocks, so no float32 temporary
+    of the cache's size exists."""
+    rng = np.random.default_rng(seed)
+    q = normal_bits(rng, (heads, dqk), 1.0, BF16)
+    kv = np.full((seq, ldkv), 0x7FC0, dtype=np.uint16)
+    for r0 in range(0, seq, 1 << 16):
+        r1 = min(seq, r0 + (1 << 16))
+        kv[r0:r1, :dqk] = normal_bits(rng, (r1 - r0, dqk), 1.0, BF16)
+    return q, kv, 1.0 / math.sqrt(QK_HEAD)
+
+
 # MatMul 2 of the paper (one token times (W^DKV | W^KR)^T) and the cache entry behind it.
 KV_EPS, ROPE_THETA = 1e-6, 10000.0      # DeepSeek-V3's RMSNorm epsilon; RoFormer's RoPE base
 

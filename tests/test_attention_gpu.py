@@ -102,6 +102,21 @@ def test_attention_identical_keys_give_the_value_row(splits):
         assert np.array_equal(got, v), f"{splits} spans: the row bit for bit"
 
 
+def test_attention_largest_cache():
+    # a cache at the largest extent the ABI accepts: 65,535 rows of 16,384 elements (576 of them
+    # data, the rest a NaN pattern that must never be read), ((seq - 1) * ldkv + 576) * 2 =
+    # 2^31 - 64,384 bytes, so the chunks' 32-bit row offsets take their largest values; one ragged
+    # block of 20 heads over the default partition (64 spans of 1,024 positions)
+    seq, ldkv = 65535, 16384
+    q, kv, scale = syn.attention_case_large(67, 20, seq, ldkv)
+    assert ((seq - 1) * ldkv + 576) * 2 < 2 ** 31
+    out = torch.full((20, 512), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, scale)
+    torch.cuda.synchronize()
+    ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=576, dv=512)
+    assert_parity(out, ref, ref_abs, what=f"attention 20 heads x {seq} positions, rows of {ldkv}")
+
+
 def test_attention_sharp_softmax_and_determinism():
     # a large scale makes the softmax nearly one-hot: stresses the running max and rescaling
     q, kv, _ = syn.attention_case(9, 32, 2000, dqk=128, dv=64)
