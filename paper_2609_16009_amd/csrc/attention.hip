@@ -10,17 +10,19 @@
 // positions, S = Q . K^T and O = P . V, with a softmax between them (flash-decoding):
 //  * A workgroup owns a block of 32 heads (two 16-head MFMA tiles) and a span of positions,
 //    walked in 64-position chunks.  A chunk's rows (the first max(d_qk, d_v) columns) are staged
-//    in LDS by buffer loads that write LDS directly, into one of two buffers while the four waves
-//    compute on the other.
-//  * Q.K^T is split by positions: wave w computes S^T = K . Q^T for positions 16w .. 16w + 15 of
-//    the chunk and all 32 heads, so each K fragment read from LDS feeds both head tiles' MFMAs
-//    (v_mfma_f32_16x16x32_bf16; Q sits in registers as MFMA fragments).
+//    in LDS by buffer loads that write LDS directly, into one of two buffers while the waves
+//    compute on the other.  This launch runs 8 waves per workgroup (two per SIMD); workgroups
+//    that share a launch with a GEMV run 4, each wave then taking both head tiles.
+//  * Q.K^T is split by positions: position group w % 4 computes S^T = K . Q^T for positions
+//    16 (w % 4) .. + 15 of the chunk (v_mfma_f32_16x16x32_bf16; Q sits in registers as MFMA
+//    fragments), for head tile w / 4 (8 waves) or both (4 waves, each K fragment read from LDS
+//    feeding both tiles' MFMAs).
 //  * The softmax reference of a head is the running maximum, moved only when a chunk exceeds it
 //    by more than 2^8 (then the output is rescaled, rarely): P = 2^(s - reference) is rounded to
 //    bf16 and exchanged through LDS.  The chunk maxima cross the waves through LDS as well.
-//  * P.V is split by output columns: wave w accumulates O^T = V^T . P^T for the 16-column tiles
-//    w, w + 4, ... of all 32 heads, V^T fragments read from the staged rows by
-//    ds_read_b64_tr_b16 (gfx950's transposing LDS read).  The accumulators stay in registers.
+//  * P.V is split by output columns: position group w % 4 accumulates O^T = V^T . P^T for the
+//    16-column tiles w % 4, w % 4 + 4, ... of its heads, V^T fragments read from the staged rows
+//    by ds_read_b64_tr_b16 (gfx950's transposing LDS read).  The accumulators stay in registers.
 //  * Spans write (reference, sum, unnormalised output) partials; a merge kernel on the same
 //    stream combines them in span order.  The head blocks of one span run on one XCD (workgroup
 //    ids 8 apart), so its L2 reads the span's cache rows from HBM once for all of them.

@@ -23,7 +23,7 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kAThreads = 256;            // 4 waves (the W_O launch's attention workgroups)
+constexpr int kAThreads = 256;            // 4 waves (attention workgroups beside a GEMV's in one launch)
 constexpr int kAThreads8 = 512;           // 8 waves (the attention launch)
 constexpr int kCh = 64;                   // cache positions per chunk (16 per wave in Q.K^T)
 constexpr int kMaxCols = 576;             // staged columns per cache row: max(d_qk, d_v)
