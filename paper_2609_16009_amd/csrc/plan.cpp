@@ -318,13 +318,15 @@ nmm_status plan_gemv_nt(int64_t M, int64_t K, int64_t N, NtPlan* p) {
     // measured faster for W_UQ's [24576, 1536] (768 workgroups) than 24 rows per wave
     int r = static_cast<int>(std::min<int64_t>(8, std::max<int64_t>(1, N / (4 * target_rb))));
     r = static_cast<int>(std::min<int64_t>(32, std::max<int64_t>(1, tuned("NMM_NT_ROWS", r))));
-    // rows per load step (rgroup) times steps in flight is 8 loads per lane.  One-row tiles take
-    // two rows per step, so four steps stay in flight: with eight rows per step the next step's
-    // loads wait for this step's multiply-adds (measured on MI355X at M = 1: W_O [7168, 16384]
-    // 39.0 against 41.7 us, W_UQ [24576, 1536] 14.7 against 15.1; one row per step reads x from LDS
-    // for every load and is slower still).  Taller tiles, whose x reads grow with MT, share each
-    // read across as many rows as they have.
-    q.rgroup = q.mt == 1 ? (r >= 2 ? 2 : 1) : r >= 8 ? 8 : r >= 4 ? 4 : r >= 2 ? 2 : 1;
+    // rows per load step (rgroup) times steps in flight is 8 loads per lane.  With eight rows per
+    // step only one step is in flight, so the next step's loads wait for this step's multiply-adds;
+    // with one row per step x is read from LDS for every load.  Measured on MI355X: one-row tiles
+    // take two rows per step (four steps in flight; W_O [7168, 16384] 39.0 against 41.7 us with
+    // eight, W_UQ [24576, 1536] 14.7 against 15.1), taller tiles, whose x reads per step grow with
+    // MT, four (two steps in flight; at M = 2 W_O 46.6 against 49.1, W_UQ 15.6 against 16.7, down
+    // [2112, 7168] 12.2 against 13.5 with its rows per wave raised from 2 to 4; at M = 4 W_O 55.8
+    // against 61.7).  One row per wave (small N) keeps one.
+    q.rgroup = r < 2 ? 1 : q.mt == 1 ? 2 : 4;
     const int rg = tuned("NMM_NT_GROUP", q.rgroup);
     if (rg == 1 || rg == 2 || rg == 4 || rg == 8) q.rgroup = rg;
     q.depth = (q.mt == 1 && tuned("NMM_NT_DEPTH", 8) == 16) ? 16 : 8;

@@ -232,7 +232,7 @@ def test_gemv_nt_launch_stays_in_bounds(M, K, N, ldx, ldwt):
     ks = -(-K // slice_k)
     target_rb = max(1, 256 // (ks * mblocks))
     r = min(8, max(1, N // (4 * target_rb)))
-    rg = (2 if r >= 2 else 1) if mt == 1 else 8 if r >= 8 else 4 if r >= 4 else 2 if r >= 2 else 1
+    rg = 1 if r < 2 else 2 if mt == 1 else 4
     r = -(-r // rg) * rg
     R = 4 * r
     row_blocks = -(-N // R)
