@@ -226,8 +226,9 @@ nmm_status nmm_mla_query_path_run(const nmm_mla_query_path* qp, void* workspace,
  * [N, K] (Wt[n * ldwt + k]), the layout of a torch Linear weight and the one a dense
  * y = x . Wt^T GEMM reads, so one weight copy serves both (the paper keeps the matrix-unit
  * path's weight layout in global memory, Section IV-C; its Algorithm 1 multiplies rows by
- * columns).  Each output is the dot product of two contiguous rows: a wave streams 512 k of up
- * to 8 Wt rows per step and folds its lanes at the end of the rows.  K is split (partials in
+ * columns).  Each output is the dot product of two contiguous rows: a wave streams 512 k of a
+ * few Wt rows per step (two for one x row, four for more) with several steps in flight, and
+ * folds its lanes at the end of the rows.  K is split (partials in
  * the workspace, combined in slice order in the same launch) only beyond 16384 / mt values,
  * mt = min(M, 4) rounded up to 1, 2 or 4; M above 4 runs in blocks of 4 rows, each reading Wt
  * again.
