@@ -53,7 +53,7 @@ void attention_kernel(const AttnParams p) {
 }
 
 __global__ __launch_bounds__(kMergeThreads) void attention_merge_kernel(const AttnParams p) {
-    merge_block(p, static_cast<int>(blockIdx.x));
+    merge_block_wide(p, static_cast<int>(blockIdx.x));
 }
 
 struct AttnPlan {
@@ -192,7 +192,10 @@ namespace nmm {
 
 nmm_status launch_attention_merge(const AttnLaunch& l, hipStream_t s) {
     if (l.merge_grid == 0) return NMM_OK;
-    hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(l.merge_grid)), dim3(kMergeThreads), 0, s,
+    // merge_block_wide's blocks (two heads each); merge_grid counts merge_block's, which the GEMV
+    // launches that carry the merge use
+    const int64_t grid = (int64_t(l.p.heads) + kMergeHeads - 1) / kMergeHeads;
+    hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kMergeThreads), 0, s,
                        l.p);
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
 }

@@ -503,14 +503,37 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 
 // Merge the spans of each head in span order:
 //   out = sum_s w_s O_s / sum_s w_s l_s,  w_s = 2^(m_s - M),  M = max_s m_s.
-// Merge block `blk` owns one head and kMergeThreads of its columns (heads x ceil(d_v / 256)
-// blocks in all).  Lane s of every wave loads span s's (m, l) (at most 64 spans), so M and the
-// normaliser come from one load and fixed-order butterflies; each thread then loads its column of
-// every span at once and sums them in span order, the weights taken from lane s.  A block waits
-// for about two memory round trips.  Called by 256-thread workgroups: the merge launch, or the
-// workgroups of a GEMV launch that carry the merge beside the GEMV.
+// Lane s of every wave loads span s's (m, l) (at most 64 spans), so M and the normaliser come from
+// one load and fixed-order butterflies; each thread loads its columns of every span at once and
+// sums them in span order with explicit fused multiply-adds, the weights taken from lane s.  A
+// block waits for about two memory round trips.  Two forms, which give the same bits (the same
+// operations on every output, in the same order):
+//  * merge_block: block `blk` owns one head and 256 of its columns, one per thread (heads x
+//    ceil(d_v / 256) blocks): many light blocks, for the workgroups a GEMV launch carries beside
+//    its own.
+//  * merge_block_wide: block `blk` owns heads 2 blk and 2 blk + 1, 128 threads each, thread t
+//    taking columns 4 t .. + 3 (d_v <= 512; heads / 2 blocks, rounded up), so each load moves
+//    1 KB of a span's row per wave: the merge launch of the attention on its own.
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBatch = 32;
+constexpr int kMergeHeads = 2;       // heads per block of merge_block_wide
+constexpr int kMergeWideBatch = 16;  // spans merge_block_wide loads at once
+
+// M's weight of this lane's span and the normaliser sum_s w_s l_s, the same in every lane
+__device__ __forceinline__ float2 merge_weights(const AttnParams& p, int64_t base, int lane) {
+#pragma clang fp contract(off)
+    float2 m_l = float2{-INFINITY, 0.f};
+    if (lane < p.nsp) m_l = *reinterpret_cast<const float2*>(p.part_ml + (base + int64_t(lane) * p.hbh) * 2);
+    float M = m_l.x;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
+    const float w = (m_l.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_l.x - M);
+    float den = w * m_l.y;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) den += __shfl_xor(den, off);
+    return float2{w, den};
+}
+
 __device__ __forceinline__ void merge_block(const AttnParams& p, int blk) {
     // no contraction of its own: every translation unit that inlines this rounds alike (the
     // products of the sum are explicit fused multiply-adds)
@@ -528,15 +551,7 @@ __device__ __forceinline__ void merge_block(const AttnParams& p, int blk) {
     float v[kMergeBatch];
 #pragma unroll
     for (int u = 0; u < kMergeBatch; ++u) v[u] = (active && u < p.nsp) ? src[u * o_step] : 0.f;
-    float2 m_l = float2{-INFINITY, 0.f};
-    if (lane < p.nsp) m_l = *reinterpret_cast<const float2*>(p.part_ml + (base + int64_t(lane) * p.hbh) * 2);
-    float M = m_l.x;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) M = fmaxf(M, __shfl_xor(M, off));
-    const float w = (m_l.x == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_l.x - M);
-    float den = w * m_l.y;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) den += __shfl_xor(den, off);
+    const float2 wd = merge_weights(p, base, lane);
     float acc = 0.f;
     for (int s0 = 0; s0 < p.nsp; s0 += kMergeBatch) {
         if (s0 > 0) {
@@ -545,16 +560,62 @@ __device__ __forceinline__ void merge_block(const AttnParams& p, int blk) {
         }
 #pragma unroll
         for (int u = 0; u < kMergeBatch; ++u)
-            if (s0 + u < p.nsp) acc = __builtin_fmaf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), s0 + u)), v[u], acc);
+            if (s0 + u < p.nsp) acc = __builtin_fmaf(__int_as_float(__builtin_amdgcn_readlane(__float_as_int(wd.x), s0 + u)), v[u], acc);
     }
     if (!active) return;
-    const float r = acc / den;
+    const float r = acc / wd.y;
     p.out[int64_t(h) * p.ldo + n] = r;
     if (p.outb) p.outb[int64_t(h) * p.ldob + n] = to_bf16_bits(r);
 }
 
+__device__ __forceinline__ void merge_block_wide(const AttnParams& p, int blk) {
+#pragma clang fp contract(off)
+    const int tid = static_cast<int>(threadIdx.x);
+    const int h = kMergeHeads * blk + (tid >> 7);   // the same in a wave
+    if (h >= p.heads) return;
+    const int c = 4 * (tid & 127);
+    const int lane = tid & 63;
+    const int hb = h / p.hbh, hl = h - hb * p.hbh;
+    const int64_t base = int64_t(hb) * p.nsp * p.hbh + hl;
+    const float* src = p.part_o + base * p.dv + c;
+    const int64_t o_step = int64_t(p.hbh) * p.dv;
+    const bool active = c < p.dv;
+    f32x4 v[kMergeWideBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeWideBatch; ++u)
+        v[u] = (active && u < p.nsp) ? *reinterpret_cast<const f32x4*>(src + u * o_step) : f32x4{0.f, 0.f, 0.f, 0.f};
+    const float2 wd = merge_weights(p, base, lane);
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < p.nsp; s0 += kMergeWideBatch) {
+        if (s0 > 0) {
+#pragma unroll
+            for (int u = 0; u < kMergeWideBatch; ++u)
+                v[u] = (active && s0 + u < p.nsp) ? *reinterpret_cast<const f32x4*>(src + (s0 + u) * o_step)
+                                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int u = 0; u < kMergeWideBatch; ++u)
+            if (s0 + u < p.nsp) {
+                const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wd.x), s0 + u));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc[e] = __builtin_fmaf(wu, v[u][e], acc[e]);
+            }
+    }
+    if (!active) return;
+    f32x4 r;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = acc[e] / wd.y;
+    *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + c) = r;
+    if (p.outb) {
+        uint16_t* d = p.outb + int64_t(h) * p.ldob + c;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) d[e] = to_bf16_bits(r[e]);
+    }
+}
+
 // A prepared attention call: kernel arguments, the attention grid (0: nothing to launch), the
-// merge grid (0: one span, no merge) and the kernel variant.
+// number of merge_block blocks (0: one span, no merge; the merge launch of its own runs
+// merge_block_wide's instead) and the kernel variant.
 constexpr int kAttnExact = 1;      // d_qk 576, d_v 512
 constexpr int kAttnGeneral = 2;    // d_qk <= 576, d_v <= 512
 struct AttnLaunch {
