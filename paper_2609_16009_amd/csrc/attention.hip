@@ -52,7 +52,7 @@ void attention_kernel(const AttnParams p) {
     attention_block<HT, 8, KS, NTW, EXACT>(p, blockIdx.x);
 }
 
-__global__ __launch_bounds__(kMergeThreads) void attention_merge_kernel(const AttnParams p) {
+__global__ __launch_bounds__(kMergeWideThreads) void attention_merge_kernel(const AttnParams p) {
     merge_block_wide(p, static_cast<int>(blockIdx.x));
 }
 
@@ -192,10 +192,9 @@ namespace nmm {
 
 nmm_status launch_attention_merge(const AttnLaunch& l, hipStream_t s) {
     if (l.merge_grid == 0) return NMM_OK;
-    // merge_block_wide's blocks (two heads each); merge_grid counts merge_block's, which the GEMV
+    // merge_block_wide's blocks (one per head); merge_grid counts merge_block's, which the GEMV
     // launches that carry the merge use
-    const int64_t grid = (int64_t(l.p.heads) + kMergeHeads - 1) / kMergeHeads;
-    hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kMergeThreads), 0, s,
+    hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(l.p.heads)), dim3(kMergeWideThreads), 0, s,
                        l.p);
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
 }

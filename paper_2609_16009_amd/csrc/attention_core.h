@@ -511,12 +511,12 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 //  * merge_block: block `blk` owns one head and 256 of its columns, one per thread (heads x
 //    ceil(d_v / 256) blocks): many light blocks, for the workgroups a GEMV launch carries beside
 //    its own.
-//  * merge_block_wide: block `blk` owns heads 2 blk and 2 blk + 1, 128 threads each, thread t
-//    taking columns 4 t .. + 3 (d_v <= 512; heads / 2 blocks, rounded up), so each load moves
-//    1 KB of a span's row per wave: the merge launch of the attention on its own.
+//  * merge_block_wide: a 128-thread block `blk` owns head blk, thread t taking columns 4 t .. + 3
+//    (d_v <= 512; one block per head), so each load moves 1 KB of a span's row per wave: the
+//    merge launch of the attention on its own.
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBatch = 32;
-constexpr int kMergeHeads = 2;       // heads per block of merge_block_wide
+constexpr int kMergeWideThreads = 128;   // threads per block of merge_block_wide (one head)
 constexpr int kMergeWideBatch = 16;  // spans merge_block_wide loads at once
 
 // M's weight of this lane's span and the normaliser sum_s w_s l_s, the same in every lane
@@ -571,9 +571,8 @@ __device__ __forceinline__ void merge_block(const AttnParams& p, int blk) {
 __device__ __forceinline__ void merge_block_wide(const AttnParams& p, int blk) {
 #pragma clang fp contract(off)
     const int tid = static_cast<int>(threadIdx.x);
-    const int h = kMergeHeads * blk + (tid >> 7);   // the same in a wave
-    if (h >= p.heads) return;
-    const int c = 4 * (tid & 127);
+    const int h = blk;
+    const int c = 4 * tid;
     const int lane = tid & 63;
     const int hb = h / p.hbh, hl = h - hb * p.hbh;
     const int64_t base = int64_t(hb) * p.nsp * p.hbh + hl;
