@@ -498,9 +498,10 @@ def profile_case(name: str, launches: int) -> int:
         call = lambda i: nmm.nmm_gemv(x, Ws[i % len(Ws)], y, path=path, workspace=ws)
     elif name == "attention":
         st = syn.decode_step()
-        q, kvs = up(st.q), [up(st.kv) for _ in range(3)]
+        q = up(st.q)
+        kvs = [up(st.kv) for _ in range(copies_for(st.kv.size * 2))]   # a cold cache, as in a decode step
         out = torch.empty((q.shape[0], syn.ATTN_DV), device=dev)
-        call = lambda i: nmm.nmm_latent_attention_ex(q, kvs[i % 3], out, st.scale, d_qk=syn.ATTN_DQK,
+        call = lambda i: nmm.nmm_latent_attention_ex(q, kvs[i % len(kvs)], out, st.scale, d_qk=syn.ATTN_DQK,
                                                      d_v=syn.ATTN_DV, workspace=ws)
     elif name == "decode_step":
         st = syn.decode_step()
