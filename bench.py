@@ -602,7 +602,7 @@ def main() -> int:
     K, W = args.steps, args.warmup
     chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a) for c in range(args.copies)]
 
-    # attention beside the chain: 16 position spans per block of 32 heads, 64 workgroups on the 64
+    # attention beside the chain: 16 position spans over blocks of 32 heads, 64 workgroups on the 64
     # compute units that W_UQ's 192 leave free; the merge rides in W_O's launch.  Measured on one
     # MI355X, steps issued back to back: 75.0-75.3 us per step with 16 spans against 76.8-78.0
     # with 12 and 81.8-82.2 with 24 (attention then needs compute units W_UQ holds), and

@@ -375,12 +375,14 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
                                 float scale, float* out, int64_t ldo,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
-/* nmm_latent_attention with the partition chosen by the caller: `splits` position spans per block
- * of heads (0: the default, about 64 workgroups; the span is rounded up to whole 64-position
- * chunks, so fewer spans may result), and an optional bf16 copy of the output (out_bf16 may be
- * NULL).  Beside an HBM-bound stream a smaller partition interferes less: on MI355X the decode
- * step (nmm_mla_decode_step) is fastest with 11 to 16 spans (22 to 32 workgroups) against 32 for
- * attention alone.  Workspace:
+/* nmm_latent_attention with the partition chosen by the caller: `splits` position spans, each
+ * taken by every block of heads (0: the default, 64 / ceil(heads / 32) spans, 16 for 128 heads;
+ * the span is rounded up to whole 64-position chunks, so fewer spans may result), and an optional
+ * bf16 copy of the output (out_bf16 may be NULL).  The launch takes blocks of 16 heads: 128
+ * workgroups for 128 heads at the default.  On MI355X at 128 heads x 4096 positions attention
+ * alone is fastest with 16 to 32 spans, and so is the decode step (nmm_mla_decode_step), whose
+ * attention workgroups take blocks of 32 heads beside an HBM-bound stream.  The results depend on
+ * the spans only, not on the head blocks.  Workspace:
  * nmm_latent_attention_ex_workspace_size with the same splits. */
 nmm_status nmm_latent_attention_ex(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v,
                                    const void* q, int64_t ldq, const void* kv, int64_t ld_kv,
@@ -400,7 +402,7 @@ nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, i
  * run beside the chain's MatMuls instead of after them.  The paper's decode overlaps the narrow
  * MatMuls with matrix-unit work that does not depend on them (Condition 1 "Data Independence",
  * Section III-A; Section IV-A).  Here the overlap is fixed by the launches: the attention's
- * workgroups (splits position spans per block of 32 heads) share W_UQ's grid, the GEMV's streaming
+ * workgroups (blocks of 32 heads over the splits position spans) share W_UQ's grid, the GEMV's streaming
  * the weight while attention's use the compute units it leaves free, and the merge of the spans
  * rides on extra workgroups of W_O's launch.  With the cache entry (kv_cache), whose workgroup
  * takes W_UQ's launch, the attention and its merge share W_O's launch instead.  This needs
@@ -426,7 +428,7 @@ typedef struct {
     int64_t ldo;
     void* out_bf16;                  /* optional bf16 copy [heads, ldob], or NULL */
     int64_t ldob;
-    int64_t splits;                  /* position spans per head block (0: the default) */
+    int64_t splits;                  /* position spans (0: the default) */
 } nmm_latent_attn;
 
 nmm_status nmm_mla_decode_step(const nmm_mla_chain* chain, const nmm_latent_attn* attn, void* workspace,

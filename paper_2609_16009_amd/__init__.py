@@ -566,8 +566,8 @@ def nmm_latent_attention_bf16(q: torch.Tensor, kv: torch.Tensor, out: torch.Tens
 def nmm_latent_attention_ex(q: torch.Tensor, kv: torch.Tensor, out: torch.Tensor, scale: float, *, splits: int = 0,
                             out_bf16: torch.Tensor | None = None, d_qk: int | None = None, d_v: int = 512,
                             workspace=None, stream=None) -> torch.Tensor:
-    """nmm_latent_attention with `splits` position spans per head block (0: default) and an
-    optional bf16 copy of the output."""
+    """nmm_latent_attention with `splits` position spans (0: default) and an optional bf16 copy
+    of the output."""
     heads, seq = q.shape[0], kv.shape[0]
     d_qk = q.shape[1] if d_qk is None else d_qk
     need = lib().nmm_latent_attention_ex_workspace_size(heads, seq, d_qk, d_v, splits)

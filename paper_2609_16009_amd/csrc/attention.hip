@@ -8,15 +8,15 @@
 //
 // Every head reads the same latent cache, so the work is two dense products per span of
 // positions, S = Q . K^T and O = P . V, with a softmax between them (flash-decoding):
-//  * A workgroup owns a block of 32 heads (two 16-head MFMA tiles) and a span of positions,
-//    walked in 64-position chunks.  A chunk's rows (the first max(d_qk, d_v) columns) are staged
-//    in LDS by buffer loads that write LDS directly, into one of two buffers while the waves
-//    compute on the other.  This launch runs 8 waves per workgroup (two per SIMD); workgroups
-//    that share a launch with a GEMV run 4, each wave then taking both head tiles.
+//  * A workgroup owns a block of heads and a span of positions, walked in 64-position chunks.  A
+//    chunk's rows (the first max(d_qk, d_v) columns) are staged in LDS by buffer loads that write
+//    LDS directly, into one of two buffers while the waves compute on the other.  This launch
+//    takes blocks of 16 heads (one 16-head MFMA tile); workgroups that share a launch with a GEMV
+//    take 32 heads (two tiles), and so does this launch when such a call cannot share one.  Every
+//    workgroup has 4 waves, one per SIMD, each taking all of the block's head tiles.
 //  * Q.K^T is split by positions: position group w % 4 computes S^T = K . Q^T for positions
 //    16 (w % 4) .. + 15 of the chunk (v_mfma_f32_16x16x32_bf16; Q sits in registers as MFMA
-//    fragments), for head tile w / 4 (8 waves) or both (4 waves, each K fragment read from LDS
-//    feeding both tiles' MFMAs).
+//    fragments) for the wave's head tiles, each K fragment read from LDS feeding every tile's MFMA.
 //  * The softmax reference of a head is the running maximum, moved only when a chunk exceeds it
 //    by more than 2^8 (then the output is rescaled, rarely): P = 2^(s - reference) is rounded to
 //    bf16 and exchanged through LDS.  The chunk maxima cross the waves through LDS as well.
@@ -41,15 +41,20 @@ namespace {
 
 using namespace attn;
 
-constexpr int kHeadsPerBlock = 16 * kHt;  // 32
-constexpr int kMaxSpans = 64;                      // the merge gives each span one lane of a wave
-constexpr int kDefaultGrid = 64;          // workgroups of the default partition
+// Heads per workgroup.  The attention launch takes blocks of 16 (one head tile, 4 waves, one per
+// SIMD): twice the workgroups of 32-head blocks over the same spans, each with half the matrix work
+// per staged chunk.  Workgroups that share a launch with a GEMV take 32 (two head tiles, 4 waves),
+// so that they hold half as many compute units beside the GEMV's weight stream.  No head's
+// arithmetic depends on which heads share its block, so the two give the same bits.
+constexpr int kAloneHeads = 16;
+constexpr int kSharedHeads = 16 * kHt;   // 32
+constexpr int kMaxSpans = 64;             // the merge gives each span one lane of a wave
+constexpr int kDefaultPairs = 64;         // default partition: about this many (32-head block, span) pairs
 
-// 8 waves per workgroup (two per SIMD), one workgroup per compute unit (its LDS).
-template <int HT, int KS, int NTW, bool EXACT>
-__global__ __launch_bounds__(kAThreads8) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attention_kernel(const AttnParams p) {
-    attention_block<HT, 8, KS, NTW, EXACT>(p, blockIdx.x);
+// Attention launch workgroups of HT head tiles.
+template <int HT, bool EXACT>
+__global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p) {
+    attention_block<HT, kMaxKs, kMaxNtw, EXACT>(p, blockIdx.x);
 }
 
 __global__ __launch_bounds__(kMergeWideThreads) void attention_merge_kernel(const AttnParams p) {
@@ -57,24 +62,29 @@ __global__ __launch_bounds__(kMergeWideThreads) void attention_merge_kernel(cons
 }
 
 struct AttnPlan {
+    int hbh = kAloneHeads;
     int n_hb = 0, nsp = 1, span = 0, xcd_map = 0, cols = 0, pitch = 0;
     int grid_sp = 1;    // spans in the grid: nsp, padded to a multiple of 8 when xcd_map
     size_t ws_bytes = 0;
 };
 
-// splits > 0 asks for that many position spans per head block (the span is rounded up to whole
-// chunks, so fewer may result); 0 takes the default of about kDefaultGrid workgroups.
-nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, AttnPlan* out, int64_t splits = 0) {
+// splits > 0 asks for that many position spans (the span is rounded up to whole chunks, so fewer
+// may result); 0 takes the default.  The spans do not depend on the head block (hbh, 16 or 32),
+// and the workspace is sized for 32-head blocks, which covers both.
+nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, AttnPlan* out, int64_t splits = 0,
+                          int hbh = kAloneHeads) {
     if (heads < 0 || seq < 1 || heads >= (1 << 30) || seq >= (1 << 30)) return NMM_ERR_SHAPE;
     if (dqk < 32 || dqk > kMaxCols || dqk % 32) return NMM_ERR_SHAPE;
     if (dv < 16 || dv > 16 * 4 * kMaxNtw || dv % 16) return NMM_ERR_SHAPE;
     if (splits < 0) return NMM_ERR_ARG;
     AttnPlan a;
-    a.n_hb = static_cast<int>((heads + kHeadsPerBlock - 1) / kHeadsPerBlock);
+    a.hbh = hbh;
+    a.n_hb = static_cast<int>((heads + hbh - 1) / hbh);
     a.cols = static_cast<int>(std::max(dqk, dv));
     a.pitch = a.cols + 8 * kPadSlots;
+    const int64_t wide_blocks = (heads + kSharedHeads - 1) / kSharedHeads;
     const int64_t max_sp = (seq + kCh - 1) / kCh;
-    int64_t nsp = splits > 0 ? splits : std::max<int64_t>(1, kDefaultGrid / std::max(1, a.n_hb));
+    int64_t nsp = splits > 0 ? splits : std::max<int64_t>(1, kDefaultPairs / std::max<int64_t>(1, wide_blocks));
     nsp = std::min(std::min(nsp, max_sp), int64_t(kMaxSpans));
     int64_t span = (seq + nsp - 1) / nsp;
     span = (span + kCh - 1) / kCh * kCh;
@@ -88,15 +98,18 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     // partial results live past the workspace's counter block (which GEMV calls sharing the
     // workspace rely on being zero)
     if (a.nsp > 1)
-        a.ws_bytes = size_t(kTicketBytes) + size_t(a.n_hb) * a.nsp * kHeadsPerBlock * (size_t(dv) + 2) * 4;
+        a.ws_bytes = size_t(kTicketBytes) + size_t(wide_blocks) * kSharedHeads * a.nsp * (size_t(dv) + 2) * 4;
     *out = a;
     return NMM_OK;
 }
 
 template <bool EXACT>
 nmm_status launch_attention(const AttnParams& p, int64_t grid, hipStream_t s) {
-    hipLaunchKernelGGL((attention_kernel<kHt, kMaxKs, kMaxNtw, EXACT>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kAThreads8), 0, s, p);
+    const dim3 g(static_cast<uint32_t>(grid));
+    if (p.hbh == kAloneHeads)
+        hipLaunchKernelGGL((attention_kernel<1, EXACT>), g, dim3(kAThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL((attention_kernel<kHt, EXACT>), g, dim3(kAThreads), 0, s, p);
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
 }
 
@@ -116,15 +129,15 @@ size_t nmm_latent_attention_workspace_size(int64_t heads, int64_t seq, int64_t d
 
 namespace {
 
-// Validation, plan and kernel arguments of one attention call; out->grid stays 0 when there is
-// nothing to launch (heads == 0).
+// Validation, plan and kernel arguments of one attention call in blocks of hbh heads; out->grid
+// stays 0 when there is nothing to launch (heads == 0).
 nmm_status prepare(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const void* q, int64_t ldq,
                    const void* kv, int64_t ld_kv, float scale, float* out_, int64_t ldo, void* outb,
-                   int64_t ldob, int64_t splits, void* workspace, size_t workspace_bytes, AttnLaunch* out) {
+                   int64_t ldob, int64_t splits, void* workspace, size_t workspace_bytes, int hbh, AttnLaunch* out) {
     *out = AttnLaunch{};
     if (splits < 0) return NMM_ERR_ARG;
     AttnPlan a;
-    nmm_status st = plan_attention(heads, seq, d_qk, d_v, &a, splits);
+    nmm_status st = plan_attention(heads, seq, d_qk, d_v, &a, splits, hbh);
     if (st != NMM_OK) return st;
     if (!std::isfinite(scale)) return NMM_ERR_ARG;
     if (heads == 0) return NMM_OK;   // nothing to launch (grid 0)
@@ -154,7 +167,7 @@ nmm_status prepare(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const 
     p.ldob = ldob;
     if (a.ws_bytes) {
         p.part_o = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + kTicketBytes);
-        p.part_ml = p.part_o + size_t(a.n_hb) * a.nsp * kHeadsPerBlock * d_v;
+        p.part_ml = p.part_o + size_t(a.n_hb) * a.nsp * a.hbh * d_v;
     }
     p.heads = static_cast<int>(heads);
     p.seq = static_cast<int>(seq);
@@ -165,7 +178,7 @@ nmm_status prepare(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const 
     p.nsp = a.nsp;
     p.span = a.span;
     p.n_hb = a.n_hb;
-    p.hbh = kHeadsPerBlock;
+    p.hbh = a.hbh;
     p.xcd_map = a.xcd_map;
     p.scale_log2 = scale * 1.4426950408889634f;
     p.kv_extent = static_cast<uint32_t>(extent);
@@ -181,7 +194,7 @@ nmm_status attention_common(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_
                             int64_t ldob, int64_t splits, void* workspace, size_t workspace_bytes, void* stream) {
     AttnLaunch l;
     const nmm_status st = prepare(heads, seq, d_qk, d_v, q, ldq, kv, ld_kv, scale, out, ldo, outb, ldob, splits,
-                                  workspace, workspace_bytes, &l);
+                                  workspace, workspace_bytes, kAloneHeads, &l);
     if (st != NMM_OK) return st;
     return launch_prepared_attention(l, static_cast<hipStream_t>(stream));
 }
@@ -214,7 +227,7 @@ nmm_status prepare_attention(const AttnArgs& a, void* workspace, size_t workspac
     if (a.outb && (a.ldob < a.d_v || a.ldob >= (int64_t(1) << 31))) return NMM_ERR_SHAPE;
     if (reinterpret_cast<uintptr_t>(a.outb) & 1u) return NMM_ERR_ALIGN;
     return prepare(a.heads, a.seq, a.d_qk, a.d_v, a.q, a.ldq, a.kv, a.ld_kv, a.scale, a.out, a.ldo, a.outb, a.ldob,
-                   a.splits, workspace, workspace_bytes, out);
+                   a.splits, workspace, workspace_bytes, kSharedHeads, out);
 }
 
 nmm_status attention_workspace_bytes(const AttnArgs& a, size_t* bytes) {
@@ -229,13 +242,6 @@ nmm_status attention_workspace_bytes(const AttnArgs& a, size_t* bytes) {
 nmm_status validate_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes) {
     AttnLaunch l;
     return prepare_attention(a, workspace, workspace_bytes, &l);
-}
-
-nmm_status launch_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes, void* stream) {
-    AttnLaunch l;
-    const nmm_status st = prepare_attention(a, workspace, workspace_bytes, &l);
-    if (st != NMM_OK) return st;
-    return launch_prepared_attention(l, static_cast<hipStream_t>(stream));
 }
 
 }  // namespace nmm

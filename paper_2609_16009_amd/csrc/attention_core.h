@@ -23,8 +23,8 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kAThreads = 256;            // 4 waves (attention workgroups beside a GEMV's in one launch)
-constexpr int kAThreads8 = 512;           // 8 waves (the attention launch)
+constexpr int kAWaves = 4;                // waves per attention workgroup, one per SIMD
+constexpr int kAThreads = 64 * kAWaves;
 constexpr int kCh = 64;                   // cache positions per chunk (16 per wave in Q.K^T)
 constexpr int kMaxCols = 576;             // staged columns per cache row: max(d_qk, d_v)
 constexpr int kPadSlots = 2;              // 16-byte padding slots after each staged row
@@ -32,7 +32,7 @@ constexpr int kPitchMax = kMaxCols + 8 * kPadSlots;   // 592 elements: LDS row p
 constexpr int kMaxKs = kMaxCols / 32;     // Q.K^T k-steps (32 dims each)
 constexpr int kMaxNtw = 8;                // P.V column tiles (16 columns) per wave: d_v <= 512
 constexpr int kMaxHt = 2;                 // head tiles (16 heads) per workgroup, at most
-constexpr int kHt = 2;                    // head tiles per workgroup of the attention launches
+constexpr int kHt = 2;                    // head tiles per workgroup beside a GEMV's
 constexpr int kPPitch = kCh + 8;          // row pitch (elements) of P in LDS
 constexpr int kKw = 6;                    // K fragments in flight in Q.K^T
 constexpr int kRsrcWord3 = 0x00020000;
@@ -180,10 +180,8 @@ __device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int* hb, 
     return true;
 }
 
-// One workgroup of the attention launch: HT * 16 heads (head block hb) over one span of positions,
-// with W = 4 or 8 waves.  Wave w has position group pw = w % 4 and head group hg = w / 4; with 4
-// waves a wave covers all HT head tiles, with 8 waves (two per SIMD, so that one wave's latency is
-// covered by the other's work) each wave covers HT / 2 of them.
+// One attention workgroup: HT * 16 heads (head block hb) over one span of positions, with 4 waves.
+// Wave w is position group pw = w and covers all HT head tiles.
 //  * Q.K^T: a wave computes the scores of positions 16 pw .. + 15 of each 64-position chunk for its
 //    head tiles (S^T = K . Q^T on the matrix cores, K fragments read from LDS and used for each of
 //    the wave's head tiles; Q held in registers as MFMA fragments).
@@ -194,14 +192,15 @@ __device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int* hb, 
 //    P <= 2^kLazyTh.
 //  * P.V: a wave accumulates the output columns of tiles pw, pw + 4, ... for its head tiles
 //    (O^T = V^T . P^T, V^T fragments by ds_read_b64_tr_b16 from the same staged rows).
-//  * The result goes through LDS so that each store instruction writes 1 KB of one row.
+//  * The result is stored straight from the accumulators, 64 contiguous bytes of 16 rows per store.
 // KS = d_qk / 32 and NTW = column tiles per position group are upper bounds; EXACT: the shape
 // matches them.
-template <int HT, int W, int KS, int NTW, bool EXACT>
+template <int HT, int KS, int NTW, bool EXACT>
 __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
+    constexpr int W = kAWaves;
     constexpr int HB = 16 * HT;
-    constexpr int HTW = HT * 4 / W;            // head tiles per wave
-    static_assert((W == 4 || W == 8) && HTW >= 1 && HTW * W == 4 * HT, "4 or 8 waves over whole head tiles");
+    constexpr int HTW = HT;                    // head tiles per wave: all of them
+    static_assert(W == 4 && HT >= 1 && HT <= kMaxHt, "one position group per wave, every wave over all head tiles");
     uint16_t* const kv_a = chunk_buffer_a();
     uint16_t* const kv_b = chunk_buffer_b();
     uint16_t* const pbuf = p_buffer();
@@ -210,7 +209,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & (W - 1);   // (the mask bounds it for the compiler)
-    const int pw = wave & 3, ht0 = (wave >> 2) * HTW;
+    const int pw = wave;
     const int g = lane >> 4, j = lane & 15;
     const int ksteps = EXACT ? KS : p.dqk / 32;
     const int ntiles = EXACT ? 4 * NTW : p.dv / 16;
@@ -251,7 +250,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     if constexpr (EXACT) wait_vm<Stage<W>::kMinPieces>();
     else __builtin_amdgcn_s_waitcnt(0);
     lds_sync();
-    // the Q fragments of the wave's head tiles: head 16 (ht0 + t) + j, dims 32 u + 8 g .. + 7; then
+    // the Q fragments of the wave's head tiles: head 16 t + j, dims 32 u + 8 g .. + 7; then
     // buffer b is free for chunk 1
     i32x4 qf[HTW][KS];
 #pragma unroll
@@ -259,12 +258,12 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 #pragma unroll
         for (int u = 0; u < KS; ++u)
             if (EXACT || u < ksteps)
-                qf[t][u] = *reinterpret_cast<const i32x4*>(kv_b + (16 * (ht0 + t) + j) * pitch + 8 * g + 32 * u);
+                qf[t][u] = *reinterpret_cast<const i32x4*>(kv_b + (16 * t + j) * pitch + 8 * g + 32 * u);
     // the first chunk has landed: this wave's pieces, then every wave's
     __builtin_amdgcn_s_waitcnt(0);
     lds_sync();
 
-    f32x4 o[NTW][HTW];      // O^T tiles: lane (g, j) holds columns 16 ct + 4 g .. + 3 of head 16 (ht0 + t) + j
+    f32x4 o[NTW][HTW];      // O^T tiles: lane (g, j) holds columns 16 ct + 4 g .. + 3 of head 16 t + j
 #pragma unroll
     for (int i = 0; i < NTW; ++i)
 #pragma unroll
@@ -348,14 +347,14 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
                     pv[i] = (v == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(v - m_ref[t]);
                     lc[t] += pv[i];
                 }
-                *reinterpret_cast<uint2*>(pbuf + (16 * (ht0 + t) + j) * kPPitch + 16 * pw + 4 * g) =
+                *reinterpret_cast<uint2*>(pbuf + (16 * t + j) * kPPitch + 16 * pw + 4 * g) =
                     uint2{pack_bf16(pv[0], pv[1]), pack_bf16(pv[2], pv[3])};
             }
         };
         // every wave posts its maxima and whether any moved past its reference by more than kLazyTh
         if (g == 0) {
 #pragma unroll
-            for (int t = 0; t < HTW; ++t) red[pw * HB + 16 * (ht0 + t) + j] = mx[t];
+            for (int t = 0; t < HTW; ++t) red[pw * HB + 16 * t + j] = mx[t];
         }
         if (ck > 0) {
             write_p();
@@ -367,13 +366,9 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
         }
         bool any = ck == 0;
         if (ck > 0) {
-            // every wave's flag in one or two 16-byte LDS reads
+            // every wave's flag in one 16-byte LDS read
             const i32x4 f0 = *reinterpret_cast<const i32x4*>(flags);
             any = (f0[0] | f0[1] | f0[2] | f0[3]) != 0;
-            if constexpr (W == 8) {
-                const i32x4 f1 = *reinterpret_cast<const i32x4*>(flags + 4);
-                any |= (f1[0] | f1[1] | f1[2] | f1[3]) != 0;
-            }
         }
         // ---- a reference moves (the same decision in every wave: all read the same maxima): the
         // chunk maximum of each head, the output rescaled, and P written again
@@ -382,7 +377,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
             float alpha[HTW];
 #pragma unroll
             for (int t = 0; t < HTW; ++t) {
-                const int hh = 16 * (ht0 + t) + j;
+                const int hh = 16 * t + j;
                 const float mc = fmaxf(fmaxf(red[hh], red[HB + hh]), fmaxf(red[2 * HB + hh], red[3 * HB + hh]));
                 alpha[t] = 1.f;
                 if (mc > m_ref[t] + kLazyTh) {
@@ -410,7 +405,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
             i32x4 pf[HTW];
 #pragma unroll
             for (int t = 0; t < HTW; ++t)
-                pf[t] = *reinterpret_cast<const i32x4*>(pbuf + (16 * (ht0 + t) + j) * kPPitch + 32 * kk + 8 * g);
+                pf[t] = *reinterpret_cast<const i32x4*>(pbuf + (16 * t + j) * kPPitch + 32 * kk + 8 * g);
             const uint16_t* vrow = cur + (32 * kk + 8 * g + a4) * pitch + 4 * b4;
             i32x4 vf[NTW];
 #pragma unroll
@@ -450,13 +445,13 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 #pragma unroll
     for (int t = 0; t < HTW; ++t) {
         const float lw = cols4_sum(l_acc[t]);
-        if (g == 0) red[pw * HB + 16 * (ht0 + t) + j] = lw;
+        if (g == 0) red[pw * HB + 16 * t + j] = lw;
     }
     __syncthreads();
     float lsum[HTW];
 #pragma unroll
     for (int t = 0; t < HTW; ++t) {
-        const int hh = 16 * (ht0 + t) + j;
+        const int hh = 16 * t + j;
         lsum[t] = ((red[hh] + red[HB + hh]) + red[2 * HB + hh]) + red[3 * HB + hh];
     }
 
@@ -467,7 +462,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     const int64_t pidx = int64_t(hb) * p.nsp + sp;
 #pragma unroll
     for (int t = 0; t < HTW; ++t) {
-        const int row = 16 * (ht0 + t) + j;
+        const int row = 16 * t + j;
         const int h = h0 + row;
         if (whole) {
             if (h < p.heads) {
@@ -626,6 +621,8 @@ struct AttnLaunch {
 
 }  // namespace attn
 
+// The call prepared for workgroups that share a GEMV's launch: blocks of 32 heads (two head tiles),
+// the spans of the attention launch of the same call, within the same workspace size.
 nmm_status prepare_attention(const AttnArgs& a, void* workspace, size_t workspace_bytes, attn::AttnLaunch* out);
 nmm_status launch_prepared_attention(const attn::AttnLaunch& l, hipStream_t s);   // attention, then merge
 nmm_status launch_attention_merge(const attn::AttnLaunch& l, hipStream_t s);

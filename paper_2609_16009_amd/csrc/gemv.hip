@@ -504,7 +504,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))
 void gemv_attention_kernel(const KParams p, const attn::AttnParams a, uint32_t attn_grid) {
     __shared__ int s_last;
     if (blockIdx.x < attn_grid) {
-        attn::attention_block<attn::kHt, 4, attn::kMaxKs, attn::kMaxNtw, true>(a, static_cast<int>(blockIdx.x));
+        attn::attention_block<attn::kHt, attn::kMaxKs, attn::kMaxNtw, true>(a, static_cast<int>(blockIdx.x));
     } else {
         float* lds = reinterpret_cast<float*>(attn::chunk_buffer_a());
         gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x - attn_grid, lds, &s_last);

@@ -154,8 +154,7 @@ struct AttnArgs {
 };
 // Workspace bytes of a valid call (0 when it needs none); NMM_ERR_* when the call is invalid.
 nmm_status attention_workspace_bytes(const AttnArgs& a, size_t* bytes);
-nmm_status launch_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes, void* stream);
-// Every check of launch_attention_args, without launching.
+// Every check of the attention call, without launching.
 nmm_status validate_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes);
 // The GEMV `g` (plain launch) and the attention `a` in one launch where both fit it (bf16, M = 1,
 // the 576 / 512 attention shape, the GEMV's LDS within one attention chunk buffer): attention's

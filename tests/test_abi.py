@@ -406,7 +406,7 @@ def test_attention_ex_rejects_invalid_arguments(kw, status):
 def test_attention_ex_workspace_follows_the_partition():
     w16 = L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 16)
     w32 = L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 32)
-    # the default partition: 16 spans per block of 32 heads (64 workgroups for 128 heads)
+    # the default partition: 16 spans for 128 heads (one workspace size for either head block)
     assert 0 < w16 < w32 and w16 == nmm.nmm_latent_attention_workspace_size(128, 4096, 576, 512)
     assert L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, 1) == 0     # one span: no merge
     assert L.nmm_latent_attention_ex_workspace_size(128, 4096, 576, 512, -1) == 0

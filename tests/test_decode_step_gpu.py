@@ -52,7 +52,7 @@ def assert_same(bufs_a, bufs_b, out_a, out_b, outb_a, outb_b):
         assert torch.equal(outb_a.view(torch.int16), outb_b.view(torch.int16)), "attention bf16 copy"
 
 
-@pytest.mark.parametrize("splits", [16, 0, 1, 12])   # 12: 11 spans, the grid padded to 16 per head block
+@pytest.mark.parametrize("splits", [16, 0, 1, 12])   # 12: 11 spans, the grid padded to 16 spans
 def test_full_size_step_matches_chain_and_attention(splits):
     step = syn.decode_step()
     q, kv, out, outb = attn_bufs(step.q, step.kv, syn.ATTN_DV)

@@ -298,15 +298,15 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
     """gemv_attention_kernel: workgroups [0, gemv_grid) run the GEMV exactly as its own launch
     (same ids, so the same items), the rest are attention workgroups 0 .. attention grid - 1; the
     GEMV's x slice (rows_max * 4 bytes, or the 4 x 256 x 8 floats of its reduction) must fit the
-    first attention chunk buffer of 64 x 584 bf16."""
+    first attention chunk buffer of 64 x 592 bf16.  Its attention workgroups take blocks of 32 heads."""
     p = nmm.nmm_gemv_plan(1, K, N, nmm.NMM_BF16, nmm.NMM_PATH_GEMV)
     assert p["m_tile"] == 1 and p["unroll"] in (8, 16)
     rows_max = max(p["rows_full"], p["rows_tail"])
     gemv_lds = max(rows_max * 1 * 4, 1 * 256 * 8 * 4)
-    assert gemv_lds <= 64 * 584 * 2
+    assert gemv_lds <= 64 * 592 * 2
     for heads, seq, splits in ((128, 4096, 16), (128, 4096, 0), (70, 300, 3), (1, 64, 1)):
         ws = nmm.nmm_latent_attention_workspace_size(heads, seq, 576, 512)
-        n_hb = (heads + 63) // 64
+        n_hb = (heads + 31) // 32
         span = -(-seq // max(1, min(splits or max(1, 64 // n_hb), -(-seq // 64))))
         span = -(-span // 64) * 64
         nsp = -(-seq // span)
@@ -317,6 +317,31 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
         assert np.array_equal(gemv_ids, np.arange(p["grid"]))
         assert np.array_equal(attn_ids, np.arange(agrid)) and total < 2 ** 31
         assert ws >= 0
+
+
+@pytest.mark.parametrize("heads", [1, 15, 16, 17, 20, 32, 33, 70, 128, 129])
+@pytest.mark.parametrize("seq,splits", [(4096, 0), (4096, 16), (4096, 32), (300, 3), (65535, 64), (64, 0)])
+def test_attention_spans_and_workspace_serve_both_head_blocks(heads, seq, splits):
+    """The attention launch takes blocks of 16 heads, workgroups beside a GEMV blocks of 32, over the
+    same spans (the default: 64 / ceil(heads / 32) spans).  Each form's span partials,
+    [n_hb][nsp][block heads][d_v] floats then [n_hb][nsp][block heads][2], must fit past the counter
+    block of the one workspace size the library reports for the call."""
+    dv, ticket = 512, 64 * 1024
+    L = nmm.lib()
+    ws = L.nmm_latent_attention_workspace_size(heads, seq, 576, dv) if splits == 0 else \
+        L.nmm_latent_attention_ex_workspace_size(heads, seq, 576, dv, splits)
+    nsp = splits or max(1, 64 // -(-heads // 32))
+    nsp = min(nsp, -(-seq // 64), 64)
+    span = -(-(-(-seq // nsp)) // 64) * 64
+    nsp = -(-seq // span)
+    if nsp == 1:
+        assert ws == 0
+        return
+    for hbh in (16, 32):
+        n_hb = -(-heads // hbh)
+        need = ticket + n_hb * nsp * hbh * (dv + 2) * 4
+        assert need <= ws, (hbh, need, ws)
+    assert ws == ticket + -(-heads // 32) * 32 * nsp * (dv + 2) * 4
 
 
 @pytest.mark.parametrize("n_hb,nsp", [(2, 16), (2, 11), (2, 32), (1, 9), (3, 22), (2, 3), (1, 1), (2, 64)])
