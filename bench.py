@@ -7,7 +7,7 @@ A step is one pass of the whole hot path over one token: the narrow-MatMul chain
 concurrently, latent attention (128 heads over a 4096-position latent cache, d_qk 576, d_v 512)
 -- the paper's overlap of narrow MatMul with independent matrix-unit work.  The step is one call
 of nmm_mla_decode_step on one stream: attention's workgroups share W_UQ's launch and the merge of
-its spans W_O's, so the overlap is fixed by the launches.  Steps are issued back to back (one C call each); the graph-replay form
+its spans the W_UK -> W_UV pair's, so the overlap is fixed by the launches.  Steps are issued back to back (one C call each); the graph-replay form
 and the earlier two-stream form (chain and attention on two streams, fork / join per step) are
 timed beside it.
 
@@ -603,7 +603,7 @@ def main() -> int:
     chains = [nmm.PreparedChain(d, {**copies[c][0], **inter}, workspace=ws_a) for c in range(args.copies)]
 
     # attention beside the chain: 16 position spans over blocks of 32 heads, 64 workgroups on the 64
-    # compute units that W_UQ's 192 leave free; the merge rides in W_O's launch.  Measured on one
+    # compute units that W_UQ's 192 leave free; the merge rides in the pair's launch.  Measured on one
     # MI355X, steps issued back to back: 75.0-75.3 us per step with 16 spans against 76.8-78.0
     # with 12 and 81.8-82.2 with 24 (attention then needs compute units W_UQ holds), and
     # 76.9-77.5 us for the earlier form with 8 spans beside W_O and the merge in its own launch
@@ -612,7 +612,7 @@ def main() -> int:
         nmm.nmm_latent_attention_ex(q, kv, att_out, step.scale, splits=splits, d_qk=dqk, d_v=dv, workspace=ws_b,
                                     stream=stream)
 
-    # the decode step: one call, attention's workgroups in W_UQ's launch, its merge in W_O's
+    # the decode step: one call, attention's workgroups in W_UQ's launch, its merge in the pair's
     steps_one = [nmm.PreparedStep(d, {**copies[c][0], **inter},
                                   dict(q=copies[c][1], kv=copies[c][2], out=att_out, scale=step.scale,
                                        splits=ATTN_OVERLAP_SPLITS, d_qk=dqk, d_v=dv), workspace=ws_s)
@@ -704,7 +704,7 @@ def main() -> int:
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager), \
         "two-stream steps must reproduce the first step bit for bit"
     # the step's segments from the chain's event hook (events before each launch and after the
-    # merge; a separate pass, since the events add work between the launches)
+    # last; a separate pass, since the events add work between the launches)
     ev_slots = [[ev() for _ in range(6)] for _ in range(K)]
     steps_ev = [nmm.PreparedStep(d, {**copies[c][0], **inter},
                                  dict(q=copies[c][1], kv=copies[c][2], out=att_out, scale=step.scale,
@@ -714,11 +714,11 @@ def main() -> int:
         for i in range(K):
             steps_ev[i % args.copies].launch(slot=i, stream=cap)
     torch.cuda.synchronize()
-    seg = (("down", 0, 1), ("w_uq_with_attention", 1, 2), ("w_uk_w_uv_pair", 2, 4), ("w_o_with_merge", 4, 5))
+    seg = (("down", 0, 1), ("w_uq_with_attention", 1, 2), ("w_uk_w_uv_pair_with_merge", 2, 4), ("w_o", 4, 5))
     segments = {n: round(sum(ev_slots[i][a].elapsed_time(ev_slots[i][b]) for i in range(K)) / K * 1e3, 2)
                 for n, a, b in seg}
     assert torch.equal(inter["y"], y_eager) and torch.equal(att_out, att_eager)
-    log(f"[bench] decode step (attention beside W_UQ, its merge in W_O's launch): {step_ms * 1e3:.1f} us issued back to back "
+    log(f"[bench] decode step (attention beside W_UQ, its merge in the pair's launch): {step_ms * 1e3:.1f} us issued back to back "
         f"(host {host_ms * 1e3:.1f} us per call), {graph_ms * 1e3:.1f} us as graph replays; two streams: "
         f"{two_graph_ms * 1e3:.1f} us graph replays, {two_eager_ms * 1e3:.1f} us issued")
 
@@ -847,7 +847,8 @@ def main() -> int:
             "workload": "DeepSeek-V3 MLA single-token decode step: narrow chain x[1,7168] . "
                         "down[7168,2112] . W_UQ[1536,24576] . 128 x W_UK[128,512] . 128 x W_UV[512,128] . "
                         "W_O[16384,7168], with latent attention 128 heads x 4096 positions (d_qk 576, "
-                        "d_v 512) beside the chain (its workgroups in W_UQ's launch, its merge in W_O's; "
+                        "d_v 512) beside the chain (its workgroups in W_UQ's launch, its merge in the "
+                        "W_UK -> W_UV pair's; "
                         "nmm_mla_decode_step, one stream, steps issued back to back)",
             "tokens": 1, "heads": d["heads"], "kv_len": seq, "weight_copies_rotated": args.copies,
             "bytes_per_step": chain_total + attn_total, "parallelism": "single GPU, one HIP stream",
@@ -868,12 +869,12 @@ def main() -> int:
             "frac_of_read_ceiling": wo_row.get("frac_of_read_ceiling"),
             "traffic": chain_traffic(),
             "in_the_step": {
-                "kernel": "gemv_merge_kernel: W_O's launch with one extra workgroup per block of the attention "
-                          "merge, as the timed decode step runs it (events around the launch, mean over "
-                          f"{K} steps; the step's attention ran beside W_UQ)",
-                "us": segments["w_o_with_merge"],
-                "achieved": round(cb["w_o"] / segments["w_o_with_merge"] / 1e3, 1),
-                "frac": round(cb["w_o"] / segments["w_o_with_merge"] / 1e3 / HBM_PEAK_GBPS, 4),
+                "kernel": "gemv_kernel: W_O's launch as the timed decode step runs it (events around the "
+                          f"launch, mean over {K} steps; the step's attention ran beside W_UQ and its merge "
+                          "in the W_UK -> W_UV pair's launch)",
+                "us": segments["w_o"],
+                "achieved": round(cb["w_o"] / segments["w_o"] / 1e3, 1),
+                "frac": round(cb["w_o"] / segments["w_o"] / 1e3 / HBM_PEAK_GBPS, 4),
                 "algorithmic_bytes": cb["w_o"],
             },
         },

@@ -404,8 +404,9 @@ nmm_status nmm_latent_attention_bf16(int64_t heads, int64_t seq, int64_t d_qk, i
  * Section III-A; Section IV-A).  Here the overlap is fixed by the launches: the attention's
  * workgroups (blocks of 32 heads over the splits position spans) share W_UQ's grid, the GEMV's streaming
  * the weight while attention's use the compute units it leaves free, and the merge of the spans
- * rides on extra workgroups of W_O's launch.  With the cache entry (kv_cache), whose workgroup
- * takes W_UQ's launch, the attention and its merge share W_O's launch instead.  This needs
+ * rides on extra workgroups of the W_UK -> W_UV pair's launch (of W_O's where the pair runs as two
+ * batched GEMVs).  With the cache entry (kv_cache), whose workgroup takes W_UQ's launch, the
+ * attention shares W_O's launch instead and its merge follows in a launch of its own.  This needs
  * d_qk = 576, d_v = 512 and the chain's MatMuls in their single-row bf16 form; other shapes run the
  * attention in its own launches (same results).
  *

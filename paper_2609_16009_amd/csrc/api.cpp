@@ -557,9 +557,9 @@ size_t nmm_mla_decode_chain_workspace_size(const nmm_mla_chain* chain) {
 namespace {
 
 // The chain's launches.  With `att`, the attention's workgroups share W_UQ's launch and its merge
-// shares W_O's (with the cache entry, which takes a spare workgroup of W_UQ's launch, attention and
-// merge both share W_O's instead); the attention's workspace follows the chain's at a 256-byte
-// boundary.
+// shares the W_UK -> W_UV pair's (W_O's where the pair runs as two batched GEMVs); with the cache
+// entry, which takes a spare workgroup of W_UQ's launch, the attention shares W_O's launch and
+// its merge follows.  The attention's workspace follows the chain's at a 256-byte boundary.
 nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* workspace, size_t workspace_bytes,
                      void* stream) {
     if (!chain) return NMM_ERR_NULL;
@@ -611,8 +611,13 @@ nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* work
             return NMM_ERR_HIP;
         if (pair && i == 2) continue;
         if (pair && i == 3) {
-            st = launch_head_pair(c.heads, c.nope, c.qnope_bf16, c.w_uk, c.w_uv, c.lat_f32, c.lat_bf16, c.o_f32, c.o_bf16,
-                                  stream);
+            // with attention beside W_UQ, its merge on the compute units the pair's workgroups leave
+            // free
+            st = att && !c.kv_cache
+                     ? launch_head_pair_merge(c.heads, c.nope, c.qnope_bf16, c.w_uk, c.w_uv, c.lat_f32, c.lat_bf16,
+                                              c.o_f32, c.o_bf16, *att, att_mem, att_ws, stream)
+                     : launch_head_pair(c.heads, c.nope, c.qnope_bf16, c.w_uk, c.w_uv, c.lat_f32, c.lat_bf16, c.o_f32,
+                                        c.o_bf16, stream);
             if (st != NMM_OK) return st;
             continue;
         }
@@ -629,12 +634,12 @@ nmm_status run_chain(const nmm_mla_chain* chain, const AttnArgs* att, void* work
                                              c.q_lora, c.kv_lora, c.rope, c.round, nullptr);
             st = launch_gemv_entry(ch.step[1], ch.plan[1], tickets, part, e, c.down_f32 + c.q_lora, stream);
         } else if (i == 1 && att) {
-            // attention's workgroups on the compute units W_UQ leaves free; its merge rides in
-            // W_O's launch
+            // attention's workgroups on the compute units W_UQ leaves free; its merge rides in the
+            // pair's launch, or W_O's without the pair
             st = launch_gemv_beside_attention(ch.step[1], ch.plan[1], tickets, part, *att, att_mem, att_ws, stream);
         } else if (i == 4 && att && c.kv_cache) {
             st = launch_gemv_attention(ch.step[4], ch.plan[4], tickets, part, *att, att_mem, att_ws, stream);
-        } else if (i == 4 && att) {
+        } else if (i == 4 && att && !pair) {
             st = launch_gemv_merge(ch.step[4], ch.plan[4], tickets, part, *att, att_mem, att_ws, stream);
         } else {
             st = launch_gemv(ch.step[i], ch.plan[i], tickets, part, stream);

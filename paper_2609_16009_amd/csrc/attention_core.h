@@ -503,9 +503,9 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 // sums them in span order with explicit fused multiply-adds, the weights taken from lane s.  A
 // block waits for about two memory round trips.  Two forms, which give the same bits (the same
 // operations on every output, in the same order):
-//  * merge_block: block `blk` owns one head and 256 of its columns, one per thread (heads x
-//    ceil(d_v / 256) blocks): many light blocks, for the workgroups a GEMV launch carries beside
-//    its own.
+//  * merge_block: block `blk` owns one head and 256 of its columns, one per thread `tid` (heads x
+//    ceil(d_v / 256) blocks of 256 threads): many light blocks, for the workgroups another
+//    kernel's launch carries beside its own.
 //  * merge_block_wide: a 128-thread block `blk` owns head blk, thread t taking columns 4 t .. + 3
 //    (d_v <= 512; one block per head), so each load moves 1 KB of a span's row per wave: the
 //    merge launch of the attention on its own.
@@ -529,14 +529,14 @@ __device__ __forceinline__ float2 merge_weights(const AttnParams& p, int64_t bas
     return float2{w, den};
 }
 
-__device__ __forceinline__ void merge_block(const AttnParams& p, int blk) {
+__device__ __forceinline__ void merge_block(const AttnParams& p, int blk, int tid) {
     // no contraction of its own: every translation unit that inlines this rounds alike (the
     // products of the sum are explicit fused multiply-adds)
 #pragma clang fp contract(off)
     const int n_cb = (p.dv + kMergeThreads - 1) / kMergeThreads;
     const int h = blk / n_cb, cb = blk - h * n_cb;
-    const int n = cb * kMergeThreads + static_cast<int>(threadIdx.x);
-    const int lane = threadIdx.x & 63;
+    const int n = cb * kMergeThreads + tid;
+    const int lane = tid & 63;
     const int hb = h / p.hbh, hl = h - hb * p.hbh;
     const int64_t base = int64_t(hb) * p.nsp * p.hbh + hl;      // (block, span 0, head) row
     const float* src = p.part_o + base * p.dv + n;

@@ -524,7 +524,8 @@ __global__ __launch_bounds__(kThreads) void gemv_merge_kernel(const KParams p, c
         gemv_item<NMM_BF16, 1, U, kStorePlain>(p, blockIdx.x, lds, &s_last);
     } else {
         const uint32_t n = gridDim.x - gemv_grid;
-        for (uint32_t b = blockIdx.x - gemv_grid; b < merge_blocks; b += n) attn::merge_block(a, static_cast<int>(b));
+        for (uint32_t b = blockIdx.x - gemv_grid; b < merge_blocks; b += n)
+            attn::merge_block(a, static_cast<int>(b), static_cast<int>(threadIdx.x));
     }
 }
 
@@ -1326,14 +1327,13 @@ struct PairParams {
 };
 
 template <int U, int NW>
-__global__ __launch_bounds__(64 * NW) void head_pair_kernel(const PairParams p) {
+__device__ __forceinline__ void head_pair_block(const PairParams& p, int64_t h) {
     __shared__ __attribute__((aligned(16))) float xs[kPairMaxNope];   // q_nope of the head
     __shared__ __attribute__((aligned(16))) float red[NW * kPairLat];
     __shared__ float lat_s[kPairLat];                                 // lat'_h, widened
     constexpr int kT = 64 * NW;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int64_t h = blockIdx.x;
     const int ta = p.nope / NW;                         // W_UK row-steps (a multiple of U)
     constexpr int kTb = kPairLat / (4 * NW);            // W_UV row-steps
     const __amdgpu_buffer_rsrc_t uk =
@@ -1423,15 +1423,32 @@ __global__ __launch_bounds__(64 * NW) void head_pair_kernel(const PairParams p) 
     }
 }
 
-}  // namespace
-
-bool head_pair_ok(int64_t heads, int64_t nope, int64_t kv_lora, int64_t v_head) {
-    return heads >= 1 && heads < (int64_t(1) << 31) && kv_lora == kPairLat && v_head == kPairV && nope >= 4 * kPairUnroll &&
-           nope <= kPairMaxNope && nope % (4 * kPairUnroll) == 0;
+template <int U, int NW>
+__global__ __launch_bounds__(64 * NW) void head_pair_kernel(const PairParams p) {
+    head_pair_block<U, NW>(p, blockIdx.x);
 }
 
-nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
-                            float* lat, void* lat_bf16, float* o, void* o_bf16, void* stream) {
+// The pair with the merge of an attention launched earlier: workgroups [0, heads) are the pair's,
+// the rest run merge_block's 256-thread blocks (64 NW / 256 per workgroup) in turn.  The pair's
+// one workgroup per head leaves compute units free, and the merge reads only the attention's span
+// partials, so it runs beside the pair instead of under a later GEMV's weight stream.
+template <int U, int NW>
+__global__ __launch_bounds__(64 * NW) void head_pair_merge_kernel(const PairParams p, const attn::AttnParams a,
+                                                                  uint32_t heads, uint32_t merge_blocks) {
+    static_assert((64 * NW) % attn::kMergeThreads == 0, "whole merge blocks per workgroup");
+    if (blockIdx.x < heads) {
+        head_pair_block<U, NW>(p, blockIdx.x);
+        return;
+    }
+    constexpr uint32_t kSub = 64 * NW / attn::kMergeThreads;
+    const uint32_t sub = threadIdx.x / attn::kMergeThreads, t = threadIdx.x % attn::kMergeThreads;
+    const uint32_t n = (gridDim.x - heads) * kSub;
+    for (uint32_t b = (blockIdx.x - heads) * kSub + sub; b < merge_blocks; b += n)
+        attn::merge_block(a, static_cast<int>(b), static_cast<int>(t));
+}
+
+PairParams pair_params(int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv, float* lat,
+                       void* lat_bf16, float* o, void* o_bf16) {
     PairParams pp{};
     pp.q = static_cast<const uint16_t*>(q_nope);
     pp.sq = nope;
@@ -1442,12 +1459,51 @@ nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, con
     pp.o = o;
     pp.ob = static_cast<uint16_t*>(o_bf16);
     pp.nope = static_cast<int>(nope);
+    return pp;
+}
+
+}  // namespace
+
+bool head_pair_ok(int64_t heads, int64_t nope, int64_t kv_lora, int64_t v_head) {
+    return heads >= 1 && heads < (int64_t(1) << 31) && kv_lora == kPairLat && v_head == kPairV && nope >= 4 * kPairUnroll &&
+           nope <= kPairMaxNope && nope % (4 * kPairUnroll) == 0;
+}
+
+nmm_status launch_head_pair(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
+                            float* lat, void* lat_bf16, float* o, void* o_bf16, void* stream) {
+    const PairParams pp = pair_params(nope, q_nope, w_uk, w_uv, lat, lat_bf16, o, o_bf16);
     if (nope % (8 * kPairUnroll) == 0)
         hipLaunchKernelGGL((head_pair_kernel<kPairUnroll, 8>), dim3(static_cast<uint32_t>(heads)), dim3(8 * 64), 0,
                            static_cast<hipStream_t>(stream), pp);
     else
         hipLaunchKernelGGL((head_pair_kernel<kPairUnroll, 4>), dim3(static_cast<uint32_t>(heads)), dim3(4 * 64), 0,
                            static_cast<hipStream_t>(stream), pp);
+    return last_launch_status();
+}
+
+nmm_status launch_head_pair_merge(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
+                                  float* lat, void* lat_bf16, float* o, void* o_bf16, const AttnArgs& a,
+                                  void* attn_ws, size_t attn_ws_bytes, void* stream) {
+    attn::AttnLaunch al;
+    nmm_status st = prepare_attention(a, attn_ws, attn_ws_bytes, &al);
+    if (st != NMM_OK) return st;
+    if (al.merge_grid == 0) return launch_head_pair(heads, nope, q_nope, w_uk, w_uv, lat, lat_bf16, o, o_bf16, stream);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (heads + al.merge_grid >= (int64_t(1) << 31)) {
+        st = launch_head_pair(heads, nope, q_nope, w_uk, w_uv, lat, lat_bf16, o, o_bf16, stream);
+        if (st != NMM_OK) return st;
+        return launch_attention_merge(al, s);
+    }
+    const PairParams pp = pair_params(nope, q_nope, w_uk, w_uv, lat, lat_bf16, o, o_bf16);
+    const uint32_t h = static_cast<uint32_t>(heads), mb = static_cast<uint32_t>(al.merge_grid);
+    // one workgroup per merge block pair (or block, with 4 waves): they take the compute units the
+    // pair leaves free
+    if (nope % (8 * kPairUnroll) == 0) {
+        const uint32_t extra = (mb + 1) / 2;
+        hipLaunchKernelGGL((head_pair_merge_kernel<kPairUnroll, 8>), dim3(h + extra), dim3(8 * 64), 0, s, pp, al.p, h, mb);
+    } else {
+        hipLaunchKernelGGL((head_pair_merge_kernel<kPairUnroll, 4>), dim3(h + mb), dim3(4 * 64), 0, s, pp, al.p, h, mb);
+    }
     return last_launch_status();
 }
 

@@ -158,7 +158,7 @@ nmm_status attention_workspace_bytes(const AttnArgs& a, size_t* bytes);
 nmm_status validate_attention_args(const AttnArgs& a, void* workspace, size_t workspace_bytes);
 // The GEMV `g` (plain launch) and the attention `a` in one launch where both fit it (bf16, M = 1,
 // the 576 / 512 attention shape, the GEMV's LDS within one attention chunk buffer): attention's
-// workgroups follow the GEMV's, then attention's merge.  Other shapes take the two launches in
+// workgroups first, then the GEMV's; then attention's merge launch.  Other shapes take the two launches in
 // order.  The two must not touch each other's buffers.
 nmm_status launch_gemv_attention(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
                                  const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
@@ -170,5 +170,10 @@ nmm_status launch_gemv_beside_attention(const GemvArgs& g, const GemvPlan& gp, u
                                         const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
 nmm_status launch_gemv_merge(const GemvArgs& g, const GemvPlan& gp, unsigned* tickets, float* part,
                              const AttnArgs& a, void* attn_ws, size_t attn_ws_bytes, void* stream);
+// launch_head_pair carrying the merge of an attention launched earlier (as launch_gemv_merge):
+// extra workgroups after the pair's run the merge blocks.
+nmm_status launch_head_pair_merge(int64_t heads, int64_t nope, const void* q_nope, const void* w_uk, const void* w_uv,
+                                  float* lat, void* lat_bf16, float* o, void* o_bf16, const AttnArgs& a,
+                                  void* attn_ws, size_t attn_ws_bytes, void* stream);
 
 }  // namespace nmm
