@@ -1,6 +1,7 @@
 """GPU parity of the decode step (nmm_mla_decode_step: the MLA chain and an independent latent
-attention, the attention's workgroups sharing W_UQ's launch and its merge W_O's, or with a cache
-entry the attention in W_O's launch), through the C ABI.
+attention, the attention's workgroups sharing W_UQ's launch and its merge the W_UK -> W_UV pair's
+(W_O's for chains without the pair), or with a cache entry the attention in W_O's launch),
+through the C ABI.
 
 The step must reproduce, bit for bit, what the chain (nmm_mla_decode_chain) and the attention
 (nmm_latent_attention_ex with the same partition) write when run on their own: the shared launch
@@ -16,7 +17,7 @@ import torch
 import oracle
 import synthetic as syn
 from gpu_util import assert_parity, dev16, host_bits
-from test_chain_gpu import alloc_chain, check_chain_stepwise, check_kv_row, kv_for, small_step
+from test_chain_gpu import alloc_chain, check_chain_stepwise, check_kv_row, kv_for, pair_step, small_step
 
 pytestmark = pytest.mark.gpu
 
@@ -92,6 +93,25 @@ def test_small_step_matches_chain_and_attention(heads, seq, dqk, dv, splits):
     check_chain_stepwise(step, bufs)
     ref, ref_abs = oracle.latent_attention(qb, kvb, scale, dqk=dqk, dv=dv)
     assert_parity(out, ref, ref_abs, what=f"attention {heads}x{seq} {dqk}/{dv}")
+
+
+@pytest.mark.parametrize("heads,nope,a_heads,seq,dqk,dv,splits", [
+    (3, 64, 20, 1000, 576, 512, 5),   # the pair's 4-wave form: one merge block per extra workgroup
+    (5, 128, 5, 700, 128, 64, 4),     # 8-wave form, two blocks per workgroup, an odd number of blocks
+])
+def test_paired_step_carries_the_merge(heads, nope, a_heads, seq, dqk, dv, splits):
+    step = pair_step(heads * 100 + nope, heads, nope)
+    qb, kvb, scale = syn.attention_case(60 + a_heads, a_heads, seq, dqk=dqk, dv=dv)
+    q, kv, out, outb = attn_bufs(qb, kvb, dv)
+    bufs = alloc_chain(step)
+    nmm.nmm_mla_decode_step(step.dims, bufs, dict(q=q, kv=kv, out=out, out_bf16=outb, scale=scale, splits=splits,
+                                                  d_qk=dqk, d_v=dv))
+    torch.cuda.synchronize()
+    sep, out2, outb2 = run_separately(step, q, kv, scale, splits, dqk, dv)
+    assert_same(bufs, sep, out, out2, outb, outb2)
+    check_chain_stepwise(step, bufs)
+    ref, ref_abs = oracle.latent_attention(qb, kvb, scale, dqk=dqk, dv=dv)
+    assert_parity(out, ref, ref_abs, what=f"attention {a_heads}x{seq} {dqk}/{dv} merged beside the pair")
 
 
 def test_step_with_cache_entry_and_no_bf16_copy():
