@@ -205,10 +205,9 @@ namespace nmm {
 
 nmm_status launch_attention_merge(const AttnLaunch& l, hipStream_t s) {
     if (l.merge_grid == 0) return NMM_OK;
-    // merge_block_wide's blocks (one per head); merge_grid counts merge_block's, which the GEMV
-    // launches that carry the merge use
-    hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(l.p.heads)), dim3(kMergeWideThreads), 0, s,
-                       l.p);
+    static_assert(4 * kMergeWideThreads == kMergeThreads, "the two merge forms cut a head's columns alike");
+    hipLaunchKernelGGL(attention_merge_kernel, dim3(static_cast<uint32_t>(l.merge_grid)), dim3(kMergeWideThreads), 0,
+                       s, l.p);
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
 }
 

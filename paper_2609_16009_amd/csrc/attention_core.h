@@ -506,12 +506,12 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 //  * merge_block: block `blk` owns one head and 256 of its columns, one per thread `tid` (heads x
 //    ceil(d_v / 256) blocks of 256 threads): many light blocks, for the workgroups another
 //    kernel's launch carries beside its own.
-//  * merge_block_wide: a 128-thread block `blk` owns head blk, thread t taking columns 4 t .. + 3
-//    (d_v <= 512; one block per head), so each load moves 1 KB of a span's row per wave: the
-//    merge launch of the attention on its own.
+//  * merge_block_wide: a one-wave block `blk` owns 256 columns of one head (ceil(d_v / 256) blocks
+//    per head, the same count as merge_block's), thread t taking four of them, so each load moves
+//    1 KB of a span's row: the merge launch of the attention on its own.
 constexpr int kMergeThreads = 256;
 constexpr int kMergeBatch = 32;
-constexpr int kMergeWideThreads = 128;   // threads per block of merge_block_wide (one head)
+constexpr int kMergeWideThreads = 64;    // threads per block of merge_block_wide (256 columns)
 constexpr int kMergeWideBatch = 16;  // spans merge_block_wide loads at once
 
 // M's weight of this lane's span and the normaliser sum_s w_s l_s, the same in every lane
@@ -566,8 +566,9 @@ __device__ __forceinline__ void merge_block(const AttnParams& p, int blk, int ti
 __device__ __forceinline__ void merge_block_wide(const AttnParams& p, int blk) {
 #pragma clang fp contract(off)
     const int tid = static_cast<int>(threadIdx.x);
-    const int h = blk;
-    const int c = 4 * tid;
+    const int n_cb = (p.dv + 4 * kMergeWideThreads - 1) / (4 * kMergeWideThreads);
+    const int h = blk / n_cb;
+    const int c = (blk - h * n_cb) * 4 * kMergeWideThreads + 4 * tid;
     const int lane = tid & 63;
     const int hb = h / p.hbh, hl = h - hb * p.hbh;
     const int64_t base = int64_t(hb) * p.nsp * p.hbh + hl;
@@ -608,8 +609,8 @@ __device__ __forceinline__ void merge_block_wide(const AttnParams& p, int blk) {
 }
 
 // A prepared attention call: kernel arguments, the attention grid (0: nothing to launch), the
-// number of merge_block blocks (0: one span, no merge; the merge launch of its own runs
-// merge_block_wide's instead) and the kernel variant.
+// number of merge blocks (0: one span, no merge; merge_block and merge_block_wide take the same
+// count) and the kernel variant.
 constexpr int kAttnExact = 1;      // d_qk 576, d_v 512
 constexpr int kAttnGeneral = 2;    // d_qk <= 576, d_v <= 512
 struct AttnLaunch {

@@ -344,6 +344,35 @@ def test_attention_spans_and_workspace_serve_both_head_blocks(heads, seq, splits
     assert ws == ticket + -(-heads // 32) * 32 * nsp * (dv + 2) * 4
 
 
+@pytest.mark.parametrize("heads,dv,nsp,hbh", [(128, 512, 16, 16), (128, 512, 16, 32), (70, 512, 3, 16),
+                                             (20, 64, 5, 32), (5, 272, 64, 16), (33, 16, 2, 32)])
+def test_merge_blocks_cover_every_output_once(heads, dv, nsp, hbh):
+    """The two merge forms over heads x ceil(d_v / 256) blocks: merge_block (256 threads, one column
+    each) and merge_block_wide (64 threads, four columns each) must each write every (head,
+    column < d_v) exactly once, and read the span partials [n_hb][nsp][hbh][d_v] and
+    [n_hb][nsp][hbh][2] only inside those arrays."""
+    n_cb = -(-dv // 256)
+    blocks = heads * n_cb
+    n_hb = -(-heads // hbh)
+    o_size, ml_size = n_hb * nsp * hbh * dv, n_hb * nsp * hbh * 2
+    for threads, width in ((256, 1), (64, 4)):
+        seen = np.zeros((heads, dv), dtype=np.int64)
+        for blk in range(blocks):
+            h, cb = divmod(blk, n_cb)
+            hb, hl = divmod(h, hbh)
+            base = hb * nsp * hbh + hl
+            for t in range(threads):
+                c = cb * 256 + width * t
+                if c >= dv:
+                    continue
+                for s_ in range(nsp):
+                    first = (base + s_ * hbh) * dv + c
+                    assert 0 <= first and first + width <= o_size
+                    assert (base + s_ * hbh) * 2 + 2 <= ml_size
+                seen[h, c:c + width] += 1
+        assert np.all(seen == 1), (threads, width)
+
+
 @pytest.mark.parametrize("n_hb,nsp", [(2, 16), (2, 11), (2, 32), (1, 9), (3, 22), (2, 3), (1, 1), (2, 64)])
 def test_attention_workgroups_cover_every_head_block_and_span_once(n_hb, nsp):
     """attention_block's workgroup -> (head block, span) map: from 8 spans on (xcd_map) the grid
