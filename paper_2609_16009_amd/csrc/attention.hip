@@ -23,6 +23,9 @@
 //  * P.V is split by output columns: position group w % 4 accumulates O^T = V^T . P^T for the
 //    16-column tiles w % 4, w % 4 + 4, ... of its heads, V^T fragments read from the staged rows
 //    by ds_read_b64_tr_b16 (gfx950's transposing LDS read).  The accumulators stay in registers.
+//    At 576 / 512, while the grid fits one workgroup per CU, two workgroups share each (head
+//    block, span), each taking half of the column tiles (both compute the scores): twice the
+//    workgroups, each with half the P.V work and half the stores.
 //  * Spans write (reference, sum, unnormalised output) partials; a merge kernel on the same
 //    stream combines them in span order.  The head blocks of one span run on one XCD (workgroup
 //    ids 8 apart), so its L2 reads the span's cache rows from HBM once for all of them.
@@ -50,11 +53,13 @@ constexpr int kAloneHeads = 16;
 constexpr int kSharedHeads = 16 * kHt;   // 32
 constexpr int kMaxSpans = 64;             // the merge gives each span one lane of a wave
 constexpr int kDefaultPairs = 64;         // default partition: about this many (32-head block, span) pairs
+constexpr int kComputeUnits = 256;        // MI355X; an attention workgroup holds a CU (its LDS)
 
-// Attention launch workgroups of HT head tiles.
-template <int HT, bool EXACT>
+// Attention launch workgroups of HT head tiles, each taking 4 NTW of d_v's 16-column tiles (of
+// VS column parts).
+template <int HT, int NTW, bool EXACT, int VS>
 __global__ __launch_bounds__(kAThreads) void attention_kernel(const AttnParams p) {
-    attention_block<HT, kMaxKs, kMaxNtw, EXACT>(p, blockIdx.x);
+    attention_block<HT, kMaxKs, NTW, EXACT, VS>(p, blockIdx.x);
 }
 
 __global__ __launch_bounds__(kMergeWideThreads) void attention_merge_kernel(const AttnParams p) {
@@ -63,6 +68,7 @@ __global__ __launch_bounds__(kMergeWideThreads) void attention_merge_kernel(cons
 
 struct AttnPlan {
     int hbh = kAloneHeads;
+    int vsplit = 1;     // workgroups per (head block, span)
     int n_hb = 0, nsp = 1, span = 0, xcd_map = 0, cols = 0, pitch = 0;
     int grid_sp = 1;    // spans in the grid: nsp, padded to a multiple of 8 when xcd_map
     size_t ws_bytes = 0;
@@ -95,6 +101,11 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     // the grid is padded and the padding workgroups exit at once
     a.xcd_map = (a.nsp % 8 == 0 || a.nsp > 8) ? 1 : 0;
     a.grid_sp = a.xcd_map ? (a.nsp + 7) / 8 * 8 : a.nsp;
+    // the 576 / 512 shape in 16-head blocks splits d_v over two workgroups per (head block, span)
+    // while the grid still fits one workgroup per CU
+    if (hbh == kAloneHeads && dqk == kMaxCols && dv == 16 * 4 * kMaxNtw &&
+        int64_t(a.n_hb) * 2 * a.grid_sp <= kComputeUnits)
+        a.vsplit = 2;
     // partial results live past the workspace's counter block (which GEMV calls sharing the
     // workspace rely on being zero)
     if (a.nsp > 1)
@@ -104,12 +115,14 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
 }
 
 template <bool EXACT>
-nmm_status launch_attention(const AttnParams& p, int64_t grid, hipStream_t s) {
+nmm_status launch_attention(const AttnParams& p, int64_t grid, int vsplit, hipStream_t s) {
     const dim3 g(static_cast<uint32_t>(grid));
-    if (p.hbh == kAloneHeads)
-        hipLaunchKernelGGL((attention_kernel<1, EXACT>), g, dim3(kAThreads), 0, s, p);
+    if (vsplit == 2)
+        hipLaunchKernelGGL((attention_kernel<1, kMaxNtw / 2, true, 2>), g, dim3(kAThreads), 0, s, p);
+    else if (p.hbh == kAloneHeads)
+        hipLaunchKernelGGL((attention_kernel<1, kMaxNtw, EXACT, 1>), g, dim3(kAThreads), 0, s, p);
     else
-        hipLaunchKernelGGL((attention_kernel<kHt, EXACT>), g, dim3(kAThreads), 0, s, p);
+        hipLaunchKernelGGL((attention_kernel<kHt, kMaxNtw, EXACT, 1>), g, dim3(kAThreads), 0, s, p);
     return hipGetLastError() == hipSuccess ? NMM_OK : NMM_ERR_HIP;
 }
 
@@ -183,9 +196,10 @@ nmm_status prepare(int64_t heads, int64_t seq, int64_t d_qk, int64_t d_v, const 
     p.scale_log2 = scale * 1.4426950408889634f;
     p.kv_extent = static_cast<uint32_t>(extent);
     p.q_extent = static_cast<uint32_t>(q_extent);
-    out->grid = int64_t(a.n_hb) * a.grid_sp;
+    out->grid = int64_t(a.n_hb) * a.vsplit * a.grid_sp;
     out->merge_grid = a.nsp > 1 ? heads * ((d_v + kMergeThreads - 1) / kMergeThreads) : 0;
     out->variant = (d_qk == 576 && d_v == 512) ? kAttnExact : kAttnGeneral;
+    out->vsplit = a.vsplit;
     return NMM_OK;
 }
 
@@ -213,7 +227,8 @@ nmm_status launch_attention_merge(const AttnLaunch& l, hipStream_t s) {
 
 nmm_status launch_attention_kernel(const AttnLaunch& l, hipStream_t s) {
     if (l.grid == 0) return NMM_OK;
-    return l.variant == kAttnExact ? launch_attention<true>(l.p, l.grid, s) : launch_attention<false>(l.p, l.grid, s);
+    return l.variant == kAttnExact ? launch_attention<true>(l.p, l.grid, l.vsplit, s)
+                                   : launch_attention<false>(l.p, l.grid, l.vsplit, s);
 }
 
 nmm_status launch_prepared_attention(const AttnLaunch& l, hipStream_t s) {

@@ -166,22 +166,27 @@ __device__ __forceinline__ int* flag_buffer() {
     return flags;
 }
 
-// The (head block, span) of workgroup `bid`; false for the padding workgroups of an XCD-grouped
-// grid.  With xcd_map the workgroups of one span (every head block) are 8 ids apart, so they run
-// on one XCD and its L2 serves the span's cache rows to all of them.
-__device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int* hb, int* sp) {
+// The (head block x VS + column part, span) of workgroup `bid`, nb = n_hb x VS of the first; false
+// for the padding workgroups of an XCD-grouped grid.  With xcd_map the workgroups of one span
+// (every head block and column part) are 8 ids apart, so they run on one XCD and its L2 serves the
+// span's cache rows to all of them.
+__device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int nb, int* hb, int* sp) {
     if (p.xcd_map) {
-        *sp = (bid & 7) + 8 * (bid / (8 * p.n_hb));
-        *hb = (bid >> 3) % p.n_hb;
+        *sp = (bid & 7) + 8 * (bid / (8 * nb));
+        *hb = (bid >> 3) % nb;
         return *sp < p.nsp;
     }
-    *hb = bid % p.n_hb;
-    *sp = bid / p.n_hb;
+    *hb = bid % nb;
+    *sp = bid / nb;
     return true;
 }
 
 // One attention workgroup: HT * 16 heads (head block hb) over one span of positions, with 4 waves.
-// Wave w is position group pw = w and covers all HT head tiles.
+// Wave w is position group pw = w and covers all HT head tiles.  With VS = 2 two workgroups share
+// a (head block, span): both compute the scores and probabilities, and each the product with V,
+// its stores and the merge's inputs for half of d_v's column tiles (4 NTW tiles from tile0); the
+// first also stores the reference and sum.  Each output column sees the same operations either
+// way.
 //  * Q.K^T: a wave computes the scores of positions 16 pw .. + 15 of each 64-position chunk for its
 //    head tiles (S^T = K . Q^T on the matrix cores, K fragments read from LDS and used for each of
 //    the wave's head tiles; Q held in registers as MFMA fragments).
@@ -195,7 +200,7 @@ __device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int* hb, 
 //  * The result is stored straight from the accumulators, 64 contiguous bytes of 16 rows per store.
 // KS = d_qk / 32 and NTW = column tiles per position group are upper bounds; EXACT: the shape
 // matches them.
-template <int HT, int KS, int NTW, bool EXACT>
+template <int HT, int KS, int NTW, bool EXACT, int VS = 1>
 __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     constexpr int W = kAWaves;
     constexpr int HB = 16 * HT;
@@ -217,8 +222,11 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     const int spr = pitch / 8;
     const uint32_t row_bytes = uint32_t(p.ldkv) * 2;
 
-    int hb, sp;
-    if (!block_of(p, bid, &hb, &sp)) return;
+    static_assert(VS == 1 || VS == 2, "one or two column parts");
+    int hbv, sp;
+    if (!block_of(p, bid, p.n_hb * VS, &hbv, &sp)) return;
+    const int vh = hbv % VS, hb = hbv / VS;
+    const int tile0 = vh * 4 * NTW;            // the workgroup's first 16-column tile of d_v
     const int h0 = hb * HB;
     const int s_begin = sp * p.span;
     const int s_end = min(p.seq, s_begin + p.span);
@@ -412,7 +420,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
             for (int i = 0; i < NTW; ++i) {
                 const int ct = pw + 4 * i;
                 if (EXACT || ct < ntiles) {
-                    const uint16_t* base = vrow + 16 * ct;
+                    const uint16_t* base = vrow + 16 * (tile0 + ct);
                     const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base));
                     const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(base + 4 * pitch));
                     const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
@@ -472,7 +480,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
                     const int ct = pw + 4 * i;
                     if (EXACT || ct < ntiles) {
                         const f32x4 v = o[i][t] * scl;
-                        const int c = 16 * ct + 4 * g;
+                        const int c = 16 * (tile0 + ct) + 4 * g;
                         *reinterpret_cast<f32x4*>(p.out + int64_t(h) * p.ldo + c) = v;
                         if (p.outb) {
                             uint16_t* d = p.outb + int64_t(h) * p.ldob + c;
@@ -489,9 +497,9 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 #pragma unroll
             for (int i = 0; i < NTW; ++i) {
                 const int ct = pw + 4 * i;
-                if (EXACT || ct < ntiles) *reinterpret_cast<f32x4*>(dst + 16 * ct) = o[i][t];
+                if (EXACT || ct < ntiles) *reinterpret_cast<f32x4*>(dst + 16 * (tile0 + ct)) = o[i][t];
             }
-            if (pw == 0 && g == 0) *reinterpret_cast<float2*>(p.part_ml + (pidx * HB + row) * 2) = float2{m_ref[t], lsum[t]};
+            if (vh == 0 && pw == 0 && g == 0) *reinterpret_cast<float2*>(p.part_ml + (pidx * HB + row) * 2) = float2{m_ref[t], lsum[t]};
         }
     }
 }
@@ -618,6 +626,7 @@ struct AttnLaunch {
     int64_t grid = 0;
     int64_t merge_grid = 0;
     int variant = 0;
+    int vsplit = 1;    // workgroups per (head block, span), each taking 1 / vsplit of d_v's columns
 };
 
 }  // namespace attn

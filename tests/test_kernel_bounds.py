@@ -373,27 +373,31 @@ def test_merge_blocks_cover_every_output_once(heads, dv, nsp, hbh):
         assert np.all(seen == 1), (threads, width)
 
 
-@pytest.mark.parametrize("n_hb,nsp", [(2, 16), (2, 11), (2, 32), (1, 9), (3, 22), (2, 3), (1, 1), (2, 64)])
-def test_attention_workgroups_cover_every_head_block_and_span_once(n_hb, nsp):
-    """attention_block's workgroup -> (head block, span) map: from 8 spans on (xcd_map) the grid
-    holds nsp padded to a multiple of 8 per head block, workgroup b takes span (b % 8) + 8 (b / 8
-    n_hb) of head block (b / 8) % n_hb, and the padding spans exit; otherwise the plain order.
-    Every (head block, span) runs once, and with xcd_map the workgroups of one span sit 8 ids
-    apart, on one XCD (ids are dealt to the 8 XCDs round robin; the decode step's launch puts
-    attention after 224 GEMV workgroups, a multiple of 8)."""
+@pytest.mark.parametrize("n_hb,nsp,vsplit", [(2, 16, 1), (2, 11, 1), (2, 32, 1), (1, 9, 1), (3, 22, 1), (2, 3, 1),
+                                            (1, 1, 1), (2, 64, 1), (8, 16, 2), (8, 8, 2), (5, 21, 2), (1, 3, 2)])
+def test_attention_workgroups_cover_every_head_block_and_span_once(n_hb, nsp, vsplit):
+    """attention_block's workgroup -> (head block, column part, span) map, with nb = n_hb x vsplit
+    (head block hb, column part v at hb vsplit + v): from 8 spans on (xcd_map) the grid holds nsp
+    padded to a multiple of 8 per nb, workgroup b takes span (b % 8) + 8 (b / 8 nb) of index
+    (b / 8) % nb, and the padding spans exit; otherwise the plain order.  Every (head block,
+    column part, span) runs once, and with xcd_map the workgroups of one span sit 8 ids apart, on
+    one XCD (ids are dealt to the 8 XCDs round robin; the decode step's shared launches put the
+    attention's workgroups first)."""
+    nb = n_hb * vsplit
     xcd_map = nsp % 8 == 0 or nsp > 8
     grid_sp = (nsp + 7) // 8 * 8 if xcd_map else nsp
     seen = {}
-    for b in range(n_hb * grid_sp):
+    for b in range(nb * grid_sp):
         if xcd_map:
-            sp, hb = (b & 7) + 8 * (b // (8 * n_hb)), (b >> 3) % n_hb
+            sp, hbv = (b & 7) + 8 * (b // (8 * nb)), (b >> 3) % nb
             if sp >= nsp:
                 continue
         else:
-            hb, sp = b % n_hb, b // n_hb
-        assert (hb, sp) not in seen
-        seen[(hb, sp)] = b
-    assert set(seen) == {(h, s_) for h in range(n_hb) for s_ in range(nsp)}
+            hbv, sp = b % nb, b // nb
+        key = (hbv // vsplit, hbv % vsplit, sp)
+        assert key not in seen
+        seen[key] = b
+    assert set(seen) == {(h, v, s_) for h in range(n_hb) for v in range(vsplit) for s_ in range(nsp)}
     if xcd_map:
         for s_ in range(nsp):
-            assert len({seen[(h, s_)] % 8 for h in range(n_hb)}) == 1
+            assert len({seen[(h, v, s_)] % 8 for h in range(n_hb) for v in range(vsplit)}) == 1
