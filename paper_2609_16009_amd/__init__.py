@@ -504,7 +504,8 @@ class PreparedStep:
 def nmm_mla_decode_step(dims: dict, bufs: dict, attn: dict, *, workspace=None, stream=None, events=None,
                         kv: dict | None = None) -> None:
     """One decode step (see nmm.h): the chain of nmm_mla_decode_chain and the attention ``attn``
-    ({q, kv, out, scale[, out_bf16, splits, d_qk, d_v]}), the attention sharing W_O's launch."""
+    ({q, kv, out, scale[, out_bf16, splits, d_qk, d_v]}) beside it (its workgroups in W_UQ's
+    launch, its merge in the W_UK -> W_UV pair's)."""
     PreparedStep(dims, bufs, attn, workspace=workspace, events=None if events is None else [events],
                  kv=kv).launch(stream=stream)
 

@@ -201,3 +201,39 @@ def test_step_with_no_attention_heads_is_the_chain():
     for k in OUTPUTS:
         assert torch.equal(bufs[k].view(torch.int16) if bufs[k].dtype == torch.bfloat16 else bufs[k],
                            sep[k].view(torch.int16) if sep[k].dtype == torch.bfloat16 else sep[k]), k
+
+
+def test_full_size_step_soak_bit_identical():
+    # 200 full-size steps on one workspace: the chain's split-K gathers, the attention beside
+    # W_UQ and its merge beside the pair give every output the same bits each time, and the
+    # chain's arrival counters are back at zero after the last
+    step = syn.decode_step()
+    q, kv, out, outb = attn_bufs(step.q, step.kv, syn.ATTN_DV)
+    bufs = alloc_chain(step)
+    ws = nmm.Workspace()
+    prepared = nmm.PreparedStep(step.dims, bufs, dict(q=q, kv=kv, out=out, out_bf16=outb, scale=step.scale,
+                                                      splits=16), workspace=ws)
+    prepared.launch()
+    torch.cuda.synchronize()
+    first = {k: bufs[k].clone() for k in OUTPUTS}
+    out0, outb0 = out.clone(), outb.clone()
+    saved = {k: torch.empty((20,) + tuple(v.shape), dtype=v.dtype, device="cuda") for k, v in first.items()}
+    outs = torch.empty((20,) + tuple(out.shape), dtype=out.dtype, device="cuda")
+    outbs = torch.empty((20,) + tuple(outb.shape), dtype=outb.dtype, device="cuda")
+    for batch in range(10):
+        for i in range(20):
+            prepared.launch()
+            for k in OUTPUTS:
+                saved[k][i].copy_(bufs[k])
+            outs[i].copy_(out)
+            outbs[i].copy_(outb)
+        torch.cuda.synchronize()
+        for k in OUTPUTS:
+            a, b = saved[k], first[k].unsqueeze(0).expand_as(saved[k])
+            if a.dtype == torch.bfloat16:
+                a, b = a.view(torch.int16), b.view(torch.int16)
+            assert torch.equal(a, b), f"step {batch * 20}..{batch * 20 + 19}: {k} differs from the first step"
+        assert torch.equal(outs, out0.unsqueeze(0).expand_as(outs)), f"steps {batch * 20}..: attention output"
+        assert torch.equal(outbs.view(torch.int16), outb0.view(torch.int16).unsqueeze(0).expand_as(outbs)), \
+            f"steps {batch * 20}..: attention bf16 copy"
+    assert int(ws.buf[:65536].view(torch.int32).abs().sum()) == 0
