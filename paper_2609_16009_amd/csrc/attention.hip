@@ -52,7 +52,9 @@ using namespace attn;
 constexpr int kAloneHeads = 16;
 constexpr int kSharedHeads = 16 * kHt;   // 32
 constexpr int kMaxSpans = 64;             // the merge gives each span one lane of a wave
-constexpr int kDefaultPairs = 64;         // default partition: about this many (32-head block, span) pairs
+constexpr int kDefaultPairs = 64;         // default partition: about this many (32-head block, span) pairs,
+constexpr int kDefaultMinChunks = 2;      // and spans of at least this many chunks (one-chunk spans merge
+                                          // more partials than their parallelism saves)
 constexpr int kComputeUnits = 256;        // MI355X; an attention workgroup holds a CU (its LDS)
 
 // Attention launch workgroups of HT head tiles, each taking 4 NTW of d_v's 16-column tiles (of
@@ -90,7 +92,10 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     a.pitch = a.cols + 8 * kPadSlots;
     const int64_t wide_blocks = (heads + kSharedHeads - 1) / kSharedHeads;
     const int64_t max_sp = (seq + kCh - 1) / kCh;
-    int64_t nsp = splits > 0 ? splits : std::max<int64_t>(1, kDefaultPairs / std::max<int64_t>(1, wide_blocks));
+    const int64_t few_chunk_spans = (seq + kDefaultMinChunks * kCh - 1) / (kDefaultMinChunks * kCh);
+    int64_t nsp = splits > 0 ? splits
+                             : std::max<int64_t>(1, std::min<int64_t>(few_chunk_spans,
+                                                                      kDefaultPairs / std::max<int64_t>(1, wide_blocks)));
     nsp = std::min(std::min(nsp, max_sp), int64_t(kMaxSpans));
     int64_t span = (seq + nsp - 1) / nsp;
     span = (span + kCh - 1) / kCh * kCh;
