@@ -465,7 +465,8 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 
     // ---- the block's [HB][d_v] result straight from the accumulators: lane (g, j) holds columns
     // 16 ct + 4 g .. + 3 of its head, so each store instruction writes 64 contiguous bytes of 16
-    // rows; normalised when the span is the whole sequence, else the span's partial
+    // rows; normalised when the span is the whole sequence, else the span's partial (stored
+    // non-temporal: it is read once, by the merge on other XCDs)
     const bool whole = p.nsp == 1;
     const int64_t pidx = int64_t(hb) * p.nsp + sp;
 #pragma unroll
@@ -497,7 +498,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
 #pragma unroll
             for (int i = 0; i < NTW; ++i) {
                 const int ct = pw + 4 * i;
-                if (EXACT || ct < ntiles) *reinterpret_cast<f32x4*>(dst + 16 * (tile0 + ct)) = o[i][t];
+                if (EXACT || ct < ntiles) __builtin_nontemporal_store(o[i][t], reinterpret_cast<f32x4*>(dst + 16 * (tile0 + ct)));
             }
             if (vh == 0 && pw == 0 && g == 0) *reinterpret_cast<float2*>(p.part_ml + (pidx * HB + row) * 2) = float2{m_ref[t], lsum[t]};
         }
