@@ -160,3 +160,21 @@ def test_attention_ex_partition_and_bf16_copy(splits):
     bits = host_bits(outb)
     assert np.array_equal(bits[:, :512], oracle.round_bf16(out.cpu().numpy()))
     assert np.all(bits[:, 512:] == 0)
+
+
+def test_attention_random_shapes_and_partitions():
+    # a seeded sweep over head counts (ragged 16- and 32-head blocks), lengths (one chunk, ragged
+    # last chunks and spans) and partitions (the default, one span, fewer or more spans than 8,
+    # so both workgroup maps and the padded grid, with and without the two-workgroup column
+    # split): every head of every case against the oracle
+    rng = np.random.default_rng(2024)
+    for case in range(16):
+        heads = int(rng.integers(1, 150))
+        seq = int(rng.integers(1, 2600))
+        splits = int(rng.choice([0, 0, 1, 2, 3, 5, 8, 11, 16, 23, 32, 64]))
+        q, kv, scale = syn.attention_case(300 + case, heads, seq)
+        out = torch.full((heads, 512), float("nan"), dtype=torch.float32, device="cuda")
+        nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, scale, splits=splits)
+        torch.cuda.synchronize()
+        ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=576, dv=512)
+        assert_parity(out, ref, ref_abs, what=f"case {case}: {heads} heads x {seq} positions, splits {splits}")
