@@ -250,3 +250,21 @@ def kv_update_case(seed: int = 5, hidden: int = HIDDEN, kv_lora: int = KV_LORA, 
     if ldw is not None and ldw != kv_lora + rope:
         w = padded(w, ldw)
     return KvUpdateCase(h, w, gamma, kv_lora, rope, position)
+
+
+def random_gemv_shapes(seed: int = 31, n: int = 20) -> list[tuple[int, int, int, int, int, int, str]]:
+    """Seeded (M, K, N, dt, ldx, ldw, path) cases for a sweep of the GEMV entry points: M 1-40,
+    K 1-9000, N 1-3000, either 16-bit type, row pitches rounded up to 8 elements plus 0, 8 or 64
+    more, and the path asked for ("gemv", "mfma" or "auto").  Shapes only: the GPU tests draw
+    their inputs with gemv_case, and the launch-bounds model checks the same cases."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        M = int(rng.integers(1, 41))
+        K = int(rng.integers(1, 9001))
+        N = int(rng.integers(1, 3001))
+        dt = int(rng.choice([F16, BF16]))
+        ldx = (K + 7) // 8 * 8 + int(rng.choice([0, 8]))
+        ldw = (N + 7) // 8 * 8 + int(rng.choice([0, 8, 64]))
+        out.append((M, K, N, dt, ldx, ldw, str(rng.choice(["gemv", "mfma", "auto"]))))
+    return out

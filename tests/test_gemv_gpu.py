@@ -89,6 +89,15 @@ def test_ragged_integer_exact(M, K, N, dt):
     check_case(c, path=nmm.NMM_PATH_GEMV)
 
 
+@pytest.mark.parametrize("case", syn.random_gemv_shapes(), ids=lambda c: f"{c[0]}x{c[1]}x{c[2]}_{c[6]}")
+def test_random_shapes_integer_exact(case):
+    # a seeded sweep over M, K, N, both 16-bit types, padded pitches and the three path choices
+    # (the launch-bounds model checks the same cases): small integers, so every output is exact
+    M, K, N, dt, ldx, ldw, path = case
+    c = syn.gemv_case(500 + M + K % 97, M, K, N, dt, integer=True, ldx=ldx, ldw=ldw, name=f"random_{M}x{K}x{N}_{path}")
+    check_case(c, path={"gemv": nmm.NMM_PATH_GEMV, "mfma": nmm.NMM_PATH_MFMA, "auto": nmm.NMM_PATH_AUTO}[path])
+
+
 def test_largest_weight_extent_on_every_path():
     # one weight [65521, 16384] bf16 whose extent, 65521 * 16384 * 2 = 2^31 - 491,520 bytes, is just
     # under the 2^31-byte limit, so the 32-bit buffer offsets take their largest values.  As W

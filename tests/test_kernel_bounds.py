@@ -7,6 +7,7 @@ import numpy as np
 import pytest
 
 nmm = pytest.importorskip("paper_2609_16009_amd")
+import synthetic as syn  # noqa: E402
 
 WAVES, THREADS = 4, 256
 
@@ -110,7 +111,11 @@ def test_strided_query_slice_in_bounds():
                                            (8, 100, 8, 104, 8), (32, 20000, 300, 20000, 304),
                                            (16, 65521, 16383, 65528, 16384)])
 def test_mfma_launch_stays_in_bounds(M, K, N, ldx, ldw):
-    p = nmm.nmm_gemv_plan(M, K, N, nmm.NMM_BF16, nmm.NMM_PATH_MFMA)
+    check_mfma_launch(M, K, N, ldx, ldw)
+
+
+def check_mfma_launch(M, K, N, ldx, ldw, dt=None):
+    p = nmm.nmm_gemv_plan(M, K, N, nmm.NMM_BF16 if dt is None else dt, nmm.NMM_PATH_MFMA)
     mt, rows, ks, panels = p["m_tile"], p["rows_full"], p["split_k_full"], p["n_full_panels"]
     assert mt in (16, 32) and rows % 64 == 0 and ks * rows >= K and (ks - 1) * rows < K
     assert panels * 128 >= N and (panels - 1) * 128 < N
@@ -148,6 +153,20 @@ def test_mfma_launch_stays_in_bounds(M, K, N, ldx, ldw):
         # outputs of the tile stay inside y / the partial buffer
         assert n0 + 127 >= min(N - 1, n0)
     assert p["grid"] == p["m_blocks"] * panels * ks
+
+
+@pytest.mark.parametrize("case", syn.random_gemv_shapes(), ids=lambda c: f"{c[0]}x{c[1]}x{c[2]}_{c[6]}")
+def test_random_gemv_shapes_stay_in_bounds(case):
+    """The seeded sweep the GPU tests run (synthetic.random_gemv_shapes), through the model of the
+    path each call takes."""
+    M, K, N, dt, ldx, ldw, path = case
+    code = {"gemv": nmm.NMM_PATH_GEMV, "mfma": nmm.NMM_PATH_MFMA, "auto": nmm.NMM_PATH_AUTO}[path]
+    taken = nmm.nmm_gemv_plan(M, K, N, dt, code)["path"]
+    if taken == nmm.NMM_PATH_MFMA:
+        check_mfma_launch(M, K, N, ldx, ldw, dt)
+    else:
+        assert taken == nmm.NMM_PATH_GEMV
+        check_launch(1, M, K, N, ldx, ldw, ldy=N)
 
 
 @pytest.mark.parametrize("nope", [64, 128, 192, 512])
