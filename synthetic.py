@@ -268,3 +268,20 @@ def random_gemv_shapes(seed: int = 31, n: int = 20) -> list[tuple[int, int, int,
         ldw = (N + 7) // 8 * 8 + int(rng.choice([0, 8, 64]))
         out.append((M, K, N, dt, ldx, ldw, str(rng.choice(["gemv", "mfma", "auto"]))))
     return out
+
+
+def random_nt_shapes(seed: int = 37, n: int = 16) -> list[tuple[int, int, int, int, int, int]]:
+    """Seeded (M, K, N, dt, ldx, ldwt) cases for a sweep of the transposed-weight GEMV: M 1-20,
+    K 1-20000 (past the unsplit limit of 16384 now and then), N 1-3000, either 16-bit type, row
+    pitches rounded up to 8 elements plus 0 or 8 more."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        M = int(rng.integers(1, 21))
+        K = int(rng.integers(1, 20001))
+        N = int(rng.integers(1, 3001))
+        dt = int(rng.choice([F16, BF16]))
+        ldx = (K + 7) // 8 * 8 + int(rng.choice([0, 8]))
+        ldwt = (K + 7) // 8 * 8 + int(rng.choice([0, 8]))
+        out.append((M, K, N, dt, ldx, ldwt))
+    return out

@@ -71,6 +71,15 @@ def test_nt_ragged_shapes(M, K, N, dt, ldx, ldwt):
     check_nt(ci, ldwt)
 
 
+@pytest.mark.parametrize("case", syn.random_nt_shapes(), ids=lambda c: f"{c[0]}x{c[1]}x{c[2]}")
+def test_nt_random_shapes_integer_exact(case):
+    # a seeded sweep (the launch-bounds model checks the same cases): small integers, so every
+    # output is exact, with the output rows padded past N to catch stray writes
+    M, K, N, dt, ldx, ldwt = case
+    c = syn.gemv_case(800 + M + K % 83, M, K, N, dt, integer=True, ldx=ldx, name=f"nt_random_{M}x{K}x{N}")
+    check_nt(c, ldwt, ldy=N + 5)
+
+
 def test_nt_agrees_with_the_row_major_path_within_the_bar():
     # the same product from the two layouts: both within the bar of the oracle, and close to each
     # other (the summation orders differ)

@@ -288,6 +288,13 @@ def test_gemv_nt_launch_stays_in_bounds(M, K, N, ldx, ldwt):
                             assert pbase + (mt - 1) * R + wave * r + i < part_floats
 
 
+@pytest.mark.parametrize("case", syn.random_nt_shapes(), ids=lambda c: f"{c[0]}x{c[1]}x{c[2]}")
+def test_random_nt_shapes_stay_in_bounds(case):
+    """The seeded sweep of the transposed-weight GEMV the GPU tests run (synthetic.random_nt_shapes)."""
+    M, K, N, dt, ldx, ldwt = case
+    test_gemv_nt_launch_stays_in_bounds(M, K, N, ldx, ldwt)
+
+
 @pytest.mark.parametrize("heads,nope,rope,kv,ldq", [(128, 128, 64, 512, 576), (6, 40, 24, 136, 160), (4, 16, 8, 24, 40),
                                                     (3, 8, 512, 8, 520), (1, 8, 2, 8, 10), (7, 16, 0, 8, 8)])
 def test_qrope_workgroup_covers_each_pair_once(heads, nope, rope, kv, ldq):
