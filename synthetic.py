@@ -285,3 +285,12 @@ def random_nt_shapes(seed: int = 37, n: int = 16) -> list[tuple[int, int, int, i
         ldwt = (K + 7) // 8 * 8 + int(rng.choice([0, 8]))
         out.append((M, K, N, dt, ldx, ldwt))
     return out
+
+
+def random_batched_shapes(seed: int = 41, n: int = 12) -> list[tuple[int, int, int, int]]:
+    """Seeded (batch, M, K, N) cases for a sweep of the batched GEMV over contiguous [batch, M, K] x
+    [batch, K, N] operands: batch 1-130, M 1-4, K and N multiples of 8 (the row pitch rule) up to
+    1536 and 520."""
+    rng = np.random.default_rng(seed)
+    return [(int(rng.integers(1, 131)), int(rng.integers(1, 5)), 8 * int(rng.integers(1, 193)),
+             8 * int(rng.integers(1, 66))) for _ in range(n)]

@@ -301,6 +301,21 @@ def test_batched_ragged(B, M, K, N):
     assert_parity(y, y_ref, a_ref, what=f"batched {B}x{M}x{K}x{N}")
 
 
+@pytest.mark.parametrize("case", syn.random_batched_shapes(), ids=lambda c: "x".join(map(str, c)))
+def test_batched_random_shapes_integer_exact(case):
+    # a seeded sweep (the launch-bounds model checks the same cases): small integers, so every
+    # output of every batch entry is exact
+    B, M, K, N = case
+    rng = np.random.default_rng(B * 7919 + K + N)
+    x = syn.int_bits(rng, (B, M, K), syn.BF16)
+    W = syn.int_bits(rng, (B, K, N), syn.BF16)
+    y = torch.full((B, M, N), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_batched_gemv(dev16(x, syn.BF16), dev16(W, syn.BF16), y, path=nmm.NMM_PATH_GEMV)
+    torch.cuda.synchronize()
+    y_ref, a_ref = oracle.batched_gemv(x, W, syn.BF16)
+    assert_parity(y, y_ref, a_ref, integer=True, what=f"batched {B}x{M}x{K}x{N}")
+
+
 # ------------------------------------------------------------------ matrix-core path
 
 @pytest.mark.parametrize("M", [1, 2, 3, 4, 5, 8, 16, 17, 32])

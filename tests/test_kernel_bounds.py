@@ -288,6 +288,13 @@ def test_gemv_nt_launch_stays_in_bounds(M, K, N, ldx, ldwt):
                             assert pbase + (mt - 1) * R + wave * r + i < part_floats
 
 
+@pytest.mark.parametrize("case", syn.random_batched_shapes(), ids=lambda c: "x".join(map(str, c)))
+def test_random_batched_shapes_stay_in_bounds(case):
+    """The seeded sweep of the batched GEMV the GPU tests run (synthetic.random_batched_shapes)."""
+    B, M, K, N = case
+    check_launch(B, M, K, N, ldx=K, ldw=N, ldy=N)
+
+
 @pytest.mark.parametrize("case", syn.random_nt_shapes(), ids=lambda c: f"{c[0]}x{c[1]}x{c[2]}")
 def test_random_nt_shapes_stay_in_bounds(case):
     """The seeded sweep of the transposed-weight GEMV the GPU tests run (synthetic.random_nt_shapes)."""
