@@ -23,9 +23,9 @@
 //  * P.V is split by output columns: position group w % 4 accumulates O^T = V^T . P^T for the
 //    16-column tiles w % 4, w % 4 + 4, ... of its heads, V^T fragments read from the staged rows
 //    by ds_read_b64_tr_b16 (gfx950's transposing LDS read).  The accumulators stay in registers.
-//    At 576 / 512, while the grid fits one workgroup per CU, two workgroups share each (head
-//    block, span), each taking half of the column tiles (both compute the scores): twice the
-//    workgroups, each with half the P.V work and half the stores.
+//    At 576 / 512, while the grid fits one workgroup per CU, four or two workgroups share each
+//    (head block, span), each taking its share of the column tiles (all compute the scores):
+//    more workgroups, each with a share of the P.V work and the stores.
 //  * Spans write (reference, sum, unnormalised output) partials; a merge kernel on the same
 //    stream combines them in span order.  The head blocks of one span run on one XCD (workgroup
 //    ids 8 apart), so its L2 reads the span's cache rows from HBM once for all of them.
@@ -106,11 +106,12 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     // the grid is padded and the padding workgroups exit at once
     a.xcd_map = (a.nsp % 8 == 0 || a.nsp > 8) ? 1 : 0;
     a.grid_sp = a.xcd_map ? (a.nsp + 7) / 8 * 8 : a.nsp;
-    // the 576 / 512 shape in 16-head blocks splits d_v over two workgroups per (head block, span)
-    // while the grid still fits one workgroup per CU
-    if (hbh == kAloneHeads && dqk == kMaxCols && dv == 16 * 4 * kMaxNtw &&
-        int64_t(a.n_hb) * 2 * a.grid_sp <= kComputeUnits)
-        a.vsplit = 2;
+    // the 576 / 512 shape in 16-head blocks splits d_v over four or two workgroups per (head
+    // block, span) while the grid still fits one workgroup per CU
+    if (hbh == kAloneHeads && dqk == kMaxCols && dv == 16 * 4 * kMaxNtw) {
+        if (int64_t(a.n_hb) * 4 * a.grid_sp <= kComputeUnits) a.vsplit = 4;
+        else if (int64_t(a.n_hb) * 2 * a.grid_sp <= kComputeUnits) a.vsplit = 2;
+    }
     // partial results live past the workspace's counter block (which GEMV calls sharing the
     // workspace rely on being zero)
     if (a.nsp > 1)
@@ -122,7 +123,9 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
 template <bool EXACT>
 nmm_status launch_attention(const AttnParams& p, int64_t grid, int vsplit, hipStream_t s) {
     const dim3 g(static_cast<uint32_t>(grid));
-    if (vsplit == 2)
+    if (vsplit == 4)
+        hipLaunchKernelGGL((attention_kernel<1, kMaxNtw / 4, true, 4>), g, dim3(kAThreads), 0, s, p);
+    else if (vsplit == 2)
         hipLaunchKernelGGL((attention_kernel<1, kMaxNtw / 2, true, 2>), g, dim3(kAThreads), 0, s, p);
     else if (p.hbh == kAloneHeads)
         hipLaunchKernelGGL((attention_kernel<1, kMaxNtw, EXACT, 1>), g, dim3(kAThreads), 0, s, p);

@@ -182,11 +182,11 @@ __device__ __forceinline__ bool block_of(const AttnParams& p, int bid, int nb, i
 }
 
 // One attention workgroup: HT * 16 heads (head block hb) over one span of positions, with 4 waves.
-// Wave w is position group pw = w and covers all HT head tiles.  With VS = 2 two workgroups share
-// a (head block, span): both compute the scores and probabilities, and each the product with V,
-// its stores and the merge's inputs for half of d_v's column tiles (4 NTW tiles from tile0); the
-// first also stores the reference and sum.  Each output column sees the same operations either
-// way.
+// Wave w is position group pw = w and covers all HT head tiles.  With VS = 2 or 4 that many
+// workgroups share a (head block, span): all compute the scores and probabilities, and each the
+// product with V, its stores and the merge's inputs for 1 / VS of d_v's column tiles (4 NTW tiles
+// from tile0); the first also stores the reference and sum.  Each output column sees the same
+// operations either way.
 //  * Q.K^T: a wave computes the scores of positions 16 pw .. + 15 of each 64-position chunk for its
 //    head tiles (S^T = K . Q^T on the matrix cores, K fragments read from LDS and used for each of
 //    the wave's head tiles; Q held in registers as MFMA fragments).
@@ -222,7 +222,7 @@ __device__ __forceinline__ void attention_block(const AttnParams p, int bid) {
     const int spr = pitch / 8;
     const uint32_t row_bytes = uint32_t(p.ldkv) * 2;
 
-    static_assert(VS == 1 || VS == 2, "one or two column parts");
+    static_assert(VS == 1 || VS == 2 || VS == 4, "one, two or four column parts");
     int hbv, sp;
     if (!block_of(p, bid, p.n_hb * VS, &hbv, &sp)) return;
     const int vh = hbv % VS, hb = hbv / VS;
@@ -627,7 +627,7 @@ struct AttnLaunch {
     int64_t grid = 0;
     int64_t merge_grid = 0;
     int variant = 0;
-    int vsplit = 1;    // workgroups per (head block, span), each taking 1 / vsplit of d_v's columns
+    int vsplit = 1;    // workgroups per (head block, span), each taking 1 / vsplit of d_v's columns (1, 2, 4)
 };
 
 }  // namespace attn

@@ -407,7 +407,8 @@ def test_merge_blocks_cover_every_output_once(heads, dv, nsp, hbh):
 
 
 @pytest.mark.parametrize("n_hb,nsp,vsplit", [(2, 16, 1), (2, 11, 1), (2, 32, 1), (1, 9, 1), (3, 22, 1), (2, 3, 1),
-                                            (1, 1, 1), (2, 64, 1), (8, 16, 2), (8, 8, 2), (5, 21, 2), (1, 3, 2)])
+                                            (1, 1, 1), (2, 64, 1), (8, 16, 2), (8, 8, 2), (5, 21, 2), (1, 3, 2),
+                                            (1, 32, 4), (2, 32, 4), (1, 64, 4), (2, 3, 4)])
 def test_attention_workgroups_cover_every_head_block_and_span_once(n_hb, nsp, vsplit):
     """attention_block's workgroup -> (head block, column part, span) map, with nb = n_hb x vsplit
     (head block hb, column part v at hb vsplit + v): from 8 spans on (xcd_map) the grid holds nsp
