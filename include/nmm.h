@@ -376,8 +376,9 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
                                 void* workspace, size_t workspace_bytes, void* stream);
 
 /* nmm_latent_attention with the partition chosen by the caller: `splits` position spans, each
- * taken by every block of heads (0: the default, min(64 / ceil(heads / 32), ceil(seq / 128))
- * spans: at 4096 positions 16 for 128 heads and 32 for 16 to 64;
+ * taken by every block of heads (0: the default, min(ceil(seq / 128), max(64 / ceil(heads / 32),
+ * ceil(seq / 512))) spans, at most 64: at 4096 positions 16 for 128 heads and 32 for 16 to 64, at
+ * 16384 positions 32 for 128 heads;
  * the span is rounded up to whole 64-position chunks, so fewer spans may result), and an optional
  * bf16 copy of the output (out_bf16 may be NULL).  The launch takes blocks of 16 heads, and at
  * d_qk 576 / d_v 512 four or two workgroups per block and span (each a share of d_v's columns)

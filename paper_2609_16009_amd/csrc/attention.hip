@@ -53,7 +53,8 @@ constexpr int kAloneHeads = 16;
 constexpr int kSharedHeads = 16 * kHt;   // 32
 constexpr int kMaxSpans = 64;             // the merge gives each span one lane of a wave
 constexpr int kDefaultPairs = 64;         // default partition: about this many (32-head block, span) pairs,
-constexpr int kDefaultMinChunks = 2;      // and spans of at least this many chunks (one-chunk spans merge
+constexpr int kDefaultMaxChunks = 8;      // or more spans, so that a span has at most about this many chunks,
+constexpr int kDefaultMinChunks = 2;      // but spans of at least this many chunks (one-chunk spans merge
                                           // more partials than their parallelism saves)
 constexpr int kComputeUnits = 256;        // MI355X; an attention workgroup holds a CU (its LDS)
 
@@ -93,9 +94,10 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     const int64_t wide_blocks = (heads + kSharedHeads - 1) / kSharedHeads;
     const int64_t max_sp = (seq + kCh - 1) / kCh;
     const int64_t few_chunk_spans = (seq + kDefaultMinChunks * kCh - 1) / (kDefaultMinChunks * kCh);
+    const int64_t short_spans = (seq + kDefaultMaxChunks * kCh - 1) / (kDefaultMaxChunks * kCh);
+    const int64_t pair_spans = kDefaultPairs / std::max<int64_t>(1, wide_blocks);
     int64_t nsp = splits > 0 ? splits
-                             : std::max<int64_t>(1, std::min<int64_t>(few_chunk_spans,
-                                                                      kDefaultPairs / std::max<int64_t>(1, wide_blocks)));
+                             : std::max<int64_t>(1, std::min<int64_t>(few_chunk_spans, std::max(pair_spans, short_spans)));
     nsp = std::min(std::min(nsp, max_sp), int64_t(kMaxSpans));
     int64_t span = (seq + nsp - 1) / nsp;
     span = (span + kCh - 1) / kCh * kCh;

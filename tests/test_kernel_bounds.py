@@ -340,7 +340,8 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
     for heads, seq, splits in ((128, 4096, 16), (128, 4096, 0), (70, 300, 3), (1, 64, 1)):
         ws = nmm.nmm_latent_attention_workspace_size(heads, seq, 576, 512)
         n_hb = (heads + 31) // 32
-        span = -(-seq // max(1, min(splits or max(1, min(-(-seq // 128), 64 // n_hb)), -(-seq // 64))))
+        span = -(-seq // max(1, min(splits or max(1, min(-(-seq // 128), max(64 // n_hb, -(-seq // 512)))),
+                                     -(-seq // 64))))
         span = -(-span // 64) * 64
         nsp = -(-seq // span)
         agrid = n_hb * ((nsp + 7) // 8 * 8 if (nsp % 8 == 0 or nsp > 8) else nsp)
@@ -356,14 +357,14 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
 @pytest.mark.parametrize("seq,splits", [(4096, 0), (4096, 16), (4096, 32), (300, 3), (65535, 64), (64, 0)])
 def test_attention_spans_and_workspace_serve_both_head_blocks(heads, seq, splits):
     """The attention launch takes blocks of 16 heads, workgroups beside a GEMV blocks of 32, over the
-    same spans (the default: min(64 / ceil(heads / 32), ceil(seq / 128)) spans).  Each form's span partials,
+    same spans (the default: min(ceil(seq / 128), max(64 / ceil(heads / 32), ceil(seq / 512))) spans).  Each form's span partials,
     [n_hb][nsp][block heads][d_v] floats then [n_hb][nsp][block heads][2], must fit past the counter
     block of the one workspace size the library reports for the call."""
     dv, ticket = 512, 64 * 1024
     L = nmm.lib()
     ws = L.nmm_latent_attention_workspace_size(heads, seq, 576, dv) if splits == 0 else \
         L.nmm_latent_attention_ex_workspace_size(heads, seq, 576, dv, splits)
-    nsp = splits or max(1, min(-(-seq // 128), 64 // -(-heads // 32)))
+    nsp = splits or max(1, min(-(-seq // 128), max(64 // -(-heads // 32), -(-seq // 512))))
     nsp = min(nsp, -(-seq // 64), 64)
     span = -(-(-(-seq // nsp)) // 64) * 64
     nsp = -(-seq // span)
