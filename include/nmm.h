@@ -382,7 +382,9 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
  * the span is rounded up to whole 64-position chunks, so fewer spans may result), and an optional
  * bf16 copy of the output (out_bf16 may be NULL).  The launch takes blocks of 16 heads, and at
  * d_qk 576 / d_v 512 four or two workgroups per block and span (each a share of d_v's columns)
- * while that fits one workgroup per compute unit: 256 workgroups for 128 heads at the default.  On MI355X at
+ * while that fits one workgroup per compute unit: 256 workgroups for 128 heads at the default.
+ * Where even one workgroup per 16-head block and span would exceed 256 (128 heads from 32768
+ * positions on), it takes blocks of 32 heads.  On MI355X at
  * 128 heads x 4096 positions attention alone is fastest with the default 16 spans, and so is the
  * decode step (nmm_mla_decode_step), whose attention workgroups take blocks of 32 heads beside an
  * HBM-bound stream.  The results depend on the spans only, not on the workgroups.  Workspace:

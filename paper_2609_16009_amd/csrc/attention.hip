@@ -78,8 +78,10 @@ struct AttnPlan {
 };
 
 // splits > 0 asks for that many position spans (the span is rounded up to whole chunks, so fewer
-// may result); 0 takes the default.  The spans do not depend on the head block (hbh, 16 or 32),
-// and the workspace is sized for 32-head blocks, which covers both.
+// may result); 0 takes the default.  The spans do not depend on the head block (16 or 32 heads),
+// and the workspace is sized for 32-head blocks, which covers both.  hbh == kAloneHeads asks for
+// 16-head blocks, which the plan widens to 32 heads when their grid would take more than one
+// round of the CUs (every head's arithmetic is the same in either block, so the results are too).
 nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, AttnPlan* out, int64_t splits = 0,
                           int hbh = kAloneHeads) {
     if (heads < 0 || seq < 1 || heads >= (1 << 30) || seq >= (1 << 30)) return NMM_ERR_SHAPE;
@@ -108,9 +110,15 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     // the grid is padded and the padding workgroups exit at once
     a.xcd_map = (a.nsp % 8 == 0 || a.nsp > 8) ? 1 : 0;
     a.grid_sp = a.xcd_map ? (a.nsp + 7) / 8 * 8 : a.nsp;
+    // past one workgroup per CU, 32-head blocks halve the grid (and the K / V chunk reads) rather
+    // than running the 16-head grid in two rounds
+    if (hbh == kAloneHeads && heads > kAloneHeads && int64_t(a.n_hb) * a.grid_sp > kComputeUnits) {
+        a.hbh = kSharedHeads;
+        a.n_hb = static_cast<int>(wide_blocks);
+    }
     // the 576 / 512 shape in 16-head blocks splits d_v over four or two workgroups per (head
     // block, span) while the grid still fits one workgroup per CU
-    if (hbh == kAloneHeads && dqk == kMaxCols && dv == 16 * 4 * kMaxNtw) {
+    if (a.hbh == kAloneHeads && dqk == kMaxCols && dv == 16 * 4 * kMaxNtw) {
         if (int64_t(a.n_hb) * 4 * a.grid_sp <= kComputeUnits) a.vsplit = 4;
         else if (int64_t(a.n_hb) * 2 * a.grid_sp <= kComputeUnits) a.vsplit = 2;
     }

@@ -178,3 +178,27 @@ def test_attention_random_shapes_and_partitions():
         torch.cuda.synchronize()
         ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=576, dv=512)
         assert_parity(out, ref, ref_abs, what=f"case {case}: {heads} heads x {seq} positions, splits {splits}")
+
+
+def test_attention_wide_head_blocks_match_narrow_bit_for_bit():
+    # 128 heads over 64 spans would take 512 workgroups in blocks of 16 heads, so the launch takes
+    # blocks of 32; the same heads in two calls of 64 stay in blocks of 16 (256 workgroups).  A
+    # head's arithmetic does not depend on its block: the two agree bit for bit, and both meet the
+    # oracle; then the default partition at 32,768 positions, which widens the blocks by itself
+    q, kv, scale = syn.attention_case(41, 128, 8192)
+    qd, kvd = dev16(q, syn.BF16), dev16(kv, syn.BF16)
+    wide = torch.full((128, 512), float("nan"), dtype=torch.float32, device="cuda")
+    narrow = torch.full((128, 512), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(qd, kvd, wide, scale, splits=64)
+    for h0 in (0, 64):
+        nmm.nmm_latent_attention_ex(qd[h0:h0 + 64], kvd, narrow[h0:h0 + 64], scale, splits=64)
+    torch.cuda.synchronize()
+    assert torch.equal(wide, narrow)
+    ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=576, dv=512)
+    assert_parity(wide, ref, ref_abs, what="attention 128 heads x 8192 positions, 64 spans")
+    q, kv, scale = syn.attention_case(43, 128, 32768)
+    out = torch.full((128, 512), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(dev16(q, syn.BF16), dev16(kv, syn.BF16), out, scale)
+    torch.cuda.synchronize()
+    ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=576, dv=512)
+    assert_parity(out, ref, ref_abs, what="attention 128 heads x 32768 positions, default partition")

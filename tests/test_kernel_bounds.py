@@ -356,8 +356,8 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
 @pytest.mark.parametrize("heads", [1, 15, 16, 17, 20, 32, 33, 70, 128, 129])
 @pytest.mark.parametrize("seq,splits", [(4096, 0), (4096, 16), (4096, 32), (300, 3), (65535, 64), (64, 0)])
 def test_attention_spans_and_workspace_serve_both_head_blocks(heads, seq, splits):
-    """The attention launch takes blocks of 16 heads, workgroups beside a GEMV blocks of 32, over the
-    same spans (the default: min(ceil(seq / 128), max(64 / ceil(heads / 32), ceil(seq / 512))) spans).  Each form's span partials,
+    """The attention launch takes blocks of 16 heads (32 where 16 would take over 256 workgroups),
+    workgroups beside a GEMV blocks of 32, over the same spans (the default: min(ceil(seq / 128), max(64 / ceil(heads / 32), ceil(seq / 512))) spans).  Each form's span partials,
     [n_hb][nsp][block heads][d_v] floats then [n_hb][nsp][block heads][2], must fit past the counter
     block of the one workspace size the library reports for the call."""
     dv, ticket = 512, 64 * 1024
