@@ -54,6 +54,7 @@ constexpr int kSharedHeads = 16 * kHt;   // 32
 constexpr int kMaxSpans = 64;             // the merge gives each span one lane of a wave
 constexpr int kDefaultPairs = 64;         // default partition: about this many (32-head block, span) pairs,
 constexpr int kDefaultMaxChunks = 8;      // or more spans, so that a span has at most about this many chunks,
+constexpr int kDefaultFitChunks = 4;      // or this many while one workgroup per 16-head block and span fits the CUs,
 constexpr int kDefaultMinChunks = 2;      // but spans of at least this many chunks (one-chunk spans merge
                                           // more partials than their parallelism saves)
 constexpr int kComputeUnits = 256;        // MI355X; an attention workgroup holds a CU (its LDS)
@@ -97,9 +98,14 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     const int64_t max_sp = (seq + kCh - 1) / kCh;
     const int64_t few_chunk_spans = (seq + kDefaultMinChunks * kCh - 1) / (kDefaultMinChunks * kCh);
     const int64_t short_spans = (seq + kDefaultMaxChunks * kCh - 1) / (kDefaultMaxChunks * kCh);
+    const int64_t shorter_spans = (seq + kDefaultFitChunks * kCh - 1) / (kDefaultFitChunks * kCh);
     const int64_t pair_spans = kDefaultPairs / std::max<int64_t>(1, wide_blocks);
-    int64_t nsp = splits > 0 ? splits
-                             : std::max<int64_t>(1, std::min<int64_t>(few_chunk_spans, std::max(pair_spans, short_spans)));
+    // spans that a grid of 16-head blocks holds at one workgroup per CU (a multiple of 8 from 8 on,
+    // so the XCD-grouped grid needs no padding)
+    int64_t fit_spans = kComputeUnits / std::max<int64_t>(1, (heads + kAloneHeads - 1) / kAloneHeads);
+    if (fit_spans >= 8) fit_spans = fit_spans / 8 * 8;
+    const int64_t want = std::max(std::max(pair_spans, short_spans), std::min(shorter_spans, fit_spans));
+    int64_t nsp = splits > 0 ? splits : std::max<int64_t>(1, std::min(few_chunk_spans, want));
     nsp = std::min(std::min(nsp, max_sp), int64_t(kMaxSpans));
     int64_t span = (seq + nsp - 1) / nsp;
     span = (span + kCh - 1) / kCh * kCh;

@@ -326,6 +326,16 @@ def test_qrope_workgroup_covers_each_pair_once(heads, nope, rope, kv, ldq):
     assert np.all(seen == 1)
 
 
+def default_spans(heads, seq):
+    """The default partition before the span is rounded to whole chunks: about 64 (32-head block,
+    span) pairs, or spans of at most 8 chunks, or of at most 4 while a grid of 16-head blocks
+    still holds them at 256 workgroups (a multiple of 8 from 8 on), but spans of at least 2 chunks."""
+    fit = 256 // -(-heads // 16) if heads else 256
+    fit = fit // 8 * 8 if fit >= 8 else fit
+    want = max(64 // max(1, -(-heads // 32)), -(-seq // 512), min(-(-seq // 256), fit))
+    return max(1, min(-(-seq // 128), want))
+
+
 @pytest.mark.parametrize("K,N", [(16384, 7168), (144, 1032), (2048, 512)])
 def test_gemv_attention_launch_shares_lds_and_grid(K, N):
     """gemv_attention_kernel: workgroups [0, gemv_grid) run the GEMV exactly as its own launch
@@ -340,7 +350,7 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
     for heads, seq, splits in ((128, 4096, 16), (128, 4096, 0), (70, 300, 3), (1, 64, 1)):
         ws = nmm.nmm_latent_attention_workspace_size(heads, seq, 576, 512)
         n_hb = (heads + 31) // 32
-        span = -(-seq // max(1, min(splits or max(1, min(-(-seq // 128), max(64 // n_hb, -(-seq // 512)))),
+        span = -(-seq // max(1, min(splits or default_spans(heads, seq),
                                      -(-seq // 64))))
         span = -(-span // 64) * 64
         nsp = -(-seq // span)
@@ -354,17 +364,18 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
 
 
 @pytest.mark.parametrize("heads", [1, 15, 16, 17, 20, 32, 33, 70, 128, 129])
-@pytest.mark.parametrize("seq,splits", [(4096, 0), (4096, 16), (4096, 32), (300, 3), (65535, 64), (64, 0)])
+@pytest.mark.parametrize("seq,splits", [(4096, 0), (4096, 16), (4096, 32), (300, 3), (65535, 64), (64, 0),
+                                         (8192, 0), (16384, 0), (32768, 0), (1000, 0)])
 def test_attention_spans_and_workspace_serve_both_head_blocks(heads, seq, splits):
     """The attention launch takes blocks of 16 heads (32 where 16 would take over 256 workgroups),
-    workgroups beside a GEMV blocks of 32, over the same spans (the default: min(ceil(seq / 128), max(64 / ceil(heads / 32), ceil(seq / 512))) spans).  Each form's span partials,
+    workgroups beside a GEMV blocks of 32, over the same spans (default_spans).  Each form's span partials,
     [n_hb][nsp][block heads][d_v] floats then [n_hb][nsp][block heads][2], must fit past the counter
     block of the one workspace size the library reports for the call."""
     dv, ticket = 512, 64 * 1024
     L = nmm.lib()
     ws = L.nmm_latent_attention_workspace_size(heads, seq, 576, dv) if splits == 0 else \
         L.nmm_latent_attention_ex_workspace_size(heads, seq, 576, dv, splits)
-    nsp = splits or max(1, min(-(-seq // 128), max(64 // -(-heads // 32), -(-seq // 512))))
+    nsp = splits or default_spans(heads, seq)
     nsp = min(nsp, -(-seq // 64), 64)
     span = -(-(-(-seq // nsp)) // 64) * 64
     nsp = -(-seq // span)
