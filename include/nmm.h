@@ -377,7 +377,7 @@ nmm_status nmm_latent_attention(int64_t heads, int64_t seq, int64_t d_qk, int64_
 
 /* nmm_latent_attention with the partition chosen by the caller: `splits` position spans, each
  * taken by every block of heads (0: the default, min(ceil(seq / 128), max(64 / ceil(heads / 32),
- * ceil(seq / 512), min(ceil(seq / 256), F))) spans with F = 256 / ceil(heads / 16), a multiple of 8
+ * ceil(seq / 512), min(floor(ceil(seq / 64) / 4), F))) spans with F = 256 / ceil(heads / 16), a multiple of 8
  * from 8 on, at most 64: at 4096 positions 16 for 128 heads and 32 for 16 to 64, at 8192
  * positions 32 for 128 heads, at 16384 32 for 128 heads and 64 for 16 to 64, from 32768 on 64;
  * the span is rounded up to whole 64-position chunks, so fewer spans may result), and an optional

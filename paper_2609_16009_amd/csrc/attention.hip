@@ -98,7 +98,8 @@ nmm_status plan_attention(int64_t heads, int64_t seq, int64_t dqk, int64_t dv, A
     const int64_t max_sp = (seq + kCh - 1) / kCh;
     const int64_t few_chunk_spans = (seq + kDefaultMinChunks * kCh - 1) / (kDefaultMinChunks * kCh);
     const int64_t short_spans = (seq + kDefaultMaxChunks * kCh - 1) / (kDefaultMaxChunks * kCh);
-    const int64_t shorter_spans = (seq + kDefaultFitChunks * kCh - 1) / (kDefaultFitChunks * kCh);
+    // rounded down, so that a ragged tail (4097 positions) keeps spans of more than four chunks
+    const int64_t shorter_spans = std::max<int64_t>(1, max_sp / kDefaultFitChunks);
     const int64_t pair_spans = kDefaultPairs / std::max<int64_t>(1, wide_blocks);
     // spans that a grid of 16-head blocks holds at one workgroup per CU (a multiple of 8 from 8 on,
     // so the XCD-grouped grid needs no padding)

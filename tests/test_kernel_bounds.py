@@ -328,11 +328,11 @@ def test_qrope_workgroup_covers_each_pair_once(heads, nope, rope, kv, ldq):
 
 def default_spans(heads, seq):
     """The default partition before the span is rounded to whole chunks: about 64 (32-head block,
-    span) pairs, or spans of at most 8 chunks, or of at most 4 while a grid of 16-head blocks
+    span) pairs, or spans of at most 8 chunks, or of about 4 (chunks // 4 spans) while a grid of 16-head blocks
     still holds them at 256 workgroups (a multiple of 8 from 8 on), but spans of at least 2 chunks."""
     fit = 256 // -(-heads // 16) if heads else 256
     fit = fit // 8 * 8 if fit >= 8 else fit
-    want = max(64 // max(1, -(-heads // 32)), -(-seq // 512), min(-(-seq // 256), fit))
+    want = max(64 // max(1, -(-heads // 32)), -(-seq // 512), min(max(1, -(-seq // 64) // 4), fit))
     return max(1, min(-(-seq // 128), want))
 
 
@@ -365,7 +365,7 @@ def test_gemv_attention_launch_shares_lds_and_grid(K, N):
 
 @pytest.mark.parametrize("heads", [1, 15, 16, 17, 20, 32, 33, 70, 128, 129])
 @pytest.mark.parametrize("seq,splits", [(4096, 0), (4096, 16), (4096, 32), (300, 3), (65535, 64), (64, 0),
-                                         (8192, 0), (16384, 0), (32768, 0), (1000, 0)])
+                                         (8192, 0), (16384, 0), (32768, 0), (1000, 0), (4097, 0), (8300, 0)])
 def test_attention_spans_and_workspace_serve_both_head_blocks(heads, seq, splits):
     """The attention launch takes blocks of 16 heads (32 where 16 would take over 256 workgroups),
     workgroups beside a GEMV blocks of 32, over the same spans (default_spans).  Each form's span partials,
