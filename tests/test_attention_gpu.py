@@ -202,3 +202,21 @@ def test_attention_wide_head_blocks_match_narrow_bit_for_bit():
     torch.cuda.synchronize()
     ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=576, dv=512)
     assert_parity(out, ref, ref_abs, what="attention 128 heads x 32768 positions, default partition")
+
+
+def test_attention_wide_head_blocks_general_shape():
+    # the general (not 576 / 512) kernel in blocks of 32 heads: 160 heads over 32 spans would take
+    # 320 workgroups in blocks of 16; the same heads in two calls of 80 stay in blocks of 16 (160
+    # workgroups).  Bit for bit alike, and against the oracle (ragged dims, padded cache rows)
+    heads, seq, dqk, dv, ldkv = 160, 2000, 96, 48, 104
+    q, kv, scale = syn.attention_case(47, heads, seq, dqk=dqk, dv=dv, ldkv=ldkv)
+    qd, kvd = dev16(q, syn.BF16), dev16(kv, syn.BF16)
+    wide = torch.full((heads, dv), float("nan"), dtype=torch.float32, device="cuda")
+    narrow = torch.full((heads, dv), float("nan"), dtype=torch.float32, device="cuda")
+    nmm.nmm_latent_attention_ex(qd, kvd, wide, scale, splits=40, d_v=dv)
+    for h0 in (0, 80):
+        nmm.nmm_latent_attention_ex(qd[h0:h0 + 80], kvd, narrow[h0:h0 + 80], scale, splits=40, d_v=dv)
+    torch.cuda.synchronize()
+    assert torch.equal(wide, narrow)
+    ref, ref_abs = oracle.latent_attention(q, kv, scale, dqk=dqk, dv=dv)
+    assert_parity(wide, ref, ref_abs, what=f"attention {heads}x{seq}x{dqk}/{dv}, 32 spans in 32-head blocks")
